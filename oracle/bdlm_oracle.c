@@ -1,0 +1,292 @@
+/*
+ * bdlm_oracle.c -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, fp64 CPU reference for the block-restricted bidirectional
+ * Mamba scan of BDLM Mamba-H ("Training Hybrid Block Diffusion Language Models
+ * with Partial Bidirectionality").  Only the test suite, the smoke check and
+ * the benchmark's CPU-baseline leg may load this library.  It shares no
+ * source, header, table or helper with the HIP library; the product path never
+ * calls it.
+ *
+ * What is computed, and where the paper defines it:
+ *   - selective state-space update  s_i = A_i s_{i-1} + B_i x_i,
+ *     y_i = C_i s_i + D x_i                        (Sec. 3, Eq. mamba-scan-background)
+ *     read in the Mamba-2 form the paper's mixers use (App. C): per head a
+ *     scalar A_h, token decay a_t = exp(dt_t * A_h), input B_t scaled by dt_t.
+ *   - forward boundary state s_k = F_fwd(clean prefix)   (Sec. 4, Eq. boundary-state)
+ *   - active block: forward scan continued from s_k, reverse scan of the
+ *     reversed block from a zero state, outputs summed    (Sec. 4, Eq. partial-reverse)
+ *   - block finalisation appends the clean block's forward state to the
+ *     cache                                               (Sec. 3 BDLM cache; Sec. 4.1)
+ *   - full-window bidirectional scan (DiffuMamba-style contrast: forward and
+ *     reverse over the whole window, both from zero)      (Sec. 4, Sec. 5.1)
+ *
+ * Every function takes the same stored bytes the GPU reads (fp32 or bf16
+ * activations, fp32 per-head A / D / D_rev) and decodes them exactly to
+ * double.  States are double.  Loops follow the recurrence token by token;
+ * no blocking, no fusion.  The (batch, head) loop may run on several OpenMP
+ * threads: each (batch, head) pair is independent, so the result does not
+ * depend on the thread count.
+ *
+ * Layouts (row-major, contiguous):
+ *   x    [batch][len][nheads][headdim]      dt [batch][len][nheads]
+ *   Bm,Cm[batch][len][ngroups][dstate]      A, D, D_rev [nheads] fp32
+ *   h    [nslots][nheads][headdim][dstate]  double
+ *   y    [batch][len][nheads][headdim]      double
+ * Head h reads group g = h / (nheads / ngroups).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define OR_DTYPE_F32 0
+#define OR_DTYPE_BF16 1
+
+#define OR_OK 0
+#define OR_ERR_ARG (-1)
+#define OR_ERR_OFFSET (-2)
+#define OR_ERR_SLOT (-3)
+
+typedef struct {
+    int64_t batch, nheads, headdim, dstate, ngroups, len;
+    int32_t in_dtype;
+} or_shape;
+
+/* Exact decode of one stored activation to double. */
+static double rd(const void *base, int64_t i, int dtype)
+{
+    if (dtype == OR_DTYPE_BF16) {
+        uint32_t bits = (uint32_t)((const uint16_t *)base)[i] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+    return (double)((const float *)base)[i];
+}
+
+static int shape_ok(const or_shape *s)
+{
+    if (s->batch < 0 || s->len < 0) return 0;
+    if (s->nheads <= 0 || s->headdim <= 0 || s->dstate <= 0 || s->ngroups <= 0) return 0;
+    if (s->nheads % s->ngroups) return 0;
+    if (s->in_dtype != OR_DTYPE_F32 && s->in_dtype != OR_DTYPE_BF16) return 0;
+    return 1;
+}
+
+/* Index helpers for the layouts above. */
+static int64_t ix_x(const or_shape *s, int64_t b, int64_t t, int64_t h, int64_t p)
+{
+    return ((b * s->len + t) * s->nheads + h) * s->headdim + p;
+}
+static int64_t ix_dt(const or_shape *s, int64_t b, int64_t t, int64_t h)
+{
+    return (b * s->len + t) * s->nheads + h;
+}
+static int64_t ix_bc(const or_shape *s, int64_t b, int64_t t, int64_t g, int64_t n)
+{
+    return ((b * s->len + t) * s->ngroups + g) * s->dstate + n;
+}
+
+/*
+ * One token of the selective update on a headdim x dstate state S, then the
+ * readout.  S <- a S + dt * x (outer) B ;  out[p] = sum_n S[p][n] C[n] + skip * x[p].
+ * Used for both scan directions: the reverse direction feeds tokens in
+ * reversed order and each token keeps its own (x, dt, B, C), which is what
+ * rev(F(rev(block))) means.
+ */
+static void token_update(const or_shape *s, double *S, int64_t b, int64_t t, int64_t h,
+                         int64_t g, const void *x, const void *dt, double A_h,
+                         const void *Bm, const void *Cm, double skip, double *out)
+{
+    const int64_t P = s->headdim, N = s->dstate;
+    const int dty = s->in_dtype;
+    const double dtv = rd(dt, ix_dt(s, b, t, h), dty);
+    const double a = exp(dtv * A_h);
+    for (int64_t p = 0; p < P; ++p) {
+        const double xv = rd(x, ix_x(s, b, t, h, p), dty);
+        double acc = 0.0;
+        for (int64_t n = 0; n < N; ++n) {
+            const double bv = rd(Bm, ix_bc(s, b, t, g, n), dty);
+            S[p * N + n] = a * S[p * N + n] + dtv * xv * bv;
+            acc += S[p * N + n] * rd(Cm, ix_bc(s, b, t, g, n), dty);
+        }
+        if (out) out[p] = acc + skip * xv;
+    }
+}
+
+/*
+ * Active-block step (Eq. partial-reverse), all (batch, head) pairs.
+ *   y_fwd = F_fwd(block; s_k)     forward scan from the cached state of the
+ *                                  batch row's slot (slot_idx[b], or b)
+ *   y_rev = rev(F_rev(rev(block))) reverse scan from zero, block-local
+ *   y     = y_fwd + y_rev
+ * The cache is read only.  y_fwd / y_rev may be NULL.  If h_out is non-NULL
+ * it receives the forward state after the last block token for every batch
+ * row, laid out [batch][nheads][headdim][dstate] (what a commit would store).
+ */
+int bdlm_oracle_block_step(const or_shape *s, const void *x, const void *dt, const float *A,
+                           const void *Bm, const void *Cm, const float *D, const float *D_rev,
+                           const double *h_pool, int64_t nslots, const int32_t *slot_idx,
+                           double *y, double *y_fwd, double *y_rev, double *h_out)
+{
+    if (!s || !shape_ok(s) || !x || !dt || !A || !Bm || !Cm || !D || !D_rev || !h_pool || !y)
+        return OR_ERR_ARG;
+    const int64_t Bt = s->batch, L = s->len, H = s->nheads, P = s->headdim, N = s->dstate;
+    const int64_t hpg = H / s->ngroups;
+    for (int64_t b = 0; b < Bt; ++b) {
+        const int64_t slot = slot_idx ? slot_idx[b] : b;
+        if (slot < 0 || slot >= nslots) return OR_ERR_SLOT;
+    }
+    int err = OR_OK;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t b = 0; b < Bt; ++b) {
+        for (int64_t h = 0; h < H; ++h) {
+            const int64_t slot = slot_idx ? slot_idx[b] : b;
+            const int64_t g = h / hpg;
+            double *S = (double *)malloc(sizeof(double) * P * N);
+            double *R = (double *)malloc(sizeof(double) * P * N);
+            double *yf = (double *)malloc(sizeof(double) * L * P);
+            double *yr = (double *)malloc(sizeof(double) * L * P);
+            if (!S || !R || !yf || !yr) {
+#pragma omp atomic write
+                err = OR_ERR_ARG;
+                free(S); free(R); free(yf); free(yr);
+                continue;
+            }
+            /* forward: continue from the cached boundary state */
+            memcpy(S, h_pool + (slot * H + h) * P * N, sizeof(double) * P * N);
+            for (int64_t t = 0; t < L; ++t)
+                token_update(s, S, b, t, h, g, x, dt, (double)A[h], Bm, Cm, (double)D[h],
+                             yf + t * P);
+            /* reverse: the flipped block from a zero state (nothing outside the block) */
+            memset(R, 0, sizeof(double) * P * N);
+            for (int64_t t = L - 1; t >= 0; --t)
+                token_update(s, R, b, t, h, g, x, dt, (double)A[h], Bm, Cm, (double)D_rev[h],
+                             yr + t * P);
+            for (int64_t t = 0; t < L; ++t)
+                for (int64_t p = 0; p < P; ++p) {
+                    const int64_t o = ix_x(s, b, t, h, p);
+                    y[o] = yf[t * P + p] + yr[t * P + p];
+                    if (y_fwd) y_fwd[o] = yf[t * P + p];
+                    if (y_rev) y_rev[o] = yr[t * P + p];
+                }
+            if (h_out) memcpy(h_out + (b * H + h) * P * N, S, sizeof(double) * P * N);
+            free(S); free(R); free(yf); free(yr);
+        }
+    }
+    return err;
+}
+
+/*
+ * Block finalisation: the clean block's forward scan from the cached state
+ * replaces that state (the cache now summarises prefix ++ block), and the
+ * slot's bookkeeping advances by one block of len tokens.  If y_clean is
+ * non-NULL it receives the layer output on the clean block, computed as the
+ * active-block step above from the state before the update.
+ * Every row's slot must hold exactly expected_block_index committed blocks
+ * (a negative value skips that check) and no slot may appear twice; on any
+ * violation nothing is modified.
+ */
+int bdlm_oracle_commit(const or_shape *s, const void *x, const void *dt, const float *A,
+                       const void *Bm, const void *Cm, const float *D, const float *D_rev,
+                       double *h_pool, int64_t nslots, const int32_t *slot_idx,
+                       int64_t *n_committed, int64_t *n_blocks, int64_t expected_block_index,
+                       double *y_clean)
+{
+    if (!s || !shape_ok(s) || !h_pool || !n_committed || !n_blocks) return OR_ERR_ARG;
+    const int64_t Bt = s->batch, H = s->nheads, P = s->headdim, N = s->dstate;
+    for (int64_t b = 0; b < Bt; ++b) {
+        const int64_t slot = slot_idx ? slot_idx[b] : b;
+        if (slot < 0 || slot >= nslots) return OR_ERR_SLOT;
+        for (int64_t c = 0; c < b; ++c)
+            if ((slot_idx ? slot_idx[c] : c) == slot) return OR_ERR_SLOT;
+        if (expected_block_index >= 0 && n_blocks[slot] != expected_block_index)
+            return OR_ERR_OFFSET;
+    }
+    double *hn = (double *)malloc(sizeof(double) * (Bt > 0 ? Bt : 1) * H * P * N);
+    double *yc = (double *)malloc(sizeof(double) * (Bt > 0 ? Bt : 1) * s->len * H * P + 8);
+    if (!hn || !yc) { free(hn); free(yc); return OR_ERR_ARG; }
+    int rc = bdlm_oracle_block_step(s, x, dt, A, Bm, Cm, D, D_rev, h_pool, nslots, slot_idx,
+                                    yc, NULL, NULL, hn);
+    if (rc == OR_OK) {
+        for (int64_t b = 0; b < Bt; ++b) {
+            const int64_t slot = slot_idx ? slot_idx[b] : b;
+            memcpy(h_pool + slot * H * P * N, hn + b * H * P * N, sizeof(double) * H * P * N);
+            n_committed[slot] += s->len;
+            n_blocks[slot] += 1;
+        }
+        if (y_clean) memcpy(y_clean, yc, sizeof(double) * Bt * s->len * H * P);
+    }
+    free(hn);
+    free(yc);
+    return rc;
+}
+
+/*
+ * Forward-only scan over a sequence of len tokens, continuing each batch
+ * row's state h[b] in place ([batch][nheads][headdim][dstate]).  This is how
+ * a clean prefix is summarised into its boundary state (Eq. boundary-state).
+ * If y is non-NULL it receives the forward outputs (skip term D included).
+ */
+int bdlm_oracle_scan_forward(const or_shape *s, const void *x, const void *dt, const float *A,
+                             const void *Bm, const void *Cm, const float *D, double *h,
+                             double *y)
+{
+    if (!s || !shape_ok(s) || !x || !dt || !A || !Bm || !Cm || !D || !h) return OR_ERR_ARG;
+    const int64_t Bt = s->batch, L = s->len, H = s->nheads, P = s->headdim, N = s->dstate;
+    const int64_t hpg = H / s->ngroups;
+    int err = OR_OK;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t b = 0; b < Bt; ++b) {
+        for (int64_t hh = 0; hh < H; ++hh) {
+            double *out = (double *)malloc(sizeof(double) * P);
+            if (!out) {
+#pragma omp atomic write
+                err = OR_ERR_ARG;
+                continue;
+            }
+            double *S = h + (b * H + hh) * P * N;
+            for (int64_t t = 0; t < L; ++t) {
+                token_update(s, S, b, t, hh, hh / hpg, x, dt, (double)A[hh], Bm, Cm,
+                             (double)D[hh], out);
+                if (y)
+                    for (int64_t p = 0; p < P; ++p) y[ix_x(s, b, t, hh, p)] = out[p];
+            }
+            free(out);
+        }
+    }
+    return err;
+}
+
+/*
+ * Full-window bidirectional scan (the DiffuMamba-style contrast): forward
+ * over all len tokens from zero plus reverse over all len tokens from zero,
+ * summed.  Identical to bdlm_oracle_block_step with a zero cache and the whole
+ * window as one block; kept as its own entry so tests can state that.
+ */
+int bdlm_oracle_full_window(const or_shape *s, const void *x, const void *dt, const float *A,
+                            const void *Bm, const void *Cm, const float *D, const float *D_rev,
+                            double *y)
+{
+    if (!s || !shape_ok(s)) return OR_ERR_ARG;
+    const int64_t Bt = s->batch, H = s->nheads, P = s->headdim, N = s->dstate;
+    double *zero = (double *)calloc((size_t)((Bt > 0 ? Bt : 1) * H * P * N), sizeof(double));
+    if (!zero) return OR_ERR_ARG;
+    int rc = bdlm_oracle_block_step(s, x, dt, A, Bm, Cm, D, D_rev, zero, Bt > 0 ? Bt : 1, NULL,
+                                    y, NULL, NULL, NULL);
+    free(zero);
+    return rc;
+}
+
+int bdlm_oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
