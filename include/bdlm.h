@@ -1,0 +1,209 @@
+/*
+ * bdlm.h -- C ABI of libbdlm: the block-restricted bidirectional Mamba scan of
+ * BDLM Mamba-H on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Training Hybrid Block Diffusion Language Models with Partial
+ * Bidirectionality".  Per Mamba layer, the BDLM sampler keeps one forward
+ * boundary state per sequence (Sec. 4, Eq. boundary-state).  Every denoising
+ * step of the active block continues that state forward through the block,
+ * runs a reverse scan of the block from a zero state, and sums the two outputs
+ * (Sec. 4, Eq. partial-reverse).  Once the block is final, the clean block's
+ * forward state replaces the cached one (the cache-append step of the BDLM
+ * sampler, Sec. 3; Sec. 4.1).
+ *
+ * Recurrence (Sec. 3, Eq. mamba-scan-background, in the Mamba-2 form the
+ * paper's mixers use, App. C).  For batch row b, head h, group g = h / (H/G):
+ *     a_t = exp(dt[b,t,h] * A[h])
+ *     S_t = a_t S_{t-1} + dt[b,t,h] * x[b,t,h,:] (outer) B[b,t,g,:]      (P x N)
+ *     out_t = S_t C[b,t,g,:] + skip * x[b,t,h,:]
+ * Forward branch: S_{-1} = cached state, skip = D[h].
+ * Reverse branch: tokens in reversed order (each keeps its own x, dt, B, C),
+ * S = 0 before the last token, skip = D_rev[h].   y = forward + reverse.
+ *
+ * Conventions shared by every entry point:
+ *   - Device pointers point to device memory the caller allocated and owns.
+ *     The library never allocates, frees or synchronises, and keeps no pointer
+ *     after returning.  Work is enqueued on `stream` (a hipStream_t; NULL is the
+ *     null stream) and runs asynchronously.
+ *   - Host pointers (slot_idx, n_committed, n_blocks) are read, and for a commit
+ *     updated, before the call returns.
+ *   - Every check happens on the host before anything is enqueued; on any
+ *     error nothing is enqueued and nothing is modified.  The return value is
+ *     BDLM_OK or a negative BDLM_E_* code.  No entry point aborts.
+ *   - Sizes: headdim P == 64; dstate N in {16, 32, 64, 128}; block_len L in
+ *     [0, 64]; nheads % ngroups == 0; batch >= 0.
+ *   - Activation storage (x, dt, B, C) is fp32 or bf16 (desc.in_dtype).  All
+ *     arithmetic, states and outputs are fp32.
+ */
+#ifndef BDLM_H
+#define BDLM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BDLM_ABI_VERSION 1
+#define BDLM_HEADDIM 64
+#define BDLM_MAX_BLOCK_LEN 64
+/* Largest batch for which an explicit slot_idx may be given (it is passed to
+   the kernels by value). */
+#define BDLM_MAX_SLOT_ROWS 256
+
+enum bdlm_status {
+    BDLM_OK = 0,
+    BDLM_E_NULL = -1,    /* a required pointer is NULL */
+    BDLM_E_SHAPE = -2,   /* a size is unsupported or inconsistent */
+    BDLM_E_DTYPE = -3,   /* unknown in_dtype, or reserved field not zero */
+    BDLM_E_ALIGN = -4,   /* a pointer or stride breaks the alignment contract */
+    BDLM_E_OFFSET = -5,  /* commit: a slot does not hold expected_block_index blocks */
+    BDLM_E_SLOT = -6,    /* slot index out of range, or repeated within one commit */
+    BDLM_E_LAUNCH = -7   /* the HIP runtime refused the launch */
+};
+
+enum bdlm_dtype { BDLM_DTYPE_F32 = 0, BDLM_DTYPE_BF16 = 1 };
+
+/*
+ * Shape and activation layout of one call.  Strides are in elements.
+ *   x  [batch][block_len][nheads][headdim]: x_stride = {batch, token, head};
+ *      headdim is unit stride.
+ *   dt [batch][block_len][nheads]: dt_stride = {batch, token}; heads unit stride.
+ *   B, C [batch][block_len][ngroups][dstate]: bc_stride = {batch, token, group};
+ *      dstate unit stride; B and C share strides.
+ * Strides may describe views into a larger projection output (e.g. slices of a
+ * Mamba-2 in_proj result).  bdlm_desc_init fills contiguous strides.
+ */
+typedef struct bdlm_desc {
+    int64_t batch;
+    int64_t nheads;
+    int64_t headdim;
+    int64_t dstate;
+    int64_t ngroups;
+    int64_t block_len;
+    int32_t in_dtype;   /* enum bdlm_dtype */
+    int32_t reserved;   /* must be 0 */
+    int64_t x_stride[3];
+    int64_t dt_stride[2];
+    int64_t bc_stride[3];
+} bdlm_desc_t;
+
+/* Version of this ABI (BDLM_ABI_VERSION). */
+int bdlm_abi_version(void);
+
+/* Static, NUL-terminated description of a status code; never NULL. */
+const char *bdlm_strerror(int status);
+
+/* Fill *desc for contiguous activations.  Returns BDLM_E_NULL if desc is NULL,
+   else BDLM_OK (sizes are checked by the entry points, not here). */
+int bdlm_desc_init(bdlm_desc_t *desc, int64_t batch, int64_t nheads, int64_t headdim,
+                   int64_t dstate, int64_t ngroups, int64_t block_len, int32_t in_dtype);
+
+/*
+ * Active-block denoising step (Sec. 4, Eq. partial-reverse).
+ *
+ *   y[b,t,h,:] = forward branch from the state h_pool[slot(b), h]
+ *              + reverse branch of the block from zero
+ *
+ * x, dt, B, C  device, layout per desc, in_dtype storage.  Only the L block
+ *              tokens are passed, so the reverse branch cannot see anything
+ *              outside the block and the prefix enters only through h_pool.
+ * A, D, D_rev  device fp32 [nheads].  A[h] < 0 keeps every decay below 1.
+ * h_pool       device fp32 state pool, nslots x nheads states of 64 x dstate,
+ *              16-byte aligned, in the pool layout (see bdlm_state_pack).  Read
+ *              only (the cache is never written by a step).
+ * slot_idx     host int32 [batch] mapping batch row -> cache slot, or NULL for
+ *              slot(b) = b.  Non-NULL requires batch <= BDLM_MAX_SLOT_ROWS.
+ *              Rows may share a slot.
+ * y            device fp32 [batch][block_len][nheads][64], contiguous, 16-byte
+ *              aligned.  Fully overwritten.  Must not overlap any input.
+ * Alignment: x, B and C base pointers 16-byte aligned, and every x_stride and
+ * bc_stride entry a multiple of 16 bytes (8 bf16 or 4 fp32 elements); dt, A, D,
+ * D_rev and y aligned to their element size.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE, BDLM_E_ALIGN, BDLM_E_SLOT,
+ * BDLM_E_LAUNCH.  batch == 0 or block_len == 0 enqueues nothing; x, dt, B, C and
+ * y may then be NULL.
+ */
+int bdlm_scan_block_step(const bdlm_desc_t *desc, const void *x, const void *dt,
+                         const float *A, const void *B, const void *C, const float *D,
+                         const float *D_rev, const float *h_pool, int64_t nslots,
+                         const int32_t *slot_idx, float *y, void *stream);
+
+/*
+ * Block finalisation: commit the clean block's forward boundary state
+ * (Sec. 4, Eq. boundary-state; cache append of Sec. 3 and Sec. 4.1).
+ *
+ *   h_pool[slot(b), h] <- forward state after the L clean tokens, continued
+ *                          from h_pool[slot(b), h]
+ *   n_committed[slot(b)] += L;  n_blocks[slot(b)] += 1
+ *
+ * Inputs as for bdlm_scan_block_step, but h_pool is updated in place and the
+ * rows' slots must be distinct.
+ * n_committed, n_blocks  host int64 [nslots]: tokens and blocks committed per
+ *              slot.  Every row's slot must satisfy n_blocks[slot] ==
+ *              expected_block_index (pass a negative value to skip the check).
+ *              Updated only after the launch has been enqueued successfully.
+ * y_clean      device fp32 [batch][block_len][nheads][64] (16-byte aligned) or NULL.  If given, it
+ *              receives the layer output on the clean block, computed exactly as
+ *              bdlm_scan_block_step would from the state before the update.
+ * Errors: as bdlm_scan_block_step, plus BDLM_E_OFFSET, and BDLM_E_SLOT for a
+ * repeated slot.  block_len == 0 leaves states unchanged but still counts a
+ * block.
+ */
+int bdlm_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
+                         const float *A, const void *B, const void *C, const float *D,
+                         const float *D_rev, float *h_pool, int64_t nslots,
+                         const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
+                         int64_t expected_block_index, float *y_clean, void *stream);
+
+/*
+ * State pool layout.  The state of one (slot, head) is the 64 x dstate matrix
+ * s[p][n] of the recurrence.  In a pool, state k = slot * nheads + head starts
+ * at float offset k * 64 * dstate and stores s[p][n] at
+ *     ((n / 4) * 64 + p) * 4 + n % 4,
+ * i.e. dstate/4 blocks of [64][4]: groups of four consecutive state columns,
+ * row by row.  The kernels read and write whole 16-byte groups, and a 64-wide
+ * wave then moves 1 KB of contiguous memory per instruction.
+ *
+ * bdlm_state_pack copies nstates row-major states (s[p][n] at p * dstate + n)
+ * into the pool layout; bdlm_state_unpack does the reverse.  Both pointers are
+ * device fp32, 16-byte aligned, and must not overlap.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE (dstate not in {16, 32, 64, 128}, nstates < 0,
+ * or overlap), BDLM_E_ALIGN, BDLM_E_LAUNCH.
+ */
+int bdlm_state_pack(const float *rowmajor, float *pool, int64_t nstates, int64_t dstate,
+                    void *stream);
+int bdlm_state_unpack(const float *pool, float *rowmajor, int64_t nstates, int64_t dstate,
+                      void *stream);
+
+/*
+ * Reset cache slots to the empty prefix: states to zero (with a fill kernel,
+ * so the call is safe inside stream capture) and n_committed / n_blocks to 0.
+ * h_pool       device fp32 [nslots][state_elems], 16-byte aligned.
+ * slots        host int32 [nreset], each in [0, nslots); NULL resets all slots.
+ * n_committed, n_blocks  host int64 [nslots], may both be NULL.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_ALIGN, BDLM_E_SLOT, BDLM_E_LAUNCH.
+ */
+int bdlm_cache_reset(float *h_pool, int64_t nslots, int64_t state_elems, const int32_t *slots,
+                     int64_t nreset, int64_t *n_committed, int64_t *n_blocks, void *stream);
+
+/*
+ * Host-only argument checks used by the entry points above, exported so they
+ * can be exercised without a GPU.  Same arguments (the stream is not needed),
+ * same return codes; nothing is enqueued and nothing is modified.
+ */
+int bdlm_check_block_step(const bdlm_desc_t *desc, const void *x, const void *dt,
+                          const float *A, const void *B, const void *C, const float *D,
+                          const float *D_rev, const float *h_pool, int64_t nslots,
+                          const int32_t *slot_idx, const float *y);
+int bdlm_check_commit(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                      const void *B, const void *C, const float *D, const float *D_rev,
+                      const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                      const int64_t *n_committed, const int64_t *n_blocks,
+                      int64_t expected_block_index);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BDLM_H */

@@ -1,0 +1,353 @@
+"""Python binding of libbdlm, the MI355X (gfx950) block-restricted bidirectional Mamba scan.
+
+Argument marshalling only: every step of the computation runs in the HIP kernels
+behind the C ABI declared in ``include/bdlm.h``.  PyTorch supplies device memory
+and the stream; nothing here computes on the CPU, and there is no fallback: a
+missing library or a non-GPU tensor raises.
+
+Entry points (same names as the C ABI):
+
+* :func:`scan_block_step` -- one denoising step of the active block
+  (Sec. 4, Eq. partial-reverse): forward branch continued from the cached state,
+  block-local reverse branch from zero, summed.
+* :func:`commit_boundary` -- block finalisation: the clean block's forward state
+  replaces the cached one (Sec. 4, Eq. boundary-state).
+* :func:`cache_reset` -- empty the given cache slots.
+
+:class:`Cache` bundles a state pool with its host-side bookkeeping.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbdlm.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "bdlm.h")
+
+HEADDIM = 64
+MAX_BLOCK_LEN = 64
+MAX_SLOT_ROWS = 256
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+
+OK, E_NULL, E_SHAPE, E_DTYPE, E_ALIGN, E_OFFSET, E_SLOT, E_LAUNCH = 0, -1, -2, -3, -4, -5, -6, -7
+
+
+class BdlmError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {strerror(code)} (status {code})")
+
+
+class Desc(ctypes.Structure):
+    """Mirror of ``bdlm_desc_t``."""
+    _fields_ = [
+        ("batch", ctypes.c_int64),
+        ("nheads", ctypes.c_int64),
+        ("headdim", ctypes.c_int64),
+        ("dstate", ctypes.c_int64),
+        ("ngroups", ctypes.c_int64),
+        ("block_len", ctypes.c_int64),
+        ("in_dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("x_stride", ctypes.c_int64 * 3),
+        ("dt_stride", ctypes.c_int64 * 2),
+        ("bc_stride", ctypes.c_int64 * 3),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libbdlm.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2607_02805_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, fp = ctypes.c_void_p, ctypes.c_void_p
+        i64, i32p = ctypes.c_int64, ctypes.POINTER(ctypes.c_int32)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        dp = ctypes.POINTER(Desc)
+        L.bdlm_abi_version.restype = ctypes.c_int
+        L.bdlm_strerror.argtypes = [ctypes.c_int]
+        L.bdlm_strerror.restype = ctypes.c_char_p
+        L.bdlm_desc_init.argtypes = [dp, i64, i64, i64, i64, i64, i64, ctypes.c_int32]
+        L.bdlm_check_block_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, i64, i32p, fp]
+        L.bdlm_check_commit.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, i64, i32p, i64p, i64p,
+                                        i64]
+        L.bdlm_scan_block_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, i64, i32p, fp, vp]
+        L.bdlm_commit_boundary.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, i64, i32p, i64p,
+                                           i64p, i64, fp, vp]
+        L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
+        L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
+        L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
+        for name in ("bdlm_desc_init", "bdlm_check_block_step", "bdlm_check_commit",
+                     "bdlm_scan_block_step", "bdlm_commit_boundary", "bdlm_cache_reset",
+                     "bdlm_state_pack", "bdlm_state_unpack"):
+            getattr(L, name).restype = ctypes.c_int
+        if L.bdlm_abi_version() != 1:
+            raise RuntimeError("libbdlm ABI version mismatch")
+        _lib = L
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().bdlm_strerror(int(code)).decode()
+
+
+def header_functions() -> list[str]:
+    """Names of the functions ``include/bdlm.h`` declares."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(bdlm_\w+)\s*\(", text, re.M)))
+
+
+# ------------------------------------------------------------------ marshalling
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, what: str) -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor (no CPU path exists)")
+    return t.data_ptr()
+
+
+def _stream_handle(stream) -> int | None:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _desc(x, dt, Bm, Cm) -> Desc:
+    torch = _torch()
+    if x.dim() != 4 or dt.dim() != 3 or Bm.dim() != 4 or Cm.dim() != 4:
+        raise ValueError("x [B,L,H,P], dt [B,L,H], B and C [B,L,G,N] expected")
+    if not (x.dtype == dt.dtype == Bm.dtype == Cm.dtype):
+        raise ValueError("x, dt, B and C must share one dtype")
+    if x.dtype == torch.bfloat16:
+        dty = DTYPE_BF16
+    elif x.dtype == torch.float32:
+        dty = DTYPE_F32
+    else:
+        raise ValueError(f"activations must be bfloat16 or float32, got {x.dtype}")
+    bsz, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    if tuple(dt.shape) != (bsz, L, H) or tuple(Bm.shape) != (bsz, L, G, N) \
+            or tuple(Cm.shape) != tuple(Bm.shape):
+        raise ValueError("inconsistent activation shapes")
+    d = Desc()
+    if bsz * L == 0:
+        # nothing is read: the strides of an empty tensor carry no meaning
+        lib().bdlm_desc_init(ctypes.byref(d), bsz, H, P, N, G, L, dty)
+        return d
+    if x.stride(3) != 1 or dt.stride(2) != 1 or Bm.stride(3) != 1:
+        raise ValueError("innermost dimension of x, dt, B must be unit stride")
+    if tuple(Cm.stride()) != tuple(Bm.stride()):
+        raise ValueError("B and C must share strides")
+    d.batch, d.nheads, d.headdim, d.dstate, d.ngroups, d.block_len = bsz, H, P, N, G, L
+    d.in_dtype, d.reserved = dty, 0
+    d.x_stride[:] = list(x.stride()[:3])
+    d.dt_stride[:] = list(dt.stride()[:2])
+    d.bc_stride[:] = list(Bm.stride()[:3])
+    return d
+
+
+def _f32_vec(t, H, what):
+    torch = _torch()
+    if t.dtype != torch.float32 or t.dim() != 1 or t.shape[0] != H or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous float32 [{H}] tensor")
+    return _dev_ptr(t, what)
+
+
+def pool_shape(nslots: int, nheads: int, dstate: int) -> tuple:
+    """Shape of a state pool tensor: [nslots, nheads, dstate/4, 64, 4] (the pool layout of
+    include/bdlm.h: state element s[p][n] at [.., n // 4, p, n % 4])."""
+    return (nslots, nheads, dstate // 4, HEADDIM, 4)
+
+
+def _pool(h_pool, H, N):
+    torch = _torch()
+    if h_pool.dtype != torch.float32 or not h_pool.is_contiguous() or h_pool.dim() != 5 \
+            or tuple(h_pool.shape[1:]) != pool_shape(1, H, N)[1:]:
+        raise ValueError(f"h_pool must be a contiguous float32 {pool_shape('nslots', H, N)} "
+                         "tensor")
+    return _dev_ptr(h_pool, "h_pool")
+
+
+def _slots(slot_idx):
+    if slot_idx is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(slot_idx, dtype=np.int32))
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def scan_block_step(x, dt, A, B, C, D, D_rev, h_pool, y=None, slot_idx=None, stream=None):
+    """One active-block denoising step on the GPU; returns ``y`` (float32 [B, L, H, 64]).
+
+    ``h_pool`` is read only; ``slot_idx`` (host ints, optional) maps batch rows to
+    cache slots.  Work is enqueued on ``stream`` (default: torch's current stream).
+    """
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    if y is None:
+        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
+    elif y.dtype != torch.float32 or not y.is_contiguous() \
+            or tuple(y.shape) != (d.batch, d.block_len, H, HEADDIM):
+        raise ValueError("y must be a contiguous float32 [B, L, H, 64] tensor")
+    keep, sp = _slots(slot_idx)
+    rc = lib().bdlm_scan_block_step(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _pool(h_pool, H, N), h_pool.shape[0], sp, _dev_ptr(y, "y"), _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_scan_block_step")
+    return y
+
+
+def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
+                    expected_block_index=-1, slot_idx=None, y_clean=None, stream=None):
+    """Commit the clean block: ``h_pool`` updated in place, host bookkeeping advanced.
+
+    ``n_committed`` / ``n_blocks`` are host numpy int64 [nslots] arrays, updated in
+    place.  ``y_clean``: None (skip), True (allocate and return) or a float32 tensor.
+    Returns ``y_clean`` (or None).
+    """
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    nslots = h_pool.shape[0]
+    for a in (n_committed, n_blocks):
+        if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
+                or a.shape != (nslots,):
+            raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
+    if y_clean is True:
+        y_clean = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
+                              device=x.device)
+    yp = None
+    if y_clean is not None:
+        if y_clean.dtype != torch.float32 or not y_clean.is_contiguous() \
+                or tuple(y_clean.shape) != (d.batch, d.block_len, H, HEADDIM):
+            raise ValueError("y_clean must be a contiguous float32 [B, L, H, 64] tensor")
+        yp = _dev_ptr(y_clean, "y_clean")
+    keep, sp = _slots(slot_idx)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_commit_boundary(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _pool(h_pool, H, N), nslots, sp, n_committed.ctypes.data_as(i64p),
+        n_blocks.ctypes.data_as(i64p), int(expected_block_index), yp, _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_commit_boundary")
+    return y_clean
+
+
+def cache_reset(h_pool, slots=None, n_committed=None, n_blocks=None, stream=None):
+    """Zero the given slots of ``h_pool`` (all if None) and their bookkeeping."""
+    torch = _torch()
+    if h_pool.dtype != torch.float32 or not h_pool.is_contiguous():
+        raise ValueError("h_pool must be a contiguous float32 tensor")
+    nslots = h_pool.shape[0]
+    elems = h_pool[0].numel() if nslots else 0
+    keep, sp = _slots(slots)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_cache_reset(
+        _dev_ptr(h_pool, "h_pool"), nslots, elems, sp, 0 if keep is None else len(keep),
+        None if n_committed is None else n_committed.ctypes.data_as(i64p),
+        None if n_blocks is None else n_blocks.ctypes.data_as(i64p), _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_cache_reset")
+
+
+def state_pack(rowmajor, pool=None, stream=None):
+    """Row-major states [..., 64, dstate] (float32, GPU) -> a pool tensor [..., dstate/4, 64, 4]."""
+    torch = _torch()
+    if rowmajor.dtype != torch.float32 or not rowmajor.is_contiguous() or rowmajor.dim() < 2 \
+            or rowmajor.shape[-2] != HEADDIM:
+        raise ValueError("states must be a contiguous float32 [..., 64, dstate] tensor")
+    N = rowmajor.shape[-1]
+    lead = tuple(rowmajor.shape[:-2])
+    if pool is None:
+        pool = torch.empty(lead + (N // 4, HEADDIM, 4), dtype=torch.float32,
+                           device=rowmajor.device)
+    n = rowmajor.numel() // (HEADDIM * N)
+    rc = lib().bdlm_state_pack(_dev_ptr(rowmajor, "rowmajor"), _dev_ptr(pool, "pool"), n, N,
+                               _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_state_pack")
+    return pool
+
+
+def state_unpack(pool, rowmajor=None, stream=None):
+    """A pool tensor [..., dstate/4, 64, 4] -> row-major states [..., 64, dstate]."""
+    torch = _torch()
+    if pool.dtype != torch.float32 or not pool.is_contiguous() or pool.dim() < 3 \
+            or tuple(pool.shape[-2:]) != (HEADDIM, 4):
+        raise ValueError("pool must be a contiguous float32 [..., dstate/4, 64, 4] tensor")
+    N = pool.shape[-3] * 4
+    lead = tuple(pool.shape[:-3])
+    if rowmajor is None:
+        rowmajor = torch.empty(lead + (HEADDIM, N), dtype=torch.float32, device=pool.device)
+    n = pool.numel() // (HEADDIM * N)
+    rc = lib().bdlm_state_unpack(_dev_ptr(pool, "pool"), _dev_ptr(rowmajor, "rowmajor"), n, N,
+                                 _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_state_unpack")
+    return rowmajor
+
+
+class Cache:
+    """A pool of per-sequence forward boundary states for one Mamba layer.
+
+    ``h`` is a float32 GPU tensor in the pool layout, [nslots, nheads, dstate/4, 64, 4];
+    ``n_committed`` and ``n_blocks`` are host int64 arrays (tokens / blocks summarised
+    per slot).  :meth:`states` returns the states as row-major [nslots, nheads, 64, dstate].
+    """
+
+    def __init__(self, nslots: int, nheads: int, dstate: int, device="cuda"):
+        torch = _torch()
+        self.h = torch.zeros(pool_shape(nslots, nheads, dstate), dtype=torch.float32,
+                             device=device)
+        self.n_committed = np.zeros(nslots, np.int64)
+        self.n_blocks = np.zeros(nslots, np.int64)
+
+    def step(self, x, dt, A, B, C, D, D_rev, y=None, slot_idx=None, stream=None):
+        return scan_block_step(x, dt, A, B, C, D, D_rev, self.h, y, slot_idx, stream)
+
+    def commit(self, x, dt, A, B, C, D, D_rev, expected_block_index=-1, slot_idx=None,
+               y_clean=None, stream=None):
+        return commit_boundary(x, dt, A, B, C, D, D_rev, self.h, self.n_committed,
+                               self.n_blocks, expected_block_index, slot_idx, y_clean, stream)
+
+    def reset(self, slots=None, stream=None):
+        cache_reset(self.h, slots, self.n_committed, self.n_blocks, stream)
+
+    def states(self, stream=None):
+        """The cached states as a row-major [nslots, nheads, 64, dstate] tensor."""
+        return state_unpack(self.h, stream=stream)
+
+    def load_states(self, rowmajor, stream=None):
+        """Overwrite the states from a row-major [nslots, nheads, 64, dstate] tensor."""
+        state_pack(rowmajor.contiguous(), self.h, stream=stream)
+
+    def state_dict(self) -> dict:
+        """Checkpoint: the states (on the host) and the bookkeeping."""
+        return {"h": self.h.detach().cpu(), "n_committed": self.n_committed.copy(),
+                "n_blocks": self.n_blocks.copy()}
+
+    def load_state_dict(self, sd: dict) -> None:
+        if tuple(sd["h"].shape) != tuple(self.h.shape):
+            raise ValueError("checkpoint shape does not match this cache")
+        self.h.copy_(sd["h"])
+        self.n_committed[:] = sd["n_committed"]
+        self.n_blocks[:] = sd["n_blocks"]

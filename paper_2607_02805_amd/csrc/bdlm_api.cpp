@@ -1,0 +1,242 @@
+// bdlm_api.cpp -- the C ABI of libbdlm (declared in include/bdlm.h): argument
+// checks on the host, cache bookkeeping, and dispatch to the HIP launchers.
+// Every check runs before anything is enqueued, so every error path can be
+// exercised without a GPU.
+#include <stdint.h>
+#include <string.h>
+
+#include "bdlm.h"
+#include "bdlm_launch.h"
+
+namespace {
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int64_t elem_size(int32_t dt) { return dt == BDLM_DTYPE_BF16 ? 2 : 4; }
+
+// Checks shared by a step and a commit.
+int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                 const void *B, const void *C, const float *D, const float *D_rev,
+                 const float *h_pool, int64_t nslots, const int32_t *slot_idx) {
+    if (!d) return BDLM_E_NULL;
+    if (d->in_dtype != BDLM_DTYPE_F32 && d->in_dtype != BDLM_DTYPE_BF16) return BDLM_E_DTYPE;
+    if (d->reserved != 0) return BDLM_E_DTYPE;
+    if (d->batch < 0 || d->nheads <= 0 || d->ngroups <= 0 || d->block_len < 0) return BDLM_E_SHAPE;
+    if (d->headdim != BDLM_HEADDIM) return BDLM_E_SHAPE;
+    if (d->dstate != 16 && d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
+        return BDLM_E_SHAPE;
+    if (d->block_len > BDLM_MAX_BLOCK_LEN) return BDLM_E_SHAPE;
+    if (d->nheads % d->ngroups != 0) return BDLM_E_SHAPE;
+    if (nslots <= 0) return BDLM_E_SHAPE;
+    // grid and 32-bit index limits of the kernels
+    if (d->batch * d->nheads > (int64_t(1) << 30) || d->nheads > (1 << 20)) return BDLM_E_SHAPE;
+    if (nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate)) return BDLM_E_SHAPE;
+    for (int i = 0; i < 3; ++i)
+        if (d->x_stride[i] < 0 || d->bc_stride[i] < 0) return BDLM_E_SHAPE;
+    if (d->dt_stride[0] < 0 || d->dt_stride[1] < 0) return BDLM_E_SHAPE;
+    if (slot_idx && d->batch > BDLM_MAX_SLOT_ROWS) return BDLM_E_SHAPE;
+    // With no token to read, the activation pointers may be NULL (an empty tensor
+    // can have no storage).
+    const bool empty = d->batch == 0 || d->block_len == 0;
+    if (!empty && (!x || !dt || !B || !C)) return BDLM_E_NULL;
+    if (!A || !D || !D_rev || !h_pool) return BDLM_E_NULL;
+
+    // x, B and C are read in 16-byte vectors: base pointers 16-byte aligned and
+    // every stride a whole number of 16-byte units.
+    const int64_t es = elem_size(d->in_dtype);
+    const int64_t vec = 16 / es;
+    if (!aligned(x, 16) || !aligned(B, 16) || !aligned(C, 16)) return BDLM_E_ALIGN;
+    if (!aligned(dt, es)) return BDLM_E_ALIGN;
+    for (int i = 0; i < 3; ++i)
+        if (d->bc_stride[i] % vec != 0 || d->x_stride[i] % vec != 0) return BDLM_E_ALIGN;
+    if (!aligned(A, 4) || !aligned(D, 4) || !aligned(D_rev, 4)) return BDLM_E_ALIGN;
+    if (!aligned(h_pool, 16)) return BDLM_E_ALIGN;
+
+    if (slot_idx) {
+        for (int64_t b = 0; b < d->batch; ++b)
+            if (slot_idx[b] < 0 || slot_idx[b] >= nslots) return BDLM_E_SLOT;
+    } else if (d->batch > nslots) {
+        return BDLM_E_SLOT;
+    }
+    return BDLM_OK;
+}
+
+bdlm::LaunchArgs make_args(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                           const void *B, const void *C, const float *D, const float *D_rev,
+                           float *h_pool, const int32_t *slot_idx, float *y) {
+    bdlm::LaunchArgs a;
+    a.x = x;
+    a.dt = dt;
+    a.Bm = B;
+    a.Cm = C;
+    a.A = A;
+    a.D = D;
+    a.D_rev = D_rev;
+    a.h_pool = h_pool;
+    a.y = y;
+    a.xs_b = d->x_stride[0];
+    a.xs_t = d->x_stride[1];
+    a.xs_h = d->x_stride[2];
+    a.dts_b = d->dt_stride[0];
+    a.dts_t = d->dt_stride[1];
+    a.bcs_b = d->bc_stride[0];
+    a.bcs_t = d->bc_stride[1];
+    a.bcs_g = d->bc_stride[2];
+    a.batch = static_cast<int32_t>(d->batch);
+    a.nheads = static_cast<int32_t>(d->nheads);
+    a.ngroups = static_cast<int32_t>(d->ngroups);
+    a.L = static_cast<int32_t>(d->block_len);
+    a.dstate = static_cast<int32_t>(d->dstate);
+    a.bf16 = d->in_dtype == BDLM_DTYPE_BF16 ? 1 : 0;
+    a.slots = slot_idx;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bdlm_abi_version(void) { return BDLM_ABI_VERSION; }
+
+const char *bdlm_strerror(int status) {
+    switch (status) {
+        case BDLM_OK: return "ok";
+        case BDLM_E_NULL: return "a required pointer is NULL";
+        case BDLM_E_SHAPE: return "unsupported or inconsistent sizes";
+        case BDLM_E_DTYPE: return "unknown activation dtype or nonzero reserved field";
+        case BDLM_E_ALIGN: return "pointer or stride breaks the alignment contract";
+        case BDLM_E_OFFSET: return "cache slot does not hold the expected number of blocks";
+        case BDLM_E_SLOT: return "slot index out of range or repeated in a commit";
+        case BDLM_E_LAUNCH: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+int bdlm_desc_init(bdlm_desc_t *d, int64_t batch, int64_t nheads, int64_t headdim, int64_t dstate,
+                   int64_t ngroups, int64_t block_len, int32_t in_dtype) {
+    if (!d) return BDLM_E_NULL;
+    memset(d, 0, sizeof *d);
+    d->batch = batch;
+    d->nheads = nheads;
+    d->headdim = headdim;
+    d->dstate = dstate;
+    d->ngroups = ngroups;
+    d->block_len = block_len;
+    d->in_dtype = in_dtype;
+    d->x_stride[2] = headdim;
+    d->x_stride[1] = nheads * headdim;
+    d->x_stride[0] = block_len * nheads * headdim;
+    d->dt_stride[1] = nheads;
+    d->dt_stride[0] = block_len * nheads;
+    d->bc_stride[2] = dstate;
+    d->bc_stride[1] = ngroups * dstate;
+    d->bc_stride[0] = block_len * ngroups * dstate;
+    return BDLM_OK;
+}
+
+int bdlm_check_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                          const void *B, const void *C, const float *D, const float *D_rev,
+                          const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                          const float *y) {
+    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    if (rc != BDLM_OK) return rc;
+    if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
+    if (!aligned(y, 16)) return BDLM_E_ALIGN;
+    return BDLM_OK;
+}
+
+int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                      const void *B, const void *C, const float *D, const float *D_rev,
+                      const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                      const int64_t *n_committed, const int64_t *n_blocks,
+                      int64_t expected_block_index) {
+    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    if (rc != BDLM_OK) return rc;
+    if (!n_committed || !n_blocks) return BDLM_E_NULL;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        if (slot_idx)
+            for (int64_t c = 0; c < b; ++c)
+                if (slot_idx[c] == s) return BDLM_E_SLOT;
+        if (expected_block_index >= 0 && n_blocks[s] != expected_block_index) return BDLM_E_OFFSET;
+    }
+    return BDLM_OK;
+}
+
+int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, const float *D_rev,
+                         const float *h_pool, int64_t nslots, const int32_t *slot_idx, float *y,
+                         void *stream) {
+    const int rc =
+        bdlm_check_block_step(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx, y);
+    if (rc != BDLM_OK) return rc;
+    // The step never writes the cache; the kernel receives it through the same
+    // argument block as a commit, with the state update compiled out.
+    const bdlm::LaunchArgs a =
+        make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
+    return bdlm::launch_block(a, false, stream);
+}
+
+int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, const float *D_rev,
+                         float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                         int64_t *n_committed, int64_t *n_blocks, int64_t expected_block_index,
+                         float *y_clean, void *stream) {
+    int rc = bdlm_check_commit(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx, n_committed,
+                               n_blocks, expected_block_index);
+    if (rc != BDLM_OK) return rc;
+    if (y_clean && !aligned(y_clean, 16)) return BDLM_E_ALIGN;
+    const bdlm::LaunchArgs a =
+        make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
+    rc = bdlm::launch_block(a, true, stream);
+    if (rc != BDLM_OK) return rc;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        n_committed[s] += d->block_len;
+        n_blocks[s] += 1;
+    }
+    return BDLM_OK;
+}
+
+static int state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
+                         bool to_pool, void *stream) {
+    if (!src || !dst) return BDLM_E_NULL;
+    if (nstates < 0 || (dstate != 16 && dstate != 32 && dstate != 64 && dstate != 128))
+        return BDLM_E_SHAPE;
+    if (!aligned(src, 16) || !aligned(dst, 16)) return BDLM_E_ALIGN;
+    const int64_t bytes = nstates * BDLM_HEADDIM * dstate * 4;
+    const char *s = reinterpret_cast<const char *>(src), *t = reinterpret_cast<const char *>(dst);
+    if (s < t + bytes && t < s + bytes && nstates > 0) return BDLM_E_SHAPE;  // overlap
+    return bdlm::launch_state_permute(src, dst, nstates, dstate, to_pool, stream);
+}
+
+int bdlm_state_pack(const float *rowmajor, float *pool, int64_t nstates, int64_t dstate,
+                    void *stream) {
+    return state_permute(rowmajor, pool, nstates, dstate, true, stream);
+}
+
+int bdlm_state_unpack(const float *pool, float *rowmajor, int64_t nstates, int64_t dstate,
+                      void *stream) {
+    return state_permute(pool, rowmajor, nstates, dstate, false, stream);
+}
+
+int bdlm_cache_reset(float *h_pool, int64_t nslots, int64_t state_elems, const int32_t *slots,
+                     int64_t nreset, int64_t *n_committed, int64_t *n_blocks, void *stream) {
+    if (!h_pool) return BDLM_E_NULL;
+    if (nslots <= 0 || state_elems <= 0 || state_elems % 4 != 0 || nreset < 0) return BDLM_E_SHAPE;
+    if (!aligned(h_pool, 16)) return BDLM_E_ALIGN;
+    if (slots)
+        for (int64_t i = 0; i < nreset; ++i)
+            if (slots[i] < 0 || slots[i] >= nslots) return BDLM_E_SLOT;
+    const int rc = bdlm::launch_reset(h_pool, nslots, state_elems, slots, nreset, stream);
+    if (rc != BDLM_OK) return rc;
+    const int64_t count = slots ? nreset : nslots;
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t s = slots ? slots[i] : i;
+        if (n_committed) n_committed[s] = 0;
+        if (n_blocks) n_blocks[s] = 0;
+    }
+    return BDLM_OK;
+}
+
+}  // extern "C"

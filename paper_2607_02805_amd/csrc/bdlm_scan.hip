@@ -1,0 +1,594 @@
+// bdlm_scan.hip -- gfx950 (CDNA4) kernels for the block-restricted bidirectional
+// Mamba scan of BDLM Mamba-H.
+//
+// What one launch computes, per batch row b and head h (group g = h / (H/G)):
+//   forward branch  (Sec. 4, Eq. partial-reverse, first row): the selective
+//     update of Sec. 3, Eq. mamba-scan-background, continued through the L block
+//     tokens from the cached boundary state s = h_pool[slot(b), h];
+//   reverse branch  (second row): the same update over the reversed block from
+//     a zero state;
+//   y = forward + reverse (third row), written in fp32;
+//   commit          (Eq. boundary-state): the forward state after the block
+//     replaces s.
+//
+// Both branches are evaluated in the masked-matrix ("state-space dual") form
+// rather than token by token.  With l_t = dt_t A_h, cs_t = l_0 + ... + l_t and
+// ex_t = cs_{t-1} (ex_0 = 0):
+//   y[t,:] = exp(cs_t) (C_t . s^T)                         prefix (forward only)
+//          + sum_j G[t,j] W[t,j] dt_j x[j,:]                both branches at once
+//          + (D + D_rev) x[t,:]
+//   G[t,j] = C_t . B_j,
+//   W[t,j] = exp(cs_t - cs_j)   for j < t   (forward decay from j to t)
+//          = 2                  for j = t   (the token's own input, once per branch)
+//          = exp(ex_j - ex_t)   for j > t   (reverse decay: a_t ... a_{j-1})
+//   s_new  = exp(cs_{L-1}) s + sum_j exp(cs_{L-1} - cs_j) dt_j x[j,:] (outer) B_j
+//
+// Work decomposition: one workgroup of four 64-wide waves per (b, h); wave w
+// owns head-dim columns [16w, 16w+16).  All contractions run on bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16 / 16x16x16) with fp32 accumulation.  Operands that
+// are not exact in bf16 (the fp32 state, the fp32 decay-weighted matrices, and
+// fp32 activations) are split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi),
+// which leaves a relative residual below 2^-16; products of bf16 values are
+// exact in fp32.
+//
+// Register layouts.  Every 16x16 MFMA tile uses lane = 16 * grp + col.  An
+// operand "quad" is the four values a lane contributes to 16 consecutive
+// contraction indices: lane (col, grp) holds indices 4*grp .. 4*grp+3 of that
+// run.  Because an MFMA only needs A and B to agree on which contraction index
+// each lane slot carries, the state s[p, n] is kept in the accumulator layout
+// of the commit product (lane (col = p, grp) holds s[p, 16q + 4grp + r],
+// r = 0..3): one 16-byte load per quad q, used directly as the B operand of
+// the prefix product and as the accumulator of the commit, then stored back
+// with one 16-byte store.  The Gram product is computed transposed (rows j,
+// columns t) so that its accumulator is already the A operand of the
+// intra-block product.
+//
+// State layout in HBM: each (slot, head) state is dstate/4 blocks of [64][4]
+// floats, s[p, n] at ((n / 4) * 64 + p) * 4 + n % 4.  A wave's 16-byte quad
+// loads then cover 1 KB of contiguous memory per instruction.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bdlm.h"
+#include "bdlm_launch.h"
+
+namespace bdlm {
+namespace {
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kP = BDLM_HEADDIM;  // 64 head-dim columns per head
+constexpr int kThreads = 256;     // 4 waves x 16 columns
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct KArgs {
+    const void *x, *dt, *Bm, *Cm;
+    const float *A, *D, *D_rev;
+    float *h_pool;
+    float *y;
+    int64_t xs_b, xs_t, xs_h;
+    int64_t dts_b, dts_t;
+    int64_t bcs_b, bcs_t, bcs_g;
+    int32_t nheads, heads_per_group, L;
+    int32_t xcd_remap;   // 1: group consecutive units per XCD (grid % 8 == 0)
+    int32_t use_slots;
+    int32_t slots[BDLM_MAX_SLOT_ROWS];
+};
+
+// ---------------------------------------------------------------- bf16 helpers
+__device__ __forceinline__ short bf16_bits(float v) {
+    return __builtin_bit_cast(short, static_cast<__bf16>(v));  // round to nearest even
+}
+__device__ __forceinline__ float bf16_to_f32(short s) {
+    return __uint_as_float(static_cast<uint32_t>(static_cast<uint16_t>(s)) << 16);
+}
+// v = hi + lo + O(2^-16 |v|)
+__device__ __forceinline__ void split4(f32x4 v, s16x4 &hi, s16x4 &lo) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const short hb = bf16_bits(v[k]);
+        hi[k] = hb;
+        lo[k] = bf16_bits(v[k] - bf16_to_f32(hb));
+    }
+}
+
+// Activation storage.
+template <bool F32> struct Act;
+template <> struct Act<false> {
+    using T = uint16_t;
+    static __device__ __forceinline__ float val(T v) {
+        return __uint_as_float(static_cast<uint32_t>(v) << 16);
+    }
+};
+template <> struct Act<true> {
+    using T = float;
+    static __device__ __forceinline__ float val(T v) { return v; }
+};
+
+// ---------------------------------------------------------------- MFMA helpers
+__device__ __forceinline__ f32x4 mma_k32(s16x4 a0, s16x4 a1, s16x4 b0, s16x4 b1, f32x4 c) {
+    const s16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    const s16x8 b = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_k16(s16x4 a, s16x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+// c += sum over Q quads of A_q B_q (16 contraction indices per quad).
+template <int Q>
+__device__ __forceinline__ f32x4 mma_quads(const s16x4 (&a)[Q], const s16x4 (&b)[Q], f32x4 c) {
+#pragma unroll
+    for (int q = 0; q + 1 < Q; q += 2) c = mma_k32(a[q], a[q + 1], b[q], b[q + 1], c);
+    if constexpr (Q & 1) c = mma_k16(a[Q - 1], b[Q - 1], c);
+    return c;
+}
+
+__device__ __forceinline__ float shfl(float v, int src) { return __shfl(v, src, 64); }
+
+// Rows past the end of the block read this zero chunk instead of activations: the
+// load address is selected, never the loaded value, so every load stays an
+// unconditional instruction that can be issued ahead of any wait.
+__device__ const uint4 kZeroChunk = {0u, 0u, 0u, 0u};
+
+// Global-address-space views, so selected pointers still compile to global loads.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const u32x4 g_u4;
+template <typename T>
+__device__ __forceinline__ const g_u4 *gchunk(const T *p) {
+    return (const g_u4 *)(p);
+}
+__device__ __forceinline__ const g_u4 *gzero() { return (const g_u4 *)(&kZeroChunk); }
+
+__device__ __forceinline__ s16x4 as_s16x4(uint2 v) { return __builtin_bit_cast(s16x4, v); }
+__device__ __forceinline__ uint2 as_u2(s16x4 v) { return __builtin_bit_cast(uint2, v); }
+
+// LDS image of B or C: the quad that lane (col, grp) of an MFMA operand holds for
+// token tile mt and dstate quad q (rows 16mt + col, columns 16q + 4grp .. +3).
+// The column-in-tile is XOR-swizzled with the index of the 16-byte global chunk
+// the quad came from, so a wave writing one row's chunks and a wave reading one
+// quad per lane both touch 16 distinct bank pairs per 16 lanes.
+template <int QN, bool F32>
+__device__ __forceinline__ int img_idx(int mt, int q, int grp, int col) {
+    const int chunk = F32 ? (4 * q + grp) : (2 * q + (grp >> 1));
+    return (mt * QN + q) * 64 + grp * 16 + (col ^ (chunk & 15));
+}
+
+// ------------------------------------------------------------------- the kernel
+// LT: block tile (16, 32 or 64 tokens; the block length L <= LT, padded tokens
+//     have dt = 0, x = B = C = 0, which changes no output and no state).
+// NS: dstate.  F32: fp32 activation storage.  COMMIT: also update the state.
+//
+// Phases:
+//   0. every global load is issued up front and unconditionally (rows past the
+//      block are clamped to a valid row and zeroed after the load): B, C, x and
+//      dt in coalesced 16-byte chunks by the whole workgroup, then the state,
+//      16 bytes per quad, into registers;
+//   1. B and C are written to LDS as "register images" (the exact per-lane quads
+//      an MFMA operand needs, so reading one is a linear, conflict-free 8-byte
+//      read), x row-major, dt as floats;
+//   2. each wave runs the decay prefix sums of the block (lane t = token t) and
+//      computes its share of the Gram tiles, turns them into the decay-weighted
+//      matrix M[t,j] = G[t,j] W[t,j] dt_j, splits it and publishes it in LDS;
+//   3. each wave contracts M with x (its 16 columns), C with its 16 rows of the
+//      state (the only step that waits for the state loads), adds the skip
+//      term and stores y; a commit then adds the block to the state in place.
+template <int LT, int NS, bool F32, bool COMMIT>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+bdlm_block_kernel(const KArgs args) {
+    constexpr int MT = LT / 16;           // token tiles = quads along the block
+    constexpr int QN = NS / 16;           // quads along dstate
+    constexpr int IMG = MT * QN * 64;     // quads in one image of B or C
+    constexpr int E = F32 ? 4 : 8;        // activations per 16-byte chunk
+    constexpr int XS = kP + 4;            // x row stride in LDS (elements)
+    using AT = typename Act<F32>::T;
+
+    __shared__ __align__(16) uint2 sC[IMG], sB[IMG];                  // bf16 quads (hi)
+    __shared__ __align__(16) uint2 sCl[F32 ? IMG : 1], sBl[F32 ? IMG : 1];  // lo, fp32 input
+    __shared__ __align__(16) AT sX[LT * XS];
+    __shared__ __align__(16) float sDt[64];
+    __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
+    constexpr int YS = kP + 4;                                         // y row stride
+    __shared__ __align__(16) float sY[LT * YS];                       // y tile for stores
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int col = lane & 15, grp = lane >> 4;
+
+    // Unit (b, h).  Workgroups are dealt to the 8 XCDs round-robin; remapping
+    // gives each XCD a contiguous run of units, so the heads of one batch row
+    // (which share B and C) sit behind one L2.
+    int u = blockIdx.x;
+    if (args.xcd_remap) u = (u & 7) * (static_cast<int>(gridDim.x) >> 3) + (u >> 3);
+    const int b = u / args.nheads;
+    const int h = u - b * args.nheads;
+    const int g = h / args.heads_per_group;
+    const int64_t slot = args.use_slots ? args.slots[b] : b;
+    const int L = args.L;                 // 1 <= L <= LT
+    const int p = wave * 16 + col;
+
+    const AT *xg = static_cast<const AT *>(args.x) + b * args.xs_b + h * args.xs_h;
+    const AT *dtg = static_cast<const AT *>(args.dt) + b * args.dts_b + h;
+    const AT *Bg = static_cast<const AT *>(args.Bm) + b * args.bcs_b + g * args.bcs_g;
+    const AT *Cg = static_cast<const AT *>(args.Cm) + b * args.bcs_b + g * args.bcs_g;
+    // this lane's quads of the state: s[p, 16q + 4grp + r] at hs + q * 1024
+    float *hs = args.h_pool + (slot * args.nheads + h) * kP * NS + (grp * kP + p) * 4;
+
+    // ---- phase 0: loads
+    constexpr int CPR = NS / E;                           // 16-byte chunks per row
+    constexpr int BC_CH = LT * CPR;                       // chunks per matrix
+    constexpr int BC_PT = BC_CH >= kThreads ? BC_CH / kThreads : 1;
+    u32x4 cch[BC_PT], bch[BC_PT];
+#pragma unroll
+    for (int k = 0; k < BC_PT; ++k) {
+        const int i = (tid + kThreads * k) % BC_CH;        // chunk fastest (coalesced)
+        const int t = i / CPR, c = i % CPR;
+        const int64_t o = t * args.bcs_t + c * E;
+        const bool ok = t < L;
+        cch[k] = *(ok ? gchunk(Cg + o) : gzero());
+        bch[k] = *(ok ? gchunk(Bg + o) : gzero());
+    }
+    constexpr int X_CH = LT * (kP / E);
+    constexpr int X_PT = X_CH >= kThreads ? X_CH / kThreads : 1;
+    u32x4 xch[X_PT];
+#pragma unroll
+    for (int k = 0; k < X_PT; ++k) {
+        const int i = (tid + kThreads * k) % X_CH;         // chunk fastest (coalesced)
+        const int j = i / (kP / E), c = i % (kP / E);
+        xch[k] = *(j < L ? gchunk(xg + j * args.xs_t + c * E) : gzero());
+    }
+    typedef __attribute__((address_space(1))) const AT g_at;
+    const AT dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
+                                : (const g_at *)(&kZeroChunk));
+    // keep the small loads above ahead of the state loads (loads return in order)
+    __builtin_amdgcn_sched_barrier(0);
+    f32x4 hq[QN];  // state s[p, 16q + 4grp + r]
+#pragma unroll
+    for (int q = 0; q < QN; ++q) hq[q] = *reinterpret_cast<const f32x4 *>(hs + q * 16 * kP);
+
+    // ---- phase 1: LDS images
+#pragma unroll
+    for (int k = 0; k < BC_PT; ++k) {
+        const int i = (tid + kThreads * k) % BC_CH;
+        const int t = i / CPR, c = i % CPR;
+        const u32x4 cz = cch[k], bz = bch[k];
+        if constexpr (F32) {
+            // 4 floats = one quad: q = c / 4, grp = c % 4
+            const int at = img_idx<QN, F32>(t >> 4, c >> 2, c & 3, t & 15);
+            s16x4 hi, lo;
+            split4(__builtin_bit_cast(f32x4, cz), hi, lo);
+            sC[at] = as_u2(hi);
+            sCl[at] = as_u2(lo);
+            split4(__builtin_bit_cast(f32x4, bz), hi, lo);
+            sB[at] = as_u2(hi);
+            sBl[at] = as_u2(lo);
+        } else {
+            // 8 bf16 = two quads: q = c / 2, grp = 2 (c % 2) and 2 (c % 2) + 1
+            const int at = img_idx<QN, F32>(t >> 4, c >> 1, 2 * (c & 1), t & 15);
+            sC[at] = uint2{cz.x, cz.y};
+            sC[at + 16] = uint2{cz.z, cz.w};
+            sB[at] = uint2{bz.x, bz.y};
+            sB[at + 16] = uint2{bz.z, bz.w};
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < X_PT; ++k) {
+        const int i = (tid + kThreads * k) % X_CH;
+        const int j = i / (kP / E), c = i % (kP / E);
+        const u32x4 v = xch[k];
+        uint2 *dst = reinterpret_cast<uint2 *>(&sX[j * XS + c * E]);
+        dst[0] = uint2{v.x, v.y};
+        dst[1] = uint2{v.z, v.w};
+    }
+    if (tid < 64) sDt[tid] = Act<F32>::val(dtraw);
+    __syncthreads();
+
+    // ---- phase 2: decay prefix sums (every wave), Gram tiles (split over waves)
+    const float dtv = sDt[lane];
+    const float A2 = args.A[h] * kLog2e;  // work in base 2
+    const float l2 = dtv * A2;
+    float cs = l2;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const float v = __shfl_up(cs, off, 64);
+        if (lane >= off) cs += v;
+    }
+    float ex = __shfl_up(cs, 1, 64);
+    if (lane == 0) ex = 0.f;
+
+    for (int tile = wave; tile < MT * MT; tile += 4) {
+        const int mt = tile / MT, jt = tile % MT;
+        // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
+        f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+        s16x4 bq[QN], cq[QN];
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+            bq[q] = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
+            cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+        }
+        gacc = mma_quads<QN>(bq, cq, gacc);
+        if constexpr (F32) {
+            s16x4 bl[QN], cl[QN];
+#pragma unroll
+            for (int q = 0; q < QN; ++q) {
+                bl[q] = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
+                cl[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+            }
+            gacc = mma_quads<QN>(bq, cl, gacc);
+            gacc = mma_quads<QN>(bl, cq, gacc);
+        }
+        const int t = 16 * mt + col;
+        const float cst = shfl(cs, t), ext = shfl(ex, t);
+        f32x4 m;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j = 16 * jt + 4 * grp + r;
+            const float csj = shfl(cs, j), exj = shfl(ex, j), dtj = shfl(dtv, j);
+            float w;
+            if (j < t) w = exp2f(cst - csj);
+            else if (j == t) w = 2.f;
+            else w = exp2f(exj - ext);
+            m[r] = gacc[r] * w * dtj;
+        }
+        s16x4 mh, ml;
+        split4(m, mh, ml);
+        const uint2 a = as_u2(mh), c2 = as_u2(ml);
+        sM[tile * 64 + lane] = uint4{a.x, a.y, c2.x, c2.y};
+    }
+    __syncthreads();
+
+    // ---- phase 3: x quads (B operand, j = 16jt + 4grp + r), products, output
+    float xv[MT][4];
+    s16x4 xq[MT], xl[MT];
+#pragma unroll
+    for (int jt = 0; jt < MT; ++jt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            xv[jt][r] = Act<F32>::val(sX[(16 * jt + 4 * grp + r) * XS + p]);
+        split4(f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}, xq[jt], xl[jt]);
+    }
+
+    float *yb = args.y;
+    const bool want_y = !COMMIT || yb != nullptr;
+    if (want_y) {
+        const float skip = args.D[h] + args.D_rev[h];
+        f32x4 ai[MT], ap[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            s16x4 mh[MT], ml[MT];
+#pragma unroll
+            for (int jt = 0; jt < MT; ++jt) {
+                const uint4 v = sM[(mt * MT + jt) * 64 + lane];
+                mh[jt] = as_s16x4(uint2{v.x, v.y});
+                ml[jt] = as_s16x4(uint2{v.z, v.w});
+            }
+            ai[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            ai[mt] = mma_quads<MT>(mh, xq, ai[mt]);
+            ai[mt] = mma_quads<MT>(ml, xq, ai[mt]);
+            if constexpr (F32) ai[mt] = mma_quads<MT>(mh, xl, ai[mt]);
+        }
+        // prefix term: C (rows t) against the state (columns p); waits for the state
+        s16x4 hh[QN], hl[QN];
+#pragma unroll
+        for (int q = 0; q < QN; ++q) split4(hq[q], hh[q], hl[q]);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            s16x4 cq[QN];
+#pragma unroll
+            for (int q = 0; q < QN; ++q) cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+            ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            ap[mt] = mma_quads<QN>(cq, hh, ap[mt]);
+            ap[mt] = mma_quads<QN>(cq, hl, ap[mt]);
+            if constexpr (F32) {
+                s16x4 cl[QN];
+#pragma unroll
+                for (int q = 0; q < QN; ++q)
+                    cl[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                ap[mt] = mma_quads<QN>(cl, hh, ap[mt]);
+            }
+        }
+        // y tile through LDS, then whole 256-byte rows out with 16-byte stores
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * mt + 4 * grp + r;
+                const float e = exp2f(shfl(cs, t));
+                sY[t * YS + p] = e * ap[mt][r] + ai[mt][r] + skip * xv[mt][r];
+            }
+        }
+        __syncthreads();
+        constexpr int Y_CH = LT * (kP / 4);
+#pragma unroll
+        for (int k = 0; k < (Y_CH + kThreads - 1) / kThreads; ++k) {
+            const int i = tid + kThreads * k;
+            const int t = i >> 4, c = i & 15;
+            if (i < Y_CH && t < L)
+                *reinterpret_cast<f32x4 *>(
+                    yb + ((static_cast<int64_t>(b) * L + t) * args.nheads + h) * kP + 4 * c) =
+                    *reinterpret_cast<const f32x4 *>(&sY[t * YS + 4 * c]);
+        }
+    }
+
+    if constexpr (COMMIT) {
+        // s_new[p, n] = exp(cs_last) s[p, n] + sum_j x[j, p] exp(cs_last - cs_j) dt_j B[j, n]
+        // A operand: lane (col, grp) holds the weighted B[16jt + 4grp + r, 16q + col],
+        // read from the B image (element (j, n) sits in the quad of tile j/16, quad
+        // n/16, group n%16/4, column j%16, at slot n%4).
+        const float cl2 = shfl(cs, 63);  // cs of the last real token (padding adds 0)
+        const float keep = exp2f(cl2);
+        float wj[MT][4];
+#pragma unroll
+        for (int jt = 0; jt < MT; ++jt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int j = 16 * jt + 4 * grp + r;
+                wj[jt][r] = exp2f(cl2 - shfl(cs, j)) * shfl(dtv, j);
+            }
+        const uint16_t *sBh = reinterpret_cast<const uint16_t *>(sB);
+        const uint16_t *sBlo = reinterpret_cast<const uint16_t *>(sBl);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+            s16x4 th[MT], tl[MT];
+#pragma unroll
+            for (int jt = 0; jt < MT; ++jt) {
+                f32x4 v;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int e = img_idx<QN, F32>(jt, q, col >> 2, 4 * grp + r) * 4 + (col & 3);
+                    float bv = bf16_to_f32(static_cast<short>(sBh[e]));
+                    if constexpr (F32) bv += bf16_to_f32(static_cast<short>(sBlo[e]));
+                    v[r] = bv * wj[jt][r];
+                }
+                split4(v, th[jt], tl[jt]);
+            }
+            f32x4 acc = hq[q] * keep;
+            acc = mma_quads<MT>(th, xq, acc);
+            acc = mma_quads<MT>(tl, xq, acc);
+            if constexpr (F32) acc = mma_quads<MT>(th, xl, acc);
+            *reinterpret_cast<f32x4 *>(hs + q * 16 * kP) = acc;
+        }
+    }
+}
+
+// Zero whole states: grid.y indexes the slot list, grid.x the float4s of a state.
+struct ResetArgs {
+    float *h_pool;
+    int64_t state_elems;
+    int64_t first_slot;  // used when use_slots == 0
+    int32_t use_slots;
+    int32_t slots[BDLM_MAX_SLOT_ROWS];
+};
+
+__global__ void __launch_bounds__(256) bdlm_reset_kernel(const ResetArgs a) {
+    const int64_t s = a.use_slots ? a.slots[blockIdx.y] : a.first_slot + blockIdx.y;
+    f32x4 *dst = reinterpret_cast<f32x4 *>(a.h_pool + s * a.state_elems);
+    const int64_t n4 = a.state_elems / 4;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n4;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        dst[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Row-major states [n][64][dstate] <-> the pool layout [n][dstate/4][64][4].
+// One thread moves one 16-byte quad; i enumerates (state, p, n/4) in row-major order.
+__global__ void __launch_bounds__(256)
+bdlm_state_permute_kernel(const float *src, float *dst, int64_t nstates, int dstate, int to_pool) {
+    const int n4s = dstate / 4;
+    const int64_t quads = nstates * kP * n4s;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < quads;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t st = i / (kP * n4s);
+        const int rem = static_cast<int>(i - st * kP * n4s);
+        const int pp = rem / n4s, n4 = rem - pp * n4s;
+        const int64_t rm = (st * kP + pp) * dstate + 4 * n4;
+        const int64_t pl = st * kP * dstate + (static_cast<int64_t>(n4) * kP + pp) * 4;
+        if (to_pool)
+            *reinterpret_cast<f32x4 *>(dst + pl) = *reinterpret_cast<const f32x4 *>(src + rm);
+        else
+            *reinterpret_cast<f32x4 *>(dst + rm) = *reinterpret_cast<const f32x4 *>(src + pl);
+    }
+}
+
+template <int LT, int NS, bool F32, bool COMMIT>
+hipError_t launch_t(const KArgs &k, unsigned grid, hipStream_t s) {
+    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT>), dim3(grid), dim3(kThreads), 0,
+                       s, k);
+    return hipGetLastError();
+}
+
+template <int LT, bool F32, bool COMMIT>
+hipError_t by_ns(int ns, const KArgs &k, unsigned grid, hipStream_t s) {
+    switch (ns) {
+        case 16: return launch_t<LT, 16, F32, COMMIT>(k, grid, s);
+        case 32: return launch_t<LT, 32, F32, COMMIT>(k, grid, s);
+        case 64: return launch_t<LT, 64, F32, COMMIT>(k, grid, s);
+        case 128: return launch_t<LT, 128, F32, COMMIT>(k, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <bool F32, bool COMMIT>
+hipError_t by_lt(int L, int ns, const KArgs &k, unsigned grid, hipStream_t s) {
+    if (L <= 16) return by_ns<16, F32, COMMIT>(ns, k, grid, s);
+    if (L <= 32) return by_ns<32, F32, COMMIT>(ns, k, grid, s);
+    return by_ns<64, F32, COMMIT>(ns, k, grid, s);
+}
+
+}  // namespace
+
+int launch_block(const LaunchArgs &a, bool commit, void *stream) {
+    if (a.batch == 0 || a.L == 0) return BDLM_OK;
+    KArgs k;
+    k.x = a.x;
+    k.dt = a.dt;
+    k.Bm = a.Bm;
+    k.Cm = a.Cm;
+    k.A = a.A;
+    k.D = a.D;
+    k.D_rev = a.D_rev;
+    k.h_pool = a.h_pool;
+    k.y = a.y;
+    k.xs_b = a.xs_b;
+    k.xs_t = a.xs_t;
+    k.xs_h = a.xs_h;
+    k.dts_b = a.dts_b;
+    k.dts_t = a.dts_t;
+    k.bcs_b = a.bcs_b;
+    k.bcs_t = a.bcs_t;
+    k.bcs_g = a.bcs_g;
+    k.nheads = a.nheads;
+    k.heads_per_group = a.nheads / a.ngroups;
+    k.L = a.L;
+    const int64_t units = static_cast<int64_t>(a.batch) * a.nheads;
+    k.xcd_remap = (units % 8 == 0) ? 1 : 0;
+    k.use_slots = a.slots ? 1 : 0;
+    for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i) k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
+    const unsigned grid = static_cast<unsigned>(units);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (a.bf16)
+        e = commit ? by_lt<false, true>(a.L, a.dstate, k, grid, s)
+                   : by_lt<false, false>(a.L, a.dstate, k, grid, s);
+    else
+        e = commit ? by_lt<true, true>(a.L, a.dstate, k, grid, s)
+                   : by_lt<true, false>(a.L, a.dstate, k, grid, s);
+    return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+}
+
+int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
+                         bool to_pool, void *stream) {
+    const int64_t quads = nstates * kP * (dstate / 4);
+    if (quads == 0) return BDLM_OK;
+    const int64_t want = (quads + 255) / 256;
+    const unsigned grid = static_cast<unsigned>(want < 8192 ? want : 8192);
+    hipLaunchKernelGGL(bdlm_state_permute_kernel, dim3(grid), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), src, dst, nstates,
+                       static_cast<int>(dstate), to_pool ? 1 : 0);
+    return hipGetLastError() == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+}
+
+int launch_reset(float *h_pool, int64_t nslots, int64_t state_elems, const int32_t *slots,
+                 int64_t nreset, void *stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t n4 = state_elems / 4;
+    const unsigned gx = static_cast<unsigned>(n4 < 256 * 64 ? (n4 + 255) / 256 : 64);
+    const int64_t count = slots ? nreset : nslots;
+    for (int64_t done = 0; done < count; done += BDLM_MAX_SLOT_ROWS) {
+        const int64_t chunk = count - done < BDLM_MAX_SLOT_ROWS ? count - done : BDLM_MAX_SLOT_ROWS;
+        ResetArgs r;
+        r.h_pool = h_pool;
+        r.state_elems = state_elems;
+        r.first_slot = done;
+        r.use_slots = slots ? 1 : 0;
+        for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i) r.slots[i] = (slots && i < chunk) ? slots[done + i] : 0;
+        hipLaunchKernelGGL(bdlm_reset_kernel, dim3(gx > 0 ? gx : 1, static_cast<unsigned>(chunk)),
+                           dim3(256), 0, s, r);
+        if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
+    }
+    return BDLM_OK;
+}
+
+}  // namespace bdlm

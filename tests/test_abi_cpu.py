@@ -1,0 +1,189 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and every argument check returns its documented code before
+anything is enqueued.  Device pointers here are fake (aligned integers): the
+checks never dereference them, and no call in this file reaches a kernel launch.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import paper_2607_02805_amd as bd
+
+FAKE = 0x7F0000000000          # a 256-byte aligned fake device address
+H, N, P = 4, 32, 64
+
+
+@pytest.fixture(scope="module")
+def L():
+    return bd.lib()
+
+
+def desc(batch=2, H=H, N=N, G=1, L=16, dtype=bd.DTYPE_BF16):
+    d = bd.Desc()
+    assert bd.lib().bdlm_desc_init(ctypes.byref(d), batch, H, P, N, G, L, dtype) == 0
+    return d
+
+
+def ptrs(**over):
+    p = dict(x=FAKE, dt=FAKE + 0x1000, A=FAKE + 0x2000, B=FAKE + 0x3000, C=FAKE + 0x4000,
+             D=FAKE + 0x5000, Drev=FAKE + 0x6000, h=FAKE + 0x7000, y=FAKE + 0x8000)
+    p.update(over)
+    return p
+
+
+def i32p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def i64p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def check_step(L, d, p, nslots=4, slots=None):
+    return L.bdlm_check_block_step(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                   p["D"], p["Drev"], p["h"], nslots, i32p(slots), p["y"])
+
+
+def check_commit(L, d, p, nslots=4, slots=None, nc=None, nb=None, expect=-1):
+    nc = np.zeros(nslots, np.int64) if nc is None else nc
+    nb = np.zeros(nslots, np.int64) if nb is None else nb
+    return L.bdlm_check_commit(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                               p["Drev"], p["h"], nslots, i32p(slots), i64p(nc), i64p(nb), expect)
+
+
+def test_exports_every_declared_function(L):
+    names = bd.header_functions()
+    assert "bdlm_scan_block_step" in names and "bdlm_commit_boundary" in names
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in include/bdlm.h but not exported"
+    assert L.bdlm_abi_version() == 1
+
+
+def test_strerror(L):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+        assert bd.strerror(code) and bd.strerror(code) != "unknown status"
+    assert bd.strerror(12345) == "unknown status"
+
+
+def test_desc_init_contiguous_strides(L):
+    d = desc(batch=3, H=8, N=64, G=2, L=32)
+    assert list(d.x_stride) == [32 * 8 * 64, 8 * 64, 64]
+    assert list(d.dt_stride) == [32 * 8, 8]
+    assert list(d.bc_stride) == [32 * 2 * 64, 2 * 64, 64]
+    assert L.bdlm_desc_init(None, 1, 1, 64, 16, 1, 1, 0) == bd.E_NULL
+
+
+def test_valid_arguments_pass(L):
+    assert check_step(L, desc(), ptrs()) == bd.OK
+    assert check_step(L, desc(dtype=bd.DTYPE_F32), ptrs()) == bd.OK
+    assert check_commit(L, desc(), ptrs()) == bd.OK
+    for N_ in (16, 32, 64, 128):
+        for L_ in (0, 1, 17, 32, 64):
+            assert check_step(L, desc(N=N_, L=L_), ptrs()) == bd.OK
+
+
+@pytest.mark.parametrize("field", ["x", "dt", "A", "B", "C", "D", "Drev", "h", "y"])
+def test_null_pointers(L, field):
+    assert check_step(L, desc(), ptrs(**{field: None})) == bd.E_NULL
+
+
+def test_null_desc_and_meta(L):
+    p = ptrs()
+    assert L.bdlm_check_block_step(None, p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                   p["Drev"], p["h"], 4, None, p["y"]) == bd.E_NULL
+    d = desc()
+    assert L.bdlm_check_commit(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                               p["Drev"], p["h"], 4, None, None, None, -1) == bd.E_NULL
+
+
+@pytest.mark.parametrize("mut,code", [
+    (dict(headdim=32), bd.E_SHAPE), (dict(dstate=48), bd.E_SHAPE), (dict(dstate=256), bd.E_SHAPE),
+    (dict(block_len=65), bd.E_SHAPE), (dict(block_len=-1), bd.E_SHAPE),
+    (dict(nheads=6, ngroups=4), bd.E_SHAPE), (dict(ngroups=0), bd.E_SHAPE),
+    (dict(nheads=0), bd.E_SHAPE), (dict(batch=-1), bd.E_SHAPE),
+    (dict(in_dtype=7), bd.E_DTYPE), (dict(reserved=1), bd.E_DTYPE),
+])
+def test_bad_shapes_and_dtypes(L, mut, code):
+    d = desc()
+    for k, v in mut.items():
+        setattr(d, k, v)
+    assert check_step(L, d, ptrs()) == code
+
+
+def test_negative_stride(L):
+    d = desc()
+    d.x_stride[1] = -64
+    assert check_step(L, d, ptrs()) == bd.E_SHAPE
+
+
+@pytest.mark.parametrize("over,dtype", [
+    (dict(x=FAKE + 1), bd.DTYPE_BF16), (dict(x=FAKE + 8), bd.DTYPE_F32),
+    (dict(B=FAKE + 0x3004), bd.DTYPE_BF16), (dict(C=FAKE + 0x4008), bd.DTYPE_F32),
+    (dict(dt=FAKE + 0x1002), bd.DTYPE_F32), (dict(dt=FAKE + 0x1001), bd.DTYPE_BF16),
+    (dict(h=FAKE + 0x7008), bd.DTYPE_BF16), (dict(A=FAKE + 0x2002), bd.DTYPE_BF16),
+    (dict(y=FAKE + 0x8002), bd.DTYPE_BF16),
+])
+def test_misaligned(L, over, dtype):
+    assert check_step(L, desc(dtype=dtype), ptrs(**over)) == bd.E_ALIGN
+
+
+@pytest.mark.parametrize("which,i,v,dtype", [
+    ("bc", 1, 36, bd.DTYPE_BF16), ("bc", 0, 1028, bd.DTYPE_BF16), ("bc", 2, 6, bd.DTYPE_F32),
+    ("x", 1, 260, bd.DTYPE_BF16), ("x", 2, 66, bd.DTYPE_F32), ("x", 0, 2052, bd.DTYPE_BF16)])
+def test_stride_alignment(L, which, i, v, dtype):
+    d = desc(dtype=dtype)
+    getattr(d, f"{which}_stride")[i] = v     # not a whole number of 16-byte units
+    assert check_step(L, d, ptrs()) == bd.E_ALIGN
+    getattr(d, f"{which}_stride")[i] = v + (16 // (2 if dtype == bd.DTYPE_BF16 else 4)) - \
+        v % (16 // (2 if dtype == bd.DTYPE_BF16 else 4))
+    assert check_step(L, d, ptrs()) == bd.OK
+
+
+def test_slots(L):
+    d = desc(batch=3)
+    assert check_step(L, d, ptrs(), nslots=4, slots=np.array([3, 0, 3], np.int32)) == bd.OK
+    assert check_step(L, d, ptrs(), nslots=4, slots=np.array([4, 0, 1], np.int32)) == bd.E_SLOT
+    assert check_step(L, d, ptrs(), nslots=4, slots=np.array([-1, 0, 1], np.int32)) == bd.E_SLOT
+    assert check_step(L, d, ptrs(), nslots=2) == bd.E_SLOT        # identity needs batch <= nslots
+    assert check_step(L, d, ptrs(), nslots=0) == bd.E_SHAPE
+    big = desc(batch=bd.MAX_SLOT_ROWS + 1)
+    slots = np.zeros(bd.MAX_SLOT_ROWS + 1, np.int32)
+    assert check_step(L, big, ptrs(), nslots=4, slots=slots) == bd.E_SHAPE
+    # repeated slots are fine for a step, not for a commit
+    assert check_commit(L, d, ptrs(), slots=np.array([3, 0, 3], np.int32)) == bd.E_SLOT
+    assert check_commit(L, d, ptrs(), slots=np.array([3, 0, 1], np.int32)) == bd.OK
+
+
+def test_commit_offsets(L):
+    d = desc(batch=2)
+    nb = np.array([5, 5, 4, 5], np.int64)
+    nc = nb * 16
+    assert check_commit(L, d, ptrs(), nc=nc, nb=nb, expect=5) == bd.OK
+    assert check_commit(L, d, ptrs(), nc=nc, nb=nb, expect=4) == bd.E_OFFSET
+    assert check_commit(L, d, ptrs(), slots=np.array([2, 3], np.int32), nc=nc, nb=nb,
+                        expect=5) == bd.E_OFFSET
+    assert check_commit(L, d, ptrs(), slots=np.array([2, 3], np.int32), nc=nc, nb=nb,
+                        expect=-1) == bd.OK
+
+
+def test_entry_points_reject_before_launch(L):
+    """The enqueueing entry points run the same checks first (no GPU is touched)."""
+    d = desc()
+    p = ptrs(x=None)
+    assert L.bdlm_scan_block_step(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                  p["D"], p["Drev"], p["h"], 4, None, p["y"], None) == bd.E_NULL
+    nc, nb = np.zeros(4, np.int64), np.array([1, 1, 1, 1], np.int64)
+    p = ptrs()
+    rc = L.bdlm_commit_boundary(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                p["Drev"], p["h"], 4, None, i64p(nc), i64p(nb), 0, None, None)
+    assert rc == bd.E_OFFSET
+    assert nb.tolist() == [1, 1, 1, 1] and nc.tolist() == [0, 0, 0, 0]   # untouched
+    rc = L.bdlm_commit_boundary(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                p["Drev"], p["h"], 4, None, i64p(nc), i64p(nb), 1, FAKE + 1, None)
+    assert rc == bd.E_ALIGN
+    assert L.bdlm_cache_reset(None, 4, 1024, None, 0, None, None, None) == bd.E_NULL
+    assert L.bdlm_cache_reset(FAKE, 4, 1022, None, 0, None, None, None) == bd.E_SHAPE
+    assert L.bdlm_cache_reset(FAKE + 8, 4, 1024, None, 0, None, None, None) == bd.E_ALIGN
+    bad = np.array([4], np.int32)
+    assert L.bdlm_cache_reset(FAKE, 4, 1024, i32p(bad), 1, None, None, None) == bd.E_SLOT
