@@ -229,6 +229,19 @@ def cpu_baseline(args, budget_s: float):
                       f"{el:.1f} s, fp64"}
 
 
+def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
+    """A plain device-to-device copy of known size, for scaling HBM counters (FETCH_SIZE,
+    WRITE_SIZE) of profiled kernels to bytes."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda:0").uniform_()
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,7 +253,12 @@ def main():
     ap.add_argument("--prefix", type=int, default=262144, help="committed prefix tokens")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds for the oracle leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 256 MiB device copy (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the block step and the commit shard over "

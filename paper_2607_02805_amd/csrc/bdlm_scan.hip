@@ -61,7 +61,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kP = BDLM_HEADDIM;  // 64 head-dim columns per head
-constexpr int kThreads = 256;     // 4 waves x 16 columns
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct KArgs {
@@ -85,15 +84,29 @@ __device__ __forceinline__ short bf16_bits(float v) {
 __device__ __forceinline__ float bf16_to_f32(short s) {
     return __uint_as_float(static_cast<uint32_t>(static_cast<uint16_t>(s)) << 16);
 }
-// v = hi + lo + O(2^-16 |v|)
-__device__ __forceinline__ void split4(f32x4 v, s16x4 &hi, s16x4 &lo) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const short hb = bf16_bits(v[k]);
-        hi[k] = hb;
-        lo[k] = bf16_bits(v[k] - bf16_to_f32(hb));
-    }
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats to two bf16 (round to nearest even), a in the low half, b in the high
+// half: a two-wide conversion compiles to one packed v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
+
+// v = hi + lo + O(2^-16 |v|), both parts rounded to nearest even
+__device__ __forceinline__ void split4(f32x4 v, s16x4 &hi, s16x4 &lo) {
+    const uint32_t h01 = cvt_pk_bf16(v[0], v[1]), h23 = cvt_pk_bf16(v[2], v[3]);
+    const float r0 = v[0] - __uint_as_float(h01 << 16);
+    const float r1 = v[1] - __uint_as_float(h01 & 0xffff0000u);
+    const float r2 = v[2] - __uint_as_float(h23 << 16);
+    const float r3 = v[3] - __uint_as_float(h23 & 0xffff0000u);
+    hi = __builtin_bit_cast(s16x4, uint2{h01, h23});
+    lo = __builtin_bit_cast(s16x4, uint2{cvt_pk_bf16(r0, r1), cvt_pk_bf16(r2, r3)});
+}
+
+// Materialise v here: later code depends on this point, so the compiler can neither
+// sink the computation of v below it nor hoist its uses above it.
+__device__ __forceinline__ void pin(float &v) { asm volatile("" : "+v"(v)); }
 
 // Activation storage.
 template <bool F32> struct Act;
@@ -161,26 +174,37 @@ __device__ __forceinline__ int img_idx(int mt, int q, int grp, int col) {
 // LT: block tile (16, 32 or 64 tokens; the block length L <= LT, padded tokens
 //     have dt = 0, x = B = C = 0, which changes no output and no state).
 // NS: dstate.  F32: fp32 activation storage.  COMMIT: also update the state.
+// NPART: the state of a head is split over NPART groups of four waves along
+//     dstate (4 * NPART waves per workgroup).  Streaming the state from HBM needs
+//     many waves per CU, each with few loads in flight; the partial prefix
+//     products of the groups are summed through LDS before y is stored.
 //
 // Phases:
 //   0. every global load is issued up front and unconditionally (rows past the
-//      block are clamped to a valid row and zeroed after the load): B, C, x and
-//      dt in coalesced 16-byte chunks by the whole workgroup, then the state,
-//      16 bytes per quad, into registers;
+//      block read a zero chunk): B, C, x, dt and the per-head parameters in
+//      coalesced 16-byte chunks by the whole workgroup, then this wave's share of
+//      the state, 16 bytes per quad, into registers;
 //   1. B and C are written to LDS as "register images" (the exact per-lane quads
 //      an MFMA operand needs, so reading one is a linear, conflict-free 8-byte
 //      read), x row-major, dt as floats;
-//   2. each wave runs the decay prefix sums of the block (lane t = token t) and
-//      computes its share of the Gram tiles, turns them into the decay-weighted
-//      matrix M[t,j] = G[t,j] W[t,j] dt_j, splits it and publishes it in LDS;
-//   3. each wave contracts M with x (its 16 columns), C with its 16 rows of the
-//      state (the only step that waits for the state loads), adds the skip
-//      term and stores y; a commit then adds the block to the state in place.
-template <int LT, int NS, bool F32, bool COMMIT>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+//   2. each wave runs the decay prefix sums of the block (lane t = token t);
+//      the Gram tiles are shared out over the waves, turned into the
+//      decay-weighted matrix M[t,j] = G[t,j] W[t,j] dt_j, split and published in
+//      LDS;
+//   3. the first group contracts M with x (its 16 columns) and precomputes the
+//      skip term and the prefix scales; every wave contracts C with its rows and
+//      dstate quads of the state (the only step that waits for the state loads);
+//      the partial products are summed and y is stored; a commit then adds the
+//      block to each wave's quads of the state in place.
+template <int LT, int NS, bool F32, bool COMMIT, int NPART>
+__global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
+    constexpr int NT = 256 * NPART;       // threads
+    constexpr int NW = 4 * NPART;         // waves
     constexpr int MT = LT / 16;           // token tiles = quads along the block
     constexpr int QN = NS / 16;           // quads along dstate
+    constexpr int QW = QN / NPART;        // dstate quads per wave
+    static_assert(QN % NPART == 0 && QW >= 1, "dstate split");
     constexpr int IMG = MT * QN * 64;     // quads in one image of B or C
     constexpr int E = F32 ? 4 : 8;        // activations per 16-byte chunk
     constexpr int XS = kP + 4;            // x row stride in LDS (elements)
@@ -190,12 +214,13 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) uint2 sCl[F32 ? IMG : 1], sBl[F32 ? IMG : 1];  // lo, fp32 input
     __shared__ __align__(16) AT sX[LT * XS];
     __shared__ __align__(16) float sDt[64];
+    __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
-    constexpr int YS = kP + 4;                                         // y row stride
-    __shared__ __align__(16) float sY[LT * YS];                       // y tile for stores
+    __shared__ __align__(16) f32x4 sRed[(NPART > 1 ? NPART - 1 : 1) * 4 * MT * 64];
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int pblk = wave & 3, part = wave >> 2;   // 16 head-dim columns, dstate share
     const int col = lane & 15, grp = lane >> 4;
 
     // Unit (b, h).  Workgroups are dealt to the 8 XCDs round-robin; remapping
@@ -208,7 +233,8 @@ bdlm_block_kernel(const KArgs args) {
     const int g = h / args.heads_per_group;
     const int64_t slot = args.use_slots ? args.slots[b] : b;
     const int L = args.L;                 // 1 <= L <= LT
-    const int p = wave * 16 + col;
+    const int p = pblk * 16 + col;
+    const int q0 = part * QW;             // first dstate quad of this wave
 
     const AT *xg = static_cast<const AT *>(args.x) + b * args.xs_b + h * args.xs_h;
     const AT *dtg = static_cast<const AT *>(args.dt) + b * args.dts_b + h;
@@ -220,39 +246,60 @@ bdlm_block_kernel(const KArgs args) {
     // ---- phase 0: loads
     constexpr int CPR = NS / E;                           // 16-byte chunks per row
     constexpr int BC_CH = LT * CPR;                       // chunks per matrix
-    constexpr int BC_PT = BC_CH >= kThreads ? BC_CH / kThreads : 1;
+    // Chunk counts are multiples of 64 (or below 64, then one partial wave loads
+    // them), so "this thread owns chunk i" is decided per wave.
+    constexpr int BC_PT = BC_CH >= NT ? BC_CH / NT : 1;
+    const bool bc_owner = tid < BC_CH;
     u32x4 cch[BC_PT], bch[BC_PT];
+    if (bc_owner) {
 #pragma unroll
-    for (int k = 0; k < BC_PT; ++k) {
-        const int i = (tid + kThreads * k) % BC_CH;        // chunk fastest (coalesced)
-        const int t = i / CPR, c = i % CPR;
-        const int64_t o = t * args.bcs_t + c * E;
-        const bool ok = t < L;
-        cch[k] = *(ok ? gchunk(Cg + o) : gzero());
-        bch[k] = *(ok ? gchunk(Bg + o) : gzero());
+        for (int k = 0; k < BC_PT; ++k) {
+            const int i = tid + NT * k;                    // chunk fastest (coalesced)
+            const int t = i / CPR, c = i % CPR;
+            const int64_t o = t * args.bcs_t + c * E;
+            const bool ok = t < L;
+            cch[k] = *(ok ? gchunk(Cg + o) : gzero());
+            bch[k] = *(ok ? gchunk(Bg + o) : gzero());
+        }
     }
     constexpr int X_CH = LT * (kP / E);
-    constexpr int X_PT = X_CH >= kThreads ? X_CH / kThreads : 1;
+    constexpr int X_PT = X_CH >= NT ? X_CH / NT : 1;
+    const bool x_owner = tid < X_CH;
     u32x4 xch[X_PT];
+    if (x_owner) {
 #pragma unroll
-    for (int k = 0; k < X_PT; ++k) {
-        const int i = (tid + kThreads * k) % X_CH;         // chunk fastest (coalesced)
-        const int j = i / (kP / E), c = i % (kP / E);
-        xch[k] = *(j < L ? gchunk(xg + j * args.xs_t + c * E) : gzero());
+        for (int k = 0; k < X_PT; ++k) {
+            const int i = tid + NT * k;                    // chunk fastest (coalesced)
+            const int j = i / (kP / E), c = i % (kP / E);
+            xch[k] = *(j < L ? gchunk(xg + j * args.xs_t + c * E) : gzero());
+        }
     }
     typedef __attribute__((address_space(1))) const AT g_at;
-    const AT dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
-                                : (const g_at *)(&kZeroChunk));
+    AT dtraw = AT(0);
+    if (wave == 0)
+        dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
+                           : (const g_at *)(&kZeroChunk));
+    // per-head parameters as vector loads in this first batch: a scalar load issued
+    // later would queue behind the state loads of every workgroup
+    typedef __attribute__((address_space(1))) const float g_f;
+    float parv = 0.f;
+    if (wave == 0) {
+        const float *par = tid == 0 ? args.A : (tid == 1 ? args.D : args.D_rev);
+        parv = *(const g_f *)(par + h);
+    }
     // keep the small loads above ahead of the state loads (loads return in order)
     __builtin_amdgcn_sched_barrier(0);
-    f32x4 hq[QN];  // state s[p, 16q + 4grp + r]
+    f32x4 hq[QW];  // state s[p, 16(q0 + k) + 4grp + r]
 #pragma unroll
-    for (int q = 0; q < QN; ++q) hq[q] = *reinterpret_cast<const f32x4 *>(hs + q * 16 * kP);
+    for (int k = 0; k < QW; ++k)  // read once per step: stream past the caches
+        hq[k] = __builtin_nontemporal_load(
+            reinterpret_cast<const f32x4 *>(hs + (q0 + k) * 16 * kP));
 
     // ---- phase 1: LDS images
 #pragma unroll
     for (int k = 0; k < BC_PT; ++k) {
-        const int i = (tid + kThreads * k) % BC_CH;
+        if (!bc_owner) break;
+        const int i = tid + NT * k;
         const int t = i / CPR, c = i % CPR;
         const u32x4 cz = cch[k], bz = bch[k];
         if constexpr (F32) {
@@ -276,7 +323,8 @@ bdlm_block_kernel(const KArgs args) {
     }
 #pragma unroll
     for (int k = 0; k < X_PT; ++k) {
-        const int i = (tid + kThreads * k) % X_CH;
+        if (!x_owner) break;
+        const int i = tid + NT * k;
         const int j = i / (kP / E), c = i % (kP / E);
         const u32x4 v = xch[k];
         uint2 *dst = reinterpret_cast<uint2 *>(&sX[j * XS + c * E]);
@@ -284,11 +332,12 @@ bdlm_block_kernel(const KArgs args) {
         dst[1] = uint2{v.z, v.w};
     }
     if (tid < 64) sDt[tid] = Act<F32>::val(dtraw);
+    if (tid < 3) sPar[tid] = parv;
     __syncthreads();
 
-    // ---- phase 2: decay prefix sums (every wave), Gram tiles (split over waves)
+    // ---- phase 2: decay prefix sums (every wave), Gram tiles (shared out)
     const float dtv = sDt[lane];
-    const float A2 = args.A[h] * kLog2e;  // work in base 2
+    const float A2 = sPar[0] * kLog2e;    // work in base 2
     const float l2 = dtv * A2;
     float cs = l2;
 #pragma unroll
@@ -299,26 +348,32 @@ bdlm_block_kernel(const KArgs args) {
     float ex = __shfl_up(cs, 1, 64);
     if (lane == 0) ex = 0.f;
 
-    for (int tile = wave; tile < MT * MT; tile += 4) {
+    for (int tile = wave; tile < MT * MT; tile += NW) {
         const int mt = tile / MT, jt = tile % MT;
         // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
         f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
-        s16x4 bq[QN], cq[QN];
 #pragma unroll
-        for (int q = 0; q < QN; ++q) {
-            bq[q] = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
-            cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-        }
-        gacc = mma_quads<QN>(bq, cq, gacc);
-        if constexpr (F32) {
-            s16x4 bl[QN], cl[QN];
-#pragma unroll
-            for (int q = 0; q < QN; ++q) {
-                bl[q] = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
-                cl[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+        for (int q = 0; q < QN; q += 2) {   // two dstate quads per product
+            const int q1 = q + 1 < QN ? q + 1 : q;
+            const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
+            const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
+            const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+            const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
+            if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
+            else gacc = mma_k16(b0, c0, gacc);
+            if constexpr (F32) {
+                const s16x4 bl0 = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
+                const s16x4 bl1 = as_s16x4(sBl[img_idx<QN, F32>(jt, q1, grp, col)]);
+                const s16x4 cl0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                const s16x4 cl1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q1, grp, col)]);
+                if (q + 1 < QN) {
+                    gacc = mma_k32(b0, b1, cl0, cl1, gacc);
+                    gacc = mma_k32(bl0, bl1, c0, c1, gacc);
+                } else {
+                    gacc = mma_k16(b0, cl0, gacc);
+                    gacc = mma_k16(bl0, c0, gacc);
+                }
             }
-            gacc = mma_quads<QN>(bq, cl, gacc);
-            gacc = mma_quads<QN>(bl, cq, gacc);
         }
         const int t = 16 * mt + col;
         const float cst = shfl(cs, t), ext = shfl(ex, t);
@@ -354,70 +409,113 @@ bdlm_block_kernel(const KArgs args) {
     float *yb = args.y;
     const bool want_y = !COMMIT || yb != nullptr;
     if (want_y) {
-        const float skip = args.D[h] + args.D_rev[h];
-        f32x4 ai[MT], ap[MT];
+        // first group: intra-block product, skip term and prefix scales, all before
+        // waiting for the state
+        float pre[MT][4], es[MT][4];
+        if (part == 0) {
+            const float skip = sPar[1] + sPar[2];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            s16x4 mh[MT], ml[MT];
+            for (int mt = 0; mt < MT; ++mt) {
+                s16x4 mh[MT], ml[MT];
 #pragma unroll
-            for (int jt = 0; jt < MT; ++jt) {
-                const uint4 v = sM[(mt * MT + jt) * 64 + lane];
-                mh[jt] = as_s16x4(uint2{v.x, v.y});
-                ml[jt] = as_s16x4(uint2{v.z, v.w});
-            }
-            ai[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            ai[mt] = mma_quads<MT>(mh, xq, ai[mt]);
-            ai[mt] = mma_quads<MT>(ml, xq, ai[mt]);
-            if constexpr (F32) ai[mt] = mma_quads<MT>(mh, xl, ai[mt]);
-        }
-        // prefix term: C (rows t) against the state (columns p); waits for the state
-        s16x4 hh[QN], hl[QN];
+                for (int jt = 0; jt < MT; ++jt) {
+                    const uint4 v = sM[(mt * MT + jt) * 64 + lane];
+                    mh[jt] = as_s16x4(uint2{v.x, v.y});
+                    ml[jt] = as_s16x4(uint2{v.z, v.w});
+                }
+                f32x4 ai = {0.f, 0.f, 0.f, 0.f};
+                ai = mma_quads<MT>(mh, xq, ai);
+                ai = mma_quads<MT>(ml, xq, ai);
+                if constexpr (F32) ai = mma_quads<MT>(mh, xl, ai);
 #pragma unroll
-        for (int q = 0; q < QN; ++q) split4(hq[q], hh[q], hl[q]);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            s16x4 cq[QN];
-#pragma unroll
-            for (int q = 0; q < QN; ++q) cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-            ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            ap[mt] = mma_quads<QN>(cq, hh, ap[mt]);
-            ap[mt] = mma_quads<QN>(cq, hl, ap[mt]);
-            if constexpr (F32) {
-                s16x4 cl[QN];
-#pragma unroll
-                for (int q = 0; q < QN; ++q)
-                    cl[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                ap[mt] = mma_quads<QN>(cl, hh, ap[mt]);
+                for (int r = 0; r < 4; ++r) {
+                    pre[mt][r] = ai[r] + skip * xv[mt][r];
+                    es[mt][r] = exp2f(shfl(cs, 16 * mt + 4 * grp + r));
+                    pin(pre[mt][r]);
+                    pin(es[mt][r]);
+                }
             }
         }
-        // y tile through LDS, then whole 256-byte rows out with 16-byte stores
+        // C quads of this wave's dstate share, before the state wait
+        s16x4 cq[MT][QW], cl[MT][F32 ? QW : 1];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int t = 16 * mt + 4 * grp + r;
-                const float e = exp2f(shfl(cs, t));
-                sY[t * YS + p] = e * ap[mt][r] + ai[mt][r] + skip * xv[mt][r];
+            for (int k = 0; k < QW; ++k) {
+                cq[mt][k] = as_s16x4(sC[img_idx<QN, F32>(mt, q0 + k, grp, col)]);
+                if constexpr (F32) cl[mt][k] = as_s16x4(sCl[img_idx<QN, F32>(mt, q0 + k, grp, col)]);
+            }
+        __builtin_amdgcn_sched_barrier(0);   // keep the above ahead of the state wait
+
+        // partial prefix term: C (rows t) against this wave's state quads (columns
+        // p), a pair of quads at a time as the loads return
+        f32x4 ap[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < QW; k += 2) {
+            if (k + 1 < QW) {
+                s16x4 h0, l0, h1, l1;
+                split4(hq[k], h0, l0);
+                split4(hq[k + 1], h1, l1);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], h0, h1, ap[mt]);
+                    ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], l0, l1, ap[mt]);
+                    if constexpr (F32) ap[mt] = mma_k32(cl[mt][k], cl[mt][k + 1], h0, h1, ap[mt]);
+                }
+            } else {
+                s16x4 h0, l0;
+                split4(hq[k], h0, l0);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    ap[mt] = mma_k16(cq[mt][k], h0, ap[mt]);
+                    ap[mt] = mma_k16(cq[mt][k], l0, ap[mt]);
+                    if constexpr (F32) ap[mt] = mma_k16(cl[mt][k], h0, ap[mt]);
+                }
             }
         }
-        __syncthreads();
-        constexpr int Y_CH = LT * (kP / 4);
+        if constexpr (NPART > 1) {
+            if (part > 0)
 #pragma unroll
-        for (int k = 0; k < (Y_CH + kThreads - 1) / kThreads; ++k) {
-            const int i = tid + kThreads * k;
-            const int t = i >> 4, c = i & 15;
-            if (i < Y_CH && t < L)
-                *reinterpret_cast<f32x4 *>(
-                    yb + ((static_cast<int64_t>(b) * L + t) * args.nheads + h) * kP + 4 * c) =
-                    *reinterpret_cast<const f32x4 *>(&sY[t * YS + 4 * c]);
+                for (int mt = 0; mt < MT; ++mt)
+                    sRed[(((part - 1) * 4 + pblk) * MT + mt) * 64 + lane] = ap[mt];
+            __syncthreads();
+            if (part == 0)
+#pragma unroll
+                for (int pt = 1; pt < NPART; ++pt)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+                        ap[mt] += sRed[(((pt - 1) * 4 + pblk) * MT + mt) * 64 + lane];
+        }
+        if (part == 0) {
+            // y straight from the accumulators: lanes of a group write 64 contiguous bytes
+            float *yrow = yb + ((static_cast<int64_t>(b) * L + 4 * grp) * args.nheads + h) * kP + p;
+            const int ytok = args.nheads * kP;           // elements between consecutive tokens
+            if (L == LT) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        __builtin_nontemporal_store(es[mt][r] * ap[mt][r] + pre[mt][r],
+                                                    yrow + (16 * mt + r) * ytok);
+            } else {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (16 * mt + 4 * grp + r < L)
+                            __builtin_nontemporal_store(es[mt][r] * ap[mt][r] + pre[mt][r],
+                                                        yrow + (16 * mt + r) * ytok);
+            }
         }
     }
 
     if constexpr (COMMIT) {
         // s_new[p, n] = exp(cs_last) s[p, n] + sum_j x[j, p] exp(cs_last - cs_j) dt_j B[j, n]
-        // A operand: lane (col, grp) holds the weighted B[16jt + 4grp + r, 16q + col],
-        // read from the B image (element (j, n) sits in the quad of tile j/16, quad
-        // n/16, group n%16/4, column j%16, at slot n%4).
+        // on this wave's dstate quads.  A operand: lane (col, grp) holds the weighted
+        // B[16jt + 4grp + r, 16q + col], read from the B image (element (j, n) sits in
+        // the quad of tile j/16, quad n/16, group n%16/4, column j%16, at slot n%4).
         const float cl2 = shfl(cs, 63);  // cs of the last real token (padding adds 0)
         const float keep = exp2f(cl2);
         float wj[MT][4];
@@ -431,7 +529,8 @@ bdlm_block_kernel(const KArgs args) {
         const uint16_t *sBh = reinterpret_cast<const uint16_t *>(sB);
         const uint16_t *sBlo = reinterpret_cast<const uint16_t *>(sBl);
 #pragma unroll
-        for (int q = 0; q < QN; ++q) {
+        for (int k = 0; k < QW; ++k) {
+            const int q = q0 + k;
             s16x4 th[MT], tl[MT];
 #pragma unroll
             for (int jt = 0; jt < MT; ++jt) {
@@ -445,11 +544,11 @@ bdlm_block_kernel(const KArgs args) {
                 }
                 split4(v, th[jt], tl[jt]);
             }
-            f32x4 acc = hq[q] * keep;
+            f32x4 acc = hq[k] * keep;
             acc = mma_quads<MT>(th, xq, acc);
             acc = mma_quads<MT>(tl, xq, acc);
             if constexpr (F32) acc = mma_quads<MT>(th, xl, acc);
-            *reinterpret_cast<f32x4 *>(hs + q * 16 * kP) = acc;
+            __builtin_nontemporal_store(acc, reinterpret_cast<f32x4 *>(hs + q * 16 * kP));
         }
     }
 }
@@ -492,9 +591,19 @@ bdlm_state_permute_kernel(const float *src, float *dst, int64_t nstates, int dst
     }
 }
 
+// Wave groups per head along dstate.  Measured on MI355X at the 350M layer shape
+// (batch 16, 32 heads, dstate 128, L = 32): two groups (8 waves) stream the
+// state slightly faster than one; four groups are slower (1024-thread workgroups
+// launch more slowly and the reduction barrier lands on the critical path).
+template <int LT, int NS>
+constexpr int nparts() {
+    return (NS / 16) % 2 == 0 ? 2 : 1;
+}
+
 template <int LT, int NS, bool F32, bool COMMIT>
 hipError_t launch_t(const KArgs &k, unsigned grid, hipStream_t s) {
-    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT>), dim3(grid), dim3(kThreads), 0,
+    constexpr int NP = nparts<LT, NS>();
+    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT, NP>), dim3(grid), dim3(256 * NP), 0,
                        s, k);
     return hipGetLastError();
 }
