@@ -36,6 +36,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_02805_amd", "csrc", "bdlm_scan.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_block_step_350m_b16_L32.md")
+STEP_KERNEL = "bdlm_block_kernel<32, 128, false, false"
+COMMIT_KERNEL = "bdlm_block_kernel<32, 128, false, true"
 
 
 def step_bytes(batch, H, P, N, G, L, in_bytes=2):
@@ -229,6 +233,76 @@ def cpu_baseline(args, budget_s: float):
                       f"{el:.1f} s, fp64"}
 
 
+def kernel_source_sha() -> str:
+    import hashlib
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per step launch from the committed counter summary, or None when the
+    kernel source changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            kv[k.strip()] = v.strip().strip("`")
+    if kv.get("kernel_source_sha256_16") != kernel_source_sha():
+        return None
+    try:
+        return int(kv["step_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _csv_rows(path):
+    import csv
+    return list(csv.DictReader(open(path)))
+
+
+def summarize_trace(stats_csv: str) -> str:
+    """Markdown table of a rocprofv3 --kernel-trace --stats kernel_stats.csv."""
+    out = ["| kernel | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    for r in _csv_rows(stats_csv):
+        name = r["Name"].replace("bdlm::(anonymous namespace)::", "").split("(")[0]
+        out.append(f"| `{name[:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.3f} | "
+                   f"{float(r['MinNs']) / 1e3:.3f} | {float(r['MaxNs']) / 1e3:.3f} | "
+                   f"{float(r['Percentage']):.1f} |")
+    return "\n".join(out)
+
+
+def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
+                      copy_bytes=256 << 20) -> dict:
+    """Per-launch HBM bytes of the step and commit kernels from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch), each scaled by the same counter's reading for a plain copy of
+    known size."""
+    import statistics as st
+
+    def per_kernel(path, counter):
+        d = {}
+        for r in _csv_rows(path):
+            if r["Counter_Name"] == counter:
+                d.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return d
+
+    def copy_kib(path, counter):
+        vals = [v for k, vs in per_kernel(path, counter).items() if "copyBuffer" in k for v in vs]
+        return st.median(vals)
+
+    f_scale = copy_bytes / 1024 / copy_kib(copy_fetch_csv, "FETCH_SIZE")
+    w_scale = copy_bytes / 1024 / copy_kib(copy_write_csv, "WRITE_SIZE")
+    res = {"fetch_scale": f_scale, "write_scale": w_scale}
+    for tag, key in (("step", STEP_KERNEL), ("commit", COMMIT_KERNEL)):
+        fk = [v for k, vs in per_kernel(fetch_csv, "FETCH_SIZE").items() if key in k for v in vs]
+        wk = [v for k, vs in per_kernel(write_csv, "WRITE_SIZE").items() if key in k for v in vs]
+        res[tag] = {"fetch_kib_median": st.median(fk), "write_kib_median": st.median(wk),
+                    "dispatches": len(fk),
+                    "fetch_bytes": int(st.median(fk) * 1024 * f_scale),
+                    "write_bytes": int(st.median(wk) * 1024 * w_scale)}
+    return res
+
+
 def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
     """A plain device-to-device copy of known size, for scaling HBM counters (FETCH_SIZE,
     WRITE_SIZE) of profiled kernels to bytes."""
@@ -255,9 +329,24 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (counter calibration) and exit")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
+                    help="print a markdown summary of a rocprofv3 kernel_stats.csv and exit")
+    ap.add_argument("--summarize-traffic", nargs=4,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_traffic:
+        r = summarize_traffic(*args.summarize_traffic)
+        r["kernel_source_sha256_16"] = kernel_source_sha()
+        r["step_alg_bytes"] = step_bytes(16, 32, 64, 128, 1, 32)
+        r["commit_alg_bytes"] = commit_bytes(16, 32, 64, 128, 1, 32)
+        print(json.dumps(r, indent=1))
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -301,7 +390,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(r["achieved_gbs"] / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if args.block_len == 32 else None,
             "bytes_per_launch": r["step_bytes"],
         },
         "cpu_baseline": cpu,
