@@ -61,9 +61,11 @@ WORKLOADS = {
 
 
 def to_bf16_bits(a: np.ndarray) -> np.ndarray:
-    """fp32 -> bf16 bit patterns (uint16), round to nearest, ties to even."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    """fp32 -> bf16 bit patterns (uint16), round to nearest, ties to even.  Finite inputs
+    only (the largest finite pattern plus the rounding increment still fits 32 bits)."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return (r >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_bits_to_f32(a: np.ndarray) -> np.ndarray:
@@ -96,6 +98,30 @@ def tokens(w: Workload, ntok: int, seed: int, batch: int | None = None) -> dict:
     out = {"x": x, "dt": dt, "B": Bm, "C": Cm}
     if w.bf16:
         out = {k: to_bf16_bits(v) for k, v in out.items()}
+    return out
+
+
+def tokens_device(w: Workload, ntok: int, seed: int, device="cuda:0",
+                  batch: int | None = None) -> dict:
+    """Like :func:`tokens`, drawn on the GPU with torch's seeded generator (for sizes too
+    large to draw on the host in reasonable time, e.g. a 65,536-token window).  Same
+    distributions; a different generator, so not the same numbers as :func:`tokens`.
+    Returns torch tensors (bfloat16 or float32) on ``device``."""
+    import torch
+    bsz = w.batch if batch is None else batch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f32 = torch.float32
+    x = torch.randn((bsz, ntok, w.nheads, w.headdim), generator=g, device=device, dtype=f32)
+    z = torch.randn((bsz, ntok, w.nheads), generator=g, device=device, dtype=f32).double()
+    dt = torch.log1p(torch.exp(0.5 * z - 4.6)).float()
+    scale = 1.0 / math.sqrt(w.dstate)
+    Bm = torch.randn((bsz, ntok, w.ngroups, w.dstate), generator=g, device=device, dtype=f32)
+    Cm = torch.randn((bsz, ntok, w.ngroups, w.dstate), generator=g, device=device, dtype=f32)
+    Bm, Cm = Bm * scale, Cm * scale
+    out = {"x": x, "dt": dt, "B": Bm, "C": Cm}
+    if w.bf16:
+        out = {k: v.to(torch.bfloat16) for k, v in out.items()}   # round to nearest even
     return out
 
 

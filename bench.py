@@ -36,7 +36,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_02805_amd", "csrc", "bdlm_scan.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_02805_amd", "csrc", f)
+               for f in ("bdlm_scan.hip", "bdlm_device.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_block_step_350m_b16_L32.md")
 STEP_KERNEL = "bdlm_block_kernel<32, 128, false, false"
 COMMIT_KERNEL = "bdlm_block_kernel<32, 128, false, true"
@@ -234,8 +235,12 @@ def cpu_baseline(args, budget_s: float):
 
 
 def kernel_source_sha() -> str:
+    """Hash of the sources the block-step kernel is compiled from."""
     import hashlib
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():

@@ -31,7 +31,9 @@
  *     error nothing is enqueued and nothing is modified.  The return value is
  *     BDLM_OK or a negative BDLM_E_* code.  No entry point aborts.
  *   - Sizes: headdim P == 64; dstate N in {16, 32, 64, 128}; block_len L in
- *     [0, 64]; nheads % ngroups == 0; batch >= 0.
+ *     [0, 64] (the sequence entry points: up to BDLM_MAX_SEQ_LEN); nheads % ngroups
+ *     == 0; batch >= 0; batch * nheads <= 2^22 (one or two workgroups per
+ *     (row, head), within the 32-bit grid of a launch).
  *   - Activation storage (x, dt, B, C) is fp32 or bf16 (desc.in_dtype).  All
  *     arithmetic, states and outputs are fp32.
  */
@@ -47,6 +49,8 @@ extern "C" {
 #define BDLM_ABI_VERSION 1
 #define BDLM_HEADDIM 64
 #define BDLM_MAX_BLOCK_LEN 64
+/* Longest sequence of bdlm_scan_full_window and bdlm_prefill. */
+#define BDLM_MAX_SEQ_LEN (((int64_t)1 << 31) - 1)
 /* Largest batch for which an explicit slot_idx may be given (it is passed to
    the kernels by value). */
 #define BDLM_MAX_SLOT_ROWS 256
@@ -157,6 +161,45 @@ int bdlm_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
                          int64_t expected_block_index, float *y_clean, void *stream);
 
 /*
+ * Full-window bidirectional scan, with no cache: the full-sequence
+ * (DiffuMamba-style) scan that the paper's block-restricted scan replaces
+ * (Sec. 4; Sec. 5.1).
+ *
+ *   y = forward scan over all desc.block_len tokens from a zero state (skip D)
+ *     + reverse scan over all desc.block_len tokens from a zero state (skip D_rev)
+ *
+ * desc.block_len is the window length, 0 .. BDLM_MAX_SEQ_LEN; every other argument
+ * is as for bdlm_scan_block_step with block_len set to the window (y is
+ * [batch][window][nheads][64] fp32, 4-byte aligned).  Two passes over the window in
+ * 64-token chunks, the state carried in registers; y is written by the forward pass
+ * and updated by the reverse pass.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE, BDLM_E_ALIGN, BDLM_E_LAUNCH.
+ */
+int bdlm_scan_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
+                          const float *A, const void *B, const void *C, const float *D,
+                          const float *D_rev, float *y, void *stream);
+
+/*
+ * Chunked prefix prefill: summarise a clean prefix of desc.block_len tokens (any
+ * length up to BDLM_MAX_SEQ_LEN) into the cached forward boundary states
+ * (Eq. boundary-state), continuing each row's state in place.  Equivalent to
+ * committing the prefix block by block, in one launch.
+ * h_pool, slot_idx  as for bdlm_commit_boundary (slots distinct).
+ * n_committed, n_blocks  host bookkeeping: every slot must hold
+ *              expected_block_index blocks (negative: unchecked); on success
+ *              n_committed += desc.block_len and n_blocks += blocks_in_prefix
+ *              (the number of sampler blocks the prefix spans, >= 0).
+ * y_fwd        fp32 [batch][len][nheads][64] or NULL: the forward outputs
+ *              (skip D) of the prefix tokens.  D_rev is not used.
+ * Errors: as bdlm_commit_boundary.
+ */
+int bdlm_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                 const void *B, const void *C, const float *D, float *h_pool, int64_t nslots,
+                 const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
+                 int64_t expected_block_index, int64_t blocks_in_prefix, float *y_fwd,
+                 void *stream);
+
+/*
  * State pool layout.  The state of one (slot, head) is the 64 x dstate matrix
  * s[p][n] of the recurrence.  In a pool, state k = slot * nheads + head starts
  * at float offset k * 64 * dstate and stores s[p][n] at
@@ -201,6 +244,14 @@ int bdlm_check_commit(const bdlm_desc_t *desc, const void *x, const void *dt, co
                       const float *h_pool, int64_t nslots, const int32_t *slot_idx,
                       const int64_t *n_committed, const int64_t *n_blocks,
                       int64_t expected_block_index);
+int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
+                           const float *A, const void *B, const void *C, const float *D,
+                           const float *D_rev, const float *y);
+int bdlm_check_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                       const void *B, const void *C, const float *D, const float *h_pool,
+                       int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,
+                       const int64_t *n_blocks, int64_t expected_block_index,
+                       int64_t blocks_in_prefix);
 
 #ifdef __cplusplus
 }

@@ -12,6 +12,9 @@ Entry points (same names as the C ABI):
   block-local reverse branch from zero, summed.
 * :func:`commit_boundary` -- block finalisation: the clean block's forward state
   replaces the cached one (Sec. 4, Eq. boundary-state).
+* :func:`scan_full_window` -- the full-sequence bidirectional scan with no cache
+  (the DiffuMamba-style contrast).
+* :func:`prefill` -- summarise a long clean prefix into the cached states in one launch.
 * :func:`cache_reset` -- empty the given cache slots.
 
 :class:`Cache` bundles a state pool with its host-side bookkeeping.
@@ -88,9 +91,16 @@ def lib() -> ctypes.CDLL:
         L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
         L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
         L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
+        L.bdlm_check_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp]
+        L.bdlm_scan_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, vp]
+        L.bdlm_check_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p,
+                                         i64, i64]
+        L.bdlm_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p, i64,
+                                   i64, fp, vp]
         for name in ("bdlm_desc_init", "bdlm_check_block_step", "bdlm_check_commit",
                      "bdlm_scan_block_step", "bdlm_commit_boundary", "bdlm_cache_reset",
-                     "bdlm_state_pack", "bdlm_state_unpack"):
+                     "bdlm_state_pack", "bdlm_state_unpack", "bdlm_check_full_window",
+                     "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -252,6 +262,57 @@ def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
     return y_clean
 
 
+def scan_full_window(x, dt, A, B, C, D, D_rev, y=None, stream=None):
+    """Full-window bidirectional scan with no cache: forward over the whole window from
+    zero plus reverse over the whole window from zero.  x is [B, W, H, 64]; returns y
+    (float32 [B, W, H, 64])."""
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H = d.nheads
+    if y is None:
+        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
+    elif y.dtype != torch.float32 or not y.is_contiguous() \
+            or tuple(y.shape) != (d.batch, d.block_len, H, HEADDIM):
+        raise ValueError("y must be a contiguous float32 [B, W, H, 64] tensor")
+    rc = lib().bdlm_scan_full_window(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _dev_ptr(y, "y"), _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_scan_full_window")
+    return y
+
+
+def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_index=-1,
+            blocks_in_prefix=0, slot_idx=None, y_fwd=None, stream=None):
+    """Summarise a clean prefix x [B, T, H, 64] (any T) into the cached states, in place.
+    Bookkeeping advances by T tokens and ``blocks_in_prefix`` blocks.  ``y_fwd``: None,
+    True (allocate and return) or a float32 tensor for the forward outputs."""
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    nslots = h_pool.shape[0]
+    for a in (n_committed, n_blocks):
+        if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
+                or a.shape != (nslots,):
+            raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
+    if y_fwd is True:
+        y_fwd = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
+                            device=x.device)
+    yp = None if y_fwd is None else _dev_ptr(y_fwd, "y_fwd")
+    keep, sp = _slots(slot_idx)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_prefill(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _pool(h_pool, H, N), nslots,
+        sp, n_committed.ctypes.data_as(i64p), n_blocks.ctypes.data_as(i64p),
+        int(expected_block_index), int(blocks_in_prefix), yp, _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_prefill")
+    return y_fwd
+
+
 def cache_reset(h_pool, slots=None, n_committed=None, n_blocks=None, stream=None):
     """Zero the given slots of ``h_pool`` (all if None) and their bookkeeping."""
     torch = _torch()
@@ -328,6 +389,11 @@ class Cache:
                y_clean=None, stream=None):
         return commit_boundary(x, dt, A, B, C, D, D_rev, self.h, self.n_committed,
                                self.n_blocks, expected_block_index, slot_idx, y_clean, stream)
+
+    def prefill(self, x, dt, A, B, C, D, expected_block_index=-1, blocks_in_prefix=0,
+                slot_idx=None, y_fwd=None, stream=None):
+        return prefill(x, dt, A, B, C, D, self.h, self.n_committed, self.n_blocks,
+                       expected_block_index, blocks_in_prefix, slot_idx, y_fwd, stream)
 
     def reset(self, slots=None, stream=None):
         cache_reset(self.h, slots, self.n_committed, self.n_blocks, stream)

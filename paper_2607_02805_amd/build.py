@@ -38,14 +38,17 @@ def _run(cmd: list[str]) -> None:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    k_obj = os.path.join(BUILD, "bdlm_scan.o")
+    objs = []
+    for src in ("bdlm_scan.hip", "bdlm_chain.hip"):
+        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),
+              "-o", obj])
+        objs.append(obj)
     a_obj = os.path.join(BUILD, "bdlm_api.o")
-    _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
-          os.path.join(CSRC, "bdlm_scan.hip"), "-o", k_obj])
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", f"-I{INCLUDE}", f"-I{CSRC}",
           "-c", os.path.join(CSRC, "bdlm_api.cpp"), "-o", a_obj])
     tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, k_obj, a_obj])
+    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs, a_obj])
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

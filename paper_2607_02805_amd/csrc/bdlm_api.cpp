@@ -15,9 +15,12 @@ bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 int64_t elem_size(int32_t dt) { return dt == BDLM_DTYPE_BF16 ? 2 : 4; }
 
 // Checks shared by a step and a commit.
+// max_len: the longest block_len the entry point accepts.  need_pool: the call
+// reads or writes a state pool (h_pool, nslots and slot_idx are checked).
 int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                  const void *B, const void *C, const float *D, const float *D_rev,
-                 const float *h_pool, int64_t nslots, const int32_t *slot_idx) {
+                 const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                 int64_t max_len = BDLM_MAX_BLOCK_LEN, bool need_pool = true) {
     if (!d) return BDLM_E_NULL;
     if (d->in_dtype != BDLM_DTYPE_F32 && d->in_dtype != BDLM_DTYPE_BF16) return BDLM_E_DTYPE;
     if (d->reserved != 0) return BDLM_E_DTYPE;
@@ -25,12 +28,15 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     if (d->headdim != BDLM_HEADDIM) return BDLM_E_SHAPE;
     if (d->dstate != 16 && d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
         return BDLM_E_SHAPE;
-    if (d->block_len > BDLM_MAX_BLOCK_LEN) return BDLM_E_SHAPE;
+    if (d->block_len > max_len) return BDLM_E_SHAPE;
     if (d->nheads % d->ngroups != 0) return BDLM_E_SHAPE;
-    if (nslots <= 0) return BDLM_E_SHAPE;
+    if (need_pool && nslots <= 0) return BDLM_E_SHAPE;
     // grid and 32-bit index limits of the kernels
-    if (d->batch * d->nheads > (int64_t(1) << 30) || d->nheads > (1 << 20)) return BDLM_E_SHAPE;
-    if (nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate)) return BDLM_E_SHAPE;
+    constexpr int64_t kMaxRows = int64_t(1) << 22;
+    if (d->batch > kMaxRows || d->nheads > kMaxRows || d->batch * d->nheads > kMaxRows)
+        return BDLM_E_SHAPE;
+    if (need_pool && nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate))
+        return BDLM_E_SHAPE;
     for (int i = 0; i < 3; ++i)
         if (d->x_stride[i] < 0 || d->bc_stride[i] < 0) return BDLM_E_SHAPE;
     if (d->dt_stride[0] < 0 || d->dt_stride[1] < 0) return BDLM_E_SHAPE;
@@ -39,7 +45,7 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     // can have no storage).
     const bool empty = d->batch == 0 || d->block_len == 0;
     if (!empty && (!x || !dt || !B || !C)) return BDLM_E_NULL;
-    if (!A || !D || !D_rev || !h_pool) return BDLM_E_NULL;
+    if (!A || !D || !D_rev || (need_pool && !h_pool)) return BDLM_E_NULL;
 
     // x, B and C are read in 16-byte vectors: base pointers 16-byte aligned and
     // every stride a whole number of 16-byte units.
@@ -50,6 +56,7 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     for (int i = 0; i < 3; ++i)
         if (d->bc_stride[i] % vec != 0 || d->x_stride[i] % vec != 0) return BDLM_E_ALIGN;
     if (!aligned(A, 4) || !aligned(D, 4) || !aligned(D_rev, 4)) return BDLM_E_ALIGN;
+    if (!need_pool) return BDLM_OK;
     if (!aligned(h_pool, 16)) return BDLM_E_ALIGN;
 
     if (slot_idx) {
@@ -145,13 +152,8 @@ int bdlm_check_block_step(const bdlm_desc_t *d, const void *x, const void *dt, c
     return BDLM_OK;
 }
 
-int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
-                      const void *B, const void *C, const float *D, const float *D_rev,
-                      const float *h_pool, int64_t nslots, const int32_t *slot_idx,
-                      const int64_t *n_committed, const int64_t *n_blocks,
-                      int64_t expected_block_index) {
-    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
-    if (rc != BDLM_OK) return rc;
+static int check_books(const bdlm_desc_t *d, const int32_t *slot_idx, const int64_t *n_committed,
+                       const int64_t *n_blocks, int64_t expected_block_index) {
     if (!n_committed || !n_blocks) return BDLM_E_NULL;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;
@@ -161,6 +163,40 @@ int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const
         if (expected_block_index >= 0 && n_blocks[s] != expected_block_index) return BDLM_E_OFFSET;
     }
     return BDLM_OK;
+}
+
+int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                      const void *B, const void *C, const float *D, const float *D_rev,
+                      const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                      const int64_t *n_committed, const int64_t *n_blocks,
+                      int64_t expected_block_index) {
+    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    if (rc != BDLM_OK) return rc;
+    return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
+}
+
+int bdlm_check_full_window(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                           const void *B, const void *C, const float *D, const float *D_rev,
+                           const float *y) {
+    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, nullptr, 0, nullptr,
+                                BDLM_MAX_SEQ_LEN, false);
+    if (rc != BDLM_OK) return rc;
+    if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
+    if (!aligned(y, 4)) return BDLM_E_ALIGN;
+    return BDLM_OK;
+}
+
+int bdlm_check_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                       const void *B, const void *C, const float *D, const float *h_pool,
+                       int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,
+                       const int64_t *n_blocks, int64_t expected_block_index,
+                       int64_t blocks_in_prefix) {
+    // D_rev is not used by a forward-only pass; D stands in for it in the checks
+    const int rc = check_common(d, x, dt, A, B, C, D, D, h_pool, nslots, slot_idx,
+                                BDLM_MAX_SEQ_LEN, true);
+    if (rc != BDLM_OK) return rc;
+    if (blocks_in_prefix < 0) return BDLM_E_SHAPE;
+    return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
 }
 
 int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
@@ -194,6 +230,35 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
         const int64_t s = slot_idx ? slot_idx[b] : b;
         n_committed[s] += d->block_len;
         n_blocks[s] += 1;
+    }
+    return BDLM_OK;
+}
+
+int bdlm_scan_full_window(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                          const void *B, const void *C, const float *D, const float *D_rev,
+                          float *y, void *stream) {
+    const int rc = bdlm_check_full_window(d, x, dt, A, B, C, D, D_rev, y);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D_rev, nullptr, nullptr, y);
+    return bdlm::launch_full_window(a, d->block_len, stream);
+}
+
+int bdlm_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                 const void *B, const void *C, const float *D, float *h_pool, int64_t nslots,
+                 const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
+                 int64_t expected_block_index, int64_t blocks_in_prefix, float *y_fwd,
+                 void *stream) {
+    int rc = bdlm_check_prefill(d, x, dt, A, B, C, D, h_pool, nslots, slot_idx, n_committed,
+                                n_blocks, expected_block_index, blocks_in_prefix);
+    if (rc != BDLM_OK) return rc;
+    if (y_fwd && !aligned(y_fwd, 4)) return BDLM_E_ALIGN;
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D, h_pool, slot_idx, y_fwd);
+    rc = bdlm::launch_prefill(a, d->block_len, stream);
+    if (rc != BDLM_OK) return rc;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        n_committed[s] += d->block_len;
+        n_blocks[s] += blocks_in_prefix;
     }
     return BDLM_OK;
 }

@@ -25,6 +25,14 @@ struct LaunchArgs {
 // Arguments are already validated.  Returns BDLM_OK or BDLM_E_LAUNCH.
 int launch_block(const LaunchArgs &a, bool commit, void *stream);
 
+// Full-window bidirectional scan over T tokens (a.L is ignored): forward pass,
+// then reverse pass adding into a.y.
+int launch_full_window(const LaunchArgs &a, int64_t T, void *stream);
+
+// Forward chain over T tokens continuing the states in a.h_pool (via a.slots),
+// writing them back; a.y (optional) receives the forward outputs.
+int launch_prefill(const LaunchArgs &a, int64_t T, void *stream);
+
 // Permute nstates states between row-major [64][dstate] and the pool layout.
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream);

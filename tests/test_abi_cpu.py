@@ -187,3 +187,79 @@ def test_entry_points_reject_before_launch(L):
     assert L.bdlm_cache_reset(FAKE + 8, 4, 1024, None, 0, None, None, None) == bd.E_ALIGN
     bad = np.array([4], np.int32)
     assert L.bdlm_cache_reset(FAKE, 4, 1024, i32p(bad), 1, None, None, None) == bd.E_SLOT
+
+
+def check_window(L, d, p):
+    return L.bdlm_check_full_window(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                    p["D"], p["Drev"], p["y"])
+
+
+def check_prefill(L, d, p, nslots=4, slots=None, nc=None, nb=None, expect=-1, blocks=0):
+    nc = np.zeros(nslots, np.int64) if nc is None else nc
+    nb = np.zeros(nslots, np.int64) if nb is None else nb
+    return L.bdlm_check_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                p["h"], nslots, i32p(slots), i64p(nc), i64p(nb), expect, blocks)
+
+
+def test_sequence_entry_points_accept_long_sequences(L):
+    """The full window and the prefill take any length up to BDLM_MAX_SEQ_LEN; the
+    block entry points stop at 64 tokens."""
+    for T in (0, 1, 65, 4096, 65536, 2 ** 31 - 1):
+        assert check_window(L, desc(L=T), ptrs()) == bd.OK
+        assert check_prefill(L, desc(L=T), ptrs(), blocks=T // 32) == bd.OK
+    assert check_window(L, desc(L=2 ** 31), ptrs()) == bd.E_SHAPE
+    assert check_prefill(L, desc(L=2 ** 31), ptrs()) == bd.E_SHAPE
+    assert check_step(L, desc(L=65), ptrs()) == bd.E_SHAPE
+
+
+def test_full_window_checks(L):
+    assert check_window(L, desc(), ptrs(h=None)) == bd.OK          # no pool involved
+    for field in ("x", "dt", "A", "B", "C", "D", "Drev", "y"):
+        assert check_window(L, desc(), ptrs(**{field: None})) == bd.E_NULL
+    assert check_window(L, desc(batch=0), ptrs(x=None, dt=None, B=None, C=None, y=None)) == bd.OK
+    assert check_window(L, desc(), ptrs(y=FAKE + 0x8004)) == bd.OK   # y only 4-byte aligned
+    assert check_window(L, desc(), ptrs(y=FAKE + 0x8002)) == bd.E_ALIGN
+    assert check_window(L, desc(), ptrs(x=FAKE + 8)) == bd.E_ALIGN
+    assert check_window(L, desc(N=48), ptrs()) == bd.E_SHAPE
+    assert L.bdlm_check_full_window(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    FAKE) == bd.E_NULL
+
+
+def test_prefill_checks(L):
+    d = desc(batch=3)
+    slots = np.array([3, 0, 1], np.int32)
+    nb = np.array([2, 2, 1, 2], np.int64)
+    nc = nb * 32
+    assert check_prefill(L, d, ptrs(Drev=None), slots=slots, nc=nc, nb=nb, expect=2) == bd.OK
+    assert check_prefill(L, d, ptrs(), slots=slots, nc=nc, nb=nb, expect=1) == bd.E_OFFSET
+    assert check_prefill(L, d, ptrs(), slots=np.array([3, 0, 3], np.int32)) == bd.E_SLOT
+    assert check_prefill(L, d, ptrs(), slots=np.array([4, 0, 1], np.int32)) == bd.E_SLOT
+    assert check_prefill(L, d, ptrs(), blocks=-1) == bd.E_SHAPE
+    assert check_prefill(L, d, ptrs(h=None)) == bd.E_NULL
+    assert check_prefill(L, d, ptrs(h=FAKE + 0x7008)) == bd.E_ALIGN
+    assert L.bdlm_check_prefill(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4,
+                                None, None, None, -1, 0) == bd.E_NULL
+
+
+def test_row_limit(L):
+    """batch * nheads is capped so that every launch grid fits 32 bits."""
+    assert check_step(L, desc(batch=2 ** 20, H=4), ptrs(), nslots=2 ** 20) == bd.OK
+    assert check_step(L, desc(batch=2 ** 20 + 1, H=4), ptrs(), nslots=2 ** 21) == bd.E_SHAPE
+    assert check_window(L, desc(batch=2 ** 21, H=4), ptrs()) == bd.E_SHAPE
+    assert check_window(L, desc(batch=2 ** 62, H=4), ptrs()) == bd.E_SHAPE   # no overflow
+
+
+def test_sequence_entry_points_reject_before_launch(L):
+    d = desc(batch=2, L=1000)
+    p = ptrs(x=None)
+    assert L.bdlm_scan_full_window(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                   p["D"], p["Drev"], p["y"], None) == bd.E_NULL
+    nc, nb = np.array([64, 64, 0, 0], np.int64), np.array([2, 2, 0, 0], np.int64)
+    p = ptrs()
+    rc = L.bdlm_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["h"],
+                        4, None, i64p(nc), i64p(nb), 3, 31, None, None)
+    assert rc == bd.E_OFFSET
+    assert nc.tolist() == [64, 64, 0, 0] and nb.tolist() == [2, 2, 0, 0]   # untouched
+    rc = L.bdlm_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["h"],
+                        4, None, i64p(nc), i64p(nb), 2, 31, FAKE + 2, None)
+    assert rc == bd.E_ALIGN

@@ -1,0 +1,168 @@
+"""GPU parity of the sequence-length kernels against the fp64 oracle:
+
+* bdlm_scan_full_window -- forward over the whole window from zero plus reverse over the
+  whole window from zero (the full-sequence contrast);
+* bdlm_prefill -- a clean prefix summarised into the cached states in one launch, which
+  must equal committing it block by block.
+
+Bar: max relative error 2e-3 (tests/gpu_util.py); bookkeeping bit-exact.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import bdlm_inputs as bi
+import oracle
+from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[gpu-chain]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def wl(batch, H, N, W, G=1, bf16=True, seed=9000):
+    return bi.Workload("t", batch, H, 64, N, G, W, 0, bf16, 1, seed)
+
+
+def full_window(d):
+    import paper_2607_02805_amd as bd
+    v = to_dev(d)
+    return bd.scan_full_window(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"])
+
+
+@pytest.mark.parametrize("N", [16, 32, 64, 128])
+@pytest.mark.parametrize("W", [1, 63, 64, 65, 200])
+def test_full_window_small(N, W):
+    w = wl(2, 3, N, W, seed=9100 + W)
+    d = bi.block_inputs(w, 0)
+    d["D_rev"] = (d["D"] * 0.5).astype(np.float32)      # distinct skips per direction
+    say("full window", w)
+    y = full_window(d)
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.full_window(d))
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
+@pytest.mark.parametrize("N,W", [(16, 130), (128, 300)])
+def test_full_window_fp32_storage(N, W):
+    w = wl(2, 2, N, W, bf16=False, seed=9200 + W)
+    d = bi.block_inputs(w, 0)
+    y = full_window(d)
+    torch.cuda.synchronize()
+    assert rel_err(y, oracle.full_window(d)) <= REL_TOL
+
+
+def test_full_window_groups_and_long():
+    w = wl(2, 4, 64, 2000, G=2, seed=9300)
+    d = bi.block_inputs(w, 0)
+    y = full_window(d)
+    torch.cuda.synchronize()
+    assert rel_err(y, oracle.full_window(d)) <= REL_TOL
+
+
+def to_host(t):
+    """GPU tensor -> the stored bytes as numpy (bf16 bit patterns as uint16)."""
+    t = t.contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16).copy()
+    return t.numpy().copy()
+
+
+def test_full_window_contrast_shape_sampled():
+    """The contrast workload: 350M layer shape, batch 4, 65,536-token window (inputs drawn
+    on the GPU).  Every output of two sampled (batch row, head) pairs against the oracle
+    run on just those rows and heads."""
+    import paper_2607_02805_amd as bd
+    w = bi.WORKLOADS[4]
+    v = bi.tokens_device(w, w.block_len, w.base_seed + 10)
+    hp = {k: torch.from_numpy(a).to(DEV) for k, a in bi.head_params(w).items()}
+    say("contrast shape", w)
+    y = bd.scan_full_window(v["x"], v["dt"], hp["A"], v["B"], v["C"], hp["D"], hp["D_rev"])
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+    for b, h in ((1, 5), (3, 30)):
+        sub = {"x": to_host(v["x"][b:b + 1, :, h:h + 1]), "dt": to_host(v["dt"][b:b + 1, :, h:h + 1]),
+               "B": to_host(v["B"][b:b + 1]), "C": to_host(v["C"][b:b + 1])}
+        sub.update({k: hp[k][h:h + 1].cpu().numpy() for k in ("A", "D", "D_rev")})
+        ref = oracle.full_window(sub)
+        e = rel_err(y[b:b + 1, :, h:h + 1], ref)
+        say("  (b, h) =", (b, h), "rel err", e)
+        assert e <= REL_TOL
+
+
+def test_full_window_equals_block_step_from_zero():
+    """With a window that fits one block, the two kernels compute the same thing."""
+    import paper_2607_02805_amd as bd
+    w = wl(3, 4, 128, 48, seed=9400)
+    d = bi.block_inputs(w, 0)
+    v = to_dev(d)
+    pool = torch.zeros((3, 4, 32, 64, 4), device=DEV)
+    y1 = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], pool)
+    y2 = full_window(d)
+    torch.cuda.synchronize()
+    ref = oracle.full_window(d)
+    assert rel_err(y1, ref) <= REL_TOL and rel_err(y2, ref) <= REL_TOL
+
+
+# ------------------------------------------------------------------------ prefill
+@pytest.mark.parametrize("N,T", [(16, 100), (64, 1000), (128, 4096)])
+def test_prefill_matches_oracle_prefix_scan(N, T):
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 3, 4, 64, N, 1, 32, T, True, 1, 9500 + T)
+    pre = bi.prefix_inputs(w)
+    s0 = bi.random_state(w, 5, 3, 0.5)
+    slots = [4, 0, 2]
+    cache = bd.Cache(5, 4, N)
+    cache.h.copy_(pool_dev(s0))
+    cache.n_blocks[:] = [1, 2, 1, 9, 1]
+    cache.n_committed[:] = cache.n_blocks * 32
+    v = to_dev(pre)
+    say("prefill", w)
+    yf = cache.prefill(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], expected_block_index=1,
+                       blocks_in_prefix=T // 32, slot_idx=slots, y_fwd=True)
+    torch.cuda.synchronize()
+    s_ref, y_ref = oracle.scan_forward(pre, s0[slots].astype(np.float64), want_y=True)
+    got = from_pool(cache.h)
+    e = rel_err(got[slots], s_ref)
+    say("  state rel err", e)
+    assert e <= REL_TOL
+    assert rel_err(yf, y_ref) <= REL_TOL
+    np.testing.assert_array_equal(got[[1, 3]], s0[[1, 3]])          # other slots untouched
+    k = T // 32
+    assert cache.n_blocks.tolist() == [1 + k, 2, 1 + k, 9, 1 + k]
+    assert cache.n_committed.tolist() == [32 + T, 64, 32 + T, 288, 32 + T]
+
+
+def test_prefill_equals_commits():
+    """One prefill launch over 64 blocks equals 64 commits of the same blocks."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, 8, 64, 128, 1, 32, 2048, True, 1, 9600)
+    pre = bi.prefix_inputs(w)
+    a, b = bd.Cache(2, 8, 128), bd.Cache(2, 8, 128)
+    v = to_dev(pre)
+    a.prefill(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], 0, 64)
+    for k in range(64):
+        blk = to_dev(bi.slice_tokens(pre, 32 * k, 32 * (k + 1)))
+        b.commit(blk["x"], blk["dt"], blk["A"], blk["B"], blk["C"], blk["D"], blk["D_rev"], k)
+    torch.cuda.synchronize()
+    assert a.n_blocks.tolist() == b.n_blocks.tolist() == [64, 64]
+    assert a.n_committed.tolist() == b.n_committed.tolist() == [2048, 2048]
+    ref = oracle.scan_forward(pre)
+    assert rel_err(a.states(), ref) <= REL_TOL and rel_err(b.states(), ref) <= REL_TOL
+
+
+def test_prefill_rejects_wrong_block_index():
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 1, 2, 64, 32, 1, 32, 64, True, 1, 9700)
+    v = to_dev(bi.prefix_inputs(w))
+    cache = bd.Cache(1, 2, 32)
+    with pytest.raises(bd.BdlmError) as ei:
+        cache.prefill(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], 3, 2)
+    assert ei.value.code == bd.E_OFFSET
+    assert cache.n_blocks.tolist() == [0]
