@@ -70,11 +70,127 @@ def to_dev(d, dev):
     return out
 
 
+class Ring:
+    """A ring of ``nl`` independent Mamba layers at one shape: per layer the ``p`` noised
+    blocks, the clean block, the outputs and a cache.  The prefix is committed into one
+    staging cache and copied into every layer's cache, so all layers sit at the same
+    prefix length."""
+
+    def __init__(self, w, nl, p, dev):
+        import torch
+
+        import bdlm_inputs as bi
+        import paper_2607_02805_amd as bd
+        self.w, self.nl, self.p, self.dev = w, nl, p, dev
+        Bsz, H, P, N, L = w.batch, w.nheads, w.headdim, w.dstate, w.block_len
+        base_steps = [to_dev(bi.block_inputs(w, s), dev) for s in range(p)]
+        base_clean = to_dev(bi.commit_inputs(w), dev)
+        self.layers = []
+        for _ in range(nl):
+            self.layers.append({
+                "steps": [{k: v.clone() for k, v in d.items()} for d in base_steps],
+                "clean": {k: v.clone() for k, v in base_clean.items()},
+                "y": torch.empty((Bsz, L, H, P), dtype=torch.float32, device=dev),
+                "y_clean": torch.empty((Bsz, L, H, P), dtype=torch.float32, device=dev)})
+        self.caches = [bd.Cache(Bsz, H, N, device=dev) for _ in range(nl)]
+        self.stage = bd.Cache(Bsz, H, N, device=dev)
+        pre = bi.prefix_inputs(w, 16 * L)
+        self.pre_blocks = [to_dev(bi.slice_tokens(pre, L * i, L * (i + 1)), dev)
+                           for i in range(16)]
+        self.graphs = None
+
+    def extend_prefix(self, tokens: int) -> float:
+        """Commit blocks (16 seeded clean blocks, cycled) until the prefix holds ``tokens``
+        tokens; returns the seconds taken."""
+        import torch
+        t0 = time.time()
+        L = self.w.block_len
+        k = int(self.stage.n_blocks[0])
+        while (k + 1) * L <= tokens:
+            d = self.pre_blocks[k % 16]
+            self.stage.commit(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
+                              expected_block_index=k)
+            k += 1
+        for c in self.caches:
+            c.h.copy_(self.stage.h)
+            c.n_committed[:] = self.stage.n_committed
+            c.n_blocks[:] = self.stage.n_blocks
+        torch.cuda.synchronize()
+        return time.time() - t0
+
+    def enqueue_steps(self):
+        import paper_2607_02805_amd as bd
+        for s in range(self.p):
+            for lay, c in zip(self.layers, self.caches):
+                d = lay["steps"][s]
+                bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
+                                   c.h, y=lay["y"])
+
+    def enqueue_commits(self):
+        import paper_2607_02805_amd as bd
+        for lay, c in zip(self.layers, self.caches):
+            d = lay["clean"]
+            # bookkeeping is advanced by the host after each replay (advance_books)
+            bd.commit_boundary(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"], c.h,
+                               c.n_committed.copy(), c.n_blocks.copy(), -1, y_clean=lay["y_clean"])
+
+    def capture(self, stream):
+        """Capture the ring's denoising steps and the ring's commits as two HIP graphs."""
+        import torch
+        g_steps, g_commit = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            self.enqueue_steps()          # eager warm-up of both kernels before capture
+            self.enqueue_commits()
+        stream.synchronize()
+        with torch.cuda.graph(g_steps, stream=stream):
+            self.enqueue_steps()
+        with torch.cuda.graph(g_commit, stream=stream):
+            self.enqueue_commits()
+        torch.cuda.synchronize()
+        self.graphs = (g_steps, g_commit)
+
+    def advance_books(self):
+        for c in self.caches:
+            c.n_committed += self.w.block_len
+            c.n_blocks += 1
+
+    def time_cycles(self, stream, steps: int, warmup: int) -> dict:
+        """Replay ``warmup`` then exactly ``steps`` block cycles (p steps + commit of every
+        layer); HIP events on the replay stream around each graph."""
+        import torch
+        g_steps, g_commit = self.graphs
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                g_steps.replay()
+                g_commit.replay()
+                self.advance_books()
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter()
+        with torch.cuda.stream(stream):
+            for k in range(steps):
+                ev[k][0].record(stream)
+                g_steps.replay()
+                ev[k][1].record(stream)
+                g_commit.replay()
+                ev[k][2].record(stream)
+                self.advance_books()
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t_wall
+        nl, p = self.nl, self.p
+        step_us = np.array([e[0].elapsed_time(e[1]) for e in ev]) * 1e3 / (p * nl)
+        commit_us = np.array([e[1].elapsed_time(e[2]) for e in ev]) * 1e3 / nl
+        t_total = ev[0][0].elapsed_time(ev[-1][2]) * 1e-3
+        return {"step_us": step_us, "commit_us": commit_us, "t_total": t_total,
+                "wall_s": wall_s, "prefix_tokens": int(self.caches[0].n_committed[0])}
+
+
 def run_gpu(args):
     import torch
 
     import bdlm_inputs as bi
-    import paper_2607_02805_amd as bd
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -82,128 +198,190 @@ def run_gpu(args):
     Bsz, H, P, N, G, L = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, w.block_len
     nl, p = args.layers, args.denoise
 
-    # ---- inputs: p noised blocks + 1 clean block, copied into every layer of the ring
-    steps_h = [bi.block_inputs(w, s) for s in range(p)]
-    clean_h = bi.commit_inputs(w)
-    base_steps = [to_dev(d, dev) for d in steps_h]
-    base_clean = to_dev(clean_h, dev)
-    layers = []
-    for _ in range(nl):
-        lay = {"steps": [{k: v.clone() for k, v in d.items()} for d in base_steps],
-               "clean": {k: v.clone() for k, v in base_clean.items()},
-               "y": torch.empty((Bsz, L, H, P), dtype=torch.float32, device=dev),
-               "y_clean": torch.empty((Bsz, L, H, P), dtype=torch.float32, device=dev)}
-        layers.append(lay)
-
-    # ---- prefix: commit args.prefix tokens into layer 0's cache (16 seeded clean blocks
-    #      cycled), then give every layer of the ring that state and bookkeeping
-    t0 = time.time()
-    cache0 = bd.Cache(Bsz, H, N, device=dev)
-    pre = bi.prefix_inputs(w, 16 * L)
-    pre_blocks = [to_dev(bi.slice_tokens(pre, L * i, L * (i + 1)), dev) for i in range(16)]
-    nblk = args.prefix // L
-    for k in range(nblk):
-        d = pre_blocks[k % 16]
-        cache0.commit(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
-                      expected_block_index=k)
-    torch.cuda.synchronize()
-    caches = []
-    for _ in range(nl):
-        c = bd.Cache(Bsz, H, N, device=dev)
-        c.h.copy_(cache0.h)
-        c.n_committed[:] = cache0.n_committed
-        c.n_blocks[:] = cache0.n_blocks
-        caches.append(c)
-    del cache0
-    torch.cuda.synchronize()
-    prefill_s = time.time() - t0
-    print(f"[bench] prefix of {args.prefix} tokens committed ({nblk} commits) in {prefill_s:.2f}s; "
-          f"ring of {nl} layers, state {nl * Bsz * H * P * N * 4 / 2**20:.0f} MiB", flush=True)
-
-    # ---- capture the ring's denoising steps and the ring's commits as two graphs
+    ring = Ring(w, nl, p, dev)
+    prefill_s = ring.extend_prefix(args.prefix)
+    print(f"[bench] prefix of {args.prefix} tokens committed ({args.prefix // L} commits) in "
+          f"{prefill_s:.2f}s; ring of {nl} layers, state {nl * Bsz * H * P * N * 4 / 2**20:.0f} MiB",
+          flush=True)
     stream = torch.cuda.Stream()
-    g_steps, g_commit = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    ring.capture(stream)
+    t = ring.time_cycles(stream, args.steps, args.warmup)
 
-    def enqueue_steps():
-        for s in range(p):
-            for li in range(nl):
-                d, c = layers[li]["steps"][s], caches[li]
-                bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
-                                   c.h, y=layers[li]["y"])
-
-    def enqueue_commits():
-        for li in range(nl):
-            d, c = layers[li]["clean"], caches[li]
-            # bookkeeping is advanced by the host after each replay (below)
-            bd.commit_boundary(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"], c.h,
-                               c.n_committed.copy(), c.n_blocks.copy(), -1,
-                               y_clean=layers[li]["y_clean"])
-
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        enqueue_steps()          # eager warm-up of both kernels before capture
-        enqueue_commits()
-    stream.synchronize()
-    with torch.cuda.graph(g_steps, stream=stream):
-        enqueue_steps()
-    with torch.cuda.graph(g_commit, stream=stream):
-        enqueue_commits()
-    torch.cuda.synchronize()
-
-    def advance_books():
-        for c in caches:
-            c.n_committed += L
-            c.n_blocks += 1
-
-    with torch.cuda.stream(stream):
-        for _ in range(args.warmup):
-            g_steps.replay()
-            g_commit.replay()
-            advance_books()
-    torch.cuda.synchronize()
-
-    # ---- timed region: exactly K block cycles
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    with torch.cuda.stream(stream):
-        for k in range(args.steps):
-            ev[k][0].record(stream)
-            g_steps.replay()
-            ev[k][1].record(stream)
-            g_commit.replay()
-            ev[k][2].record(stream)
-            advance_books()
-    torch.cuda.synchronize()
-    wall_s = time.perf_counter() - t_wall
-    t_steps = sum(e[0].elapsed_time(e[1]) for e in ev) * 1e-3        # seconds
-    t_commit = sum(e[1].elapsed_time(e[2]) for e in ev) * 1e-3
-    t_total = ev[0][0].elapsed_time(ev[-1][2]) * 1e-3
-
-    n_step_launch = args.steps * p * nl
-    n_commit_launch = args.steps * nl
-    avg_step_s = t_steps / n_step_launch
-    avg_commit_s = t_commit / n_commit_launch
-    per_layer_cycle_s = t_total / (args.steps * nl)
+    avg_step_s = float(t["step_us"].mean()) * 1e-6
+    avg_commit_s = float(t["commit_us"].mean()) * 1e-6
+    per_layer_cycle_s = t["t_total"] / (args.steps * nl)
     tokens = p * Bsz * L
-    value = tokens / per_layer_cycle_s
     sb = step_bytes(Bsz, H, P, N, G, L)
     cb = commit_bytes(Bsz, H, P, N, G, L)
-    achieved = sb / avg_step_s / 1e9
-    res = {
-        "value": value,
-        "ms_per_step": t_total / args.steps * 1e3,
-        "wall_s": wall_s,
+    del ring
+    torch.cuda.empty_cache()
+    return {
+        "value": tokens / per_layer_cycle_s,
+        "ms_per_step": t["t_total"] / args.steps * 1e3,
+        "wall_s": t["wall_s"],
         "avg_step_us": avg_step_s * 1e6,
+        "median_step_us": float(np.median(t["step_us"])),
+        "min_step_us": float(t["step_us"].min()),
         "avg_commit_us": avg_commit_s * 1e6,
         "step_bytes": sb,
         "commit_bytes": cb,
-        "achieved_gbs": achieved,
+        "achieved_gbs": sb / avg_step_s / 1e9,
         "commit_gbs": cb / avg_commit_s / 1e9,
-        "prefix_tokens": int(caches[0].n_committed[0]),
+        "prefix_tokens": t["prefix_tokens"],
         "shape": dict(batch=Bsz, nheads=H, headdim=P, dstate=N, ngroups=G, block_len=L),
     }
-    return res
+
+
+def run_flatness(args, prefixes=(4096, 65536, 262144), block_lens=(16, 32, 64)) -> dict:
+    """Per-launch block-step and commit times at each prefix length and block length: the
+    state is O(1) in the prefix, so the times must not move with it."""
+    import torch
+
+    import bdlm_inputs as bi
+    dev = "cuda:0"
+    stream = torch.cuda.Stream()
+    out = {"prefix_tokens": list(prefixes), "cycles": args.sweep_steps}
+    spreads = []
+    for L in block_lens:
+        w = bi.WORKLOADS[3].with_block_len(L)
+        ring = Ring(w, args.layers, args.denoise, dev)
+        ring.capture(stream)
+        st, cm = [], []
+        for pre in prefixes:
+            ring.extend_prefix(pre)
+            t = ring.time_cycles(stream, args.sweep_steps, 2)
+            st.append(round(float(np.median(t["step_us"])), 3))
+            cm.append(round(float(np.median(t["commit_us"])), 3))
+        out[f"L{L}"] = {"step_us": st, "commit_us": cm,
+                        "step_gbs": [round(step_bytes(16, 32, 64, 128, 1, L) / (u * 1e3), 1)
+                                     for u in st]}
+        spreads.append((max(st) - min(st)) / min(st))
+        print(f"[bench] flatness L={L}: step us {st}, commit us {cm}", flush=True)
+        del ring
+        torch.cuda.empty_cache()
+    out["max_step_spread"] = round(max(spreads), 4)
+    return out
+
+
+def full_window_bytes(batch, H, P, N, G, W, in_bytes=2):
+    """Algorithmic HBM bytes of the full-window scan: the window's inputs read once and y
+    (fp32) written once; no state."""
+    return step_bytes(batch, H, P, N, G, W, in_bytes) - batch * H * P * N * 4
+
+
+def run_contrast(args, block: dict) -> dict:
+    """The full-window bidirectional scan at batch 4 over a 65,536-token window (inputs
+    drawn on the GPU), timed with HIP events, and the ratio of per-sequence rates against
+    the block-restricted cycle at an equal number of denoising steps per block."""
+    import torch
+
+    import bdlm_inputs as bi
+    import paper_2607_02805_amd as bd
+    dev = "cuda:0"
+    w = bi.WORKLOADS[4]
+    v = bi.tokens_device(w, w.block_len, w.base_seed + 10, dev)
+    hp = {k: torch.from_numpy(a).to(dev) for k, a in bi.head_params(w).items()}
+    y = torch.empty((w.batch, w.block_len, w.nheads, w.headdim), dtype=torch.float32, device=dev)
+    stream = torch.cuda.Stream()
+    reps = args.contrast_reps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        bd.scan_full_window(v["x"], v["dt"], hp["A"], v["B"], v["C"], hp["D"], hp["D_rev"], y,
+                            stream=stream)                     # warm-up
+        ev[0].record(stream)
+        for r in range(reps):
+            bd.scan_full_window(v["x"], v["dt"], hp["A"], v["B"], v["C"], hp["D"], hp["D_rev"],
+                                y, stream=stream)
+            ev[r + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = [ev[r].elapsed_time(ev[r + 1]) for r in range(reps)]
+    t_full = float(np.median(ms)) * 1e-3
+    fb = full_window_bytes(w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, w.block_len)
+    # per-sequence time of one denoising step: the full window serves w.batch sequences per
+    # call; the block step serves 16 per launch, plus the commit once every p steps
+    s = block["shape"]
+    t_seq_full = t_full / w.batch
+    t_seq_block = (block["avg_step_us"] + block["avg_commit_us"] / args.denoise) * 1e-6 / s["batch"]
+    del v, y
+    torch.cuda.empty_cache()
+    return {
+        "workload": f"350m-mamba-layer-b{w.batch}-fullwindow{w.block_len}",
+        "full_window_ms": round(t_full * 1e3, 3),
+        "full_window_ms_all": [round(m, 3) for m in ms],
+        "alg_bytes": fb,
+        "achieved_gbs": round(fb / t_full / 1e9, 1),
+        "frac": round(fb / t_full / 1e9 / HBM_PEAK_GBS, 4),
+        "per_sequence_step_us": {"full_window": round(t_seq_full * 1e6, 3),
+                                 "block_restricted": round(t_seq_block * 1e6, 4)},
+        "ratio": round(t_seq_full / t_seq_block, 1),
+    }
+
+
+def run_prefill(args) -> dict:
+    """Chunked prefill of a clean prefix into the cached states at the 350M layer shape,
+    batch 16 (inputs drawn on the GPU)."""
+    import torch
+
+    import bdlm_inputs as bi
+    import paper_2607_02805_amd as bd
+    dev = "cuda:0"
+    w = bi.WORKLOADS[3]
+    T = args.prefill_tokens
+    v = bi.tokens_device(w, T, w.base_seed + 1, dev)
+    hp = {k: torch.from_numpy(a).to(dev) for k, a in bi.head_params(w).items()}
+    cache = bd.Cache(w.batch, w.nheads, w.dstate, device=dev)
+    stream = torch.cuda.Stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        cache.prefill(v["x"], v["dt"], hp["A"], v["B"], v["C"], hp["D"], stream=stream)
+        e0.record(stream)
+        cache.prefill(v["x"], v["dt"], hp["A"], v["B"], v["C"], hp["D"], stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3
+    nbytes = full_window_bytes(w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, T) \
+        - w.batch * T * w.nheads * w.headdim * 4 + 2 * w.batch * w.nheads * w.headdim * w.dstate * 4
+    del v, cache
+    torch.cuda.empty_cache()
+    return {"tokens": T, "batch": w.batch, "ms": round(t * 1e3, 3),
+            "tokens_per_s": round(w.batch * T / t, 1), "alg_bytes": nbytes,
+            "achieved_gbs": round(nbytes / t / 1e9, 1)}
+
+
+def run_copy_reference(nbytes: int, nbuf: int = 32, reps: int = 20) -> dict:
+    """A plain device copy moving ``nbytes`` in total (half read, half written) per launch,
+    over a ring of ``nbuf`` buffers so that every launch misses the Infinity Cache,
+    replayed from a HIP graph: what a streaming kernel of the block step's size achieves."""
+    import torch
+    dev = "cuda:0"
+    n = nbytes // 2 // 4
+    src = [torch.empty(n, dtype=torch.float32, device=dev).uniform_() for _ in range(nbuf)]
+    dst = [torch.empty(n, dtype=torch.float32, device=dev) for _ in range(nbuf)]
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for a, b in zip(src, dst):
+            b.copy_(a)
+    stream.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        for a, b in zip(src, dst):
+            b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        g.replay()
+        e0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * nbuf)
+    del src, dst, g
+    torch.cuda.empty_cache()
+    return {"bytes_per_launch": 2 * n * 4, "us_per_launch": round(us, 3),
+            "gbs": round(2 * n * 4 / us / 1e3, 1)}
 
 
 def cpu_baseline(args, budget_s: float):
@@ -332,6 +510,13 @@ def main():
     ap.add_argument("--prefix", type=int, default=262144, help="committed prefix tokens")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds for the oracle leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the flatness sweep, the full-window contrast, the prefill and "
+                         "the copy reference")
+    ap.add_argument("--sweep-steps", type=int, default=10,
+                    help="timed block cycles per point of the flatness sweep")
+    ap.add_argument("--contrast-reps", type=int, default=3)
+    ap.add_argument("--prefill-tokens", type=int, default=16384)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (counter calibration) and exit")
     ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
@@ -361,6 +546,12 @@ def main():
         sys.exit(2)
 
     r = run_gpu(args)
+    extras = {}
+    if not args.no_extras:
+        extras["copy_reference"] = run_copy_reference(r["step_bytes"])
+        extras["flatness"] = run_flatness(args)
+        extras["contrast"] = run_contrast(args, r)
+        extras["prefill"] = run_prefill(args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, args.cpu_budget)
     s = r["shape"]
     line = {
@@ -385,7 +576,10 @@ def main():
             "prefix_tokens": r["prefix_tokens"], "denoise_steps": args.denoise,
             "activations": "bf16", "state": "f32", "y": "f32",
             "layer_ring": args.layers, "launch": "hip-graph replay",
-            "step_us": round(r["avg_step_us"], 3), "commit_us": round(r["avg_commit_us"], 3),
+            "step_us": round(r["avg_step_us"], 3),
+            "step_us_median": round(r["median_step_us"], 3),
+            "step_us_min": round(r["min_step_us"], 3),
+            "commit_us": round(r["avg_commit_us"], 3),
             "commit_gbs": round(r["commit_gbs"], 1),
         },
         "roofline": {
@@ -400,6 +594,11 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if "copy_reference" in extras:
+        cr = extras["copy_reference"]
+        line["roofline"]["copy_same_bytes_gbs"] = cr["gbs"]
+        line["roofline"]["frac_of_copy"] = round(r["achieved_gbs"] / cr["gbs"], 4)
+    line.update(extras)
     print(json.dumps(line), flush=True)
 
 
