@@ -63,7 +63,8 @@ enum bdlm_status {
     BDLM_E_ALIGN = -4,   /* a pointer or stride breaks the alignment contract */
     BDLM_E_OFFSET = -5,  /* commit: a slot does not hold expected_block_index blocks */
     BDLM_E_SLOT = -6,    /* slot index out of range, or repeated within one commit */
-    BDLM_E_LAUNCH = -7   /* the HIP runtime refused the launch */
+    BDLM_E_LAUNCH = -7,  /* the HIP runtime refused the launch */
+    BDLM_E_WORKSPACE = -8 /* sequence entry points: workspace missing or too small */
 };
 
 enum bdlm_dtype { BDLM_DTYPE_F32 = 0, BDLM_DTYPE_BF16 = 1 };
@@ -161,6 +162,18 @@ int bdlm_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
                          int64_t expected_block_index, float *y_clean, void *stream);
 
 /*
+ * The sequence entry points below split the sequence into segments, one
+ * workgroup per (batch row, head, segment), and carry states between segments
+ * through a device workspace that the caller allocates (the library allocates
+ * nothing).  These return in *bytes the workspace size that bdlm_scan_full_window /
+ * bdlm_prefill need for *desc (desc.block_len = sequence length); 0 means none.
+ * The size depends only on batch, nheads, dstate and the length.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE.
+ */
+int bdlm_full_window_workspace(const bdlm_desc_t *desc, int64_t *bytes);
+int bdlm_prefill_workspace(const bdlm_desc_t *desc, int64_t *bytes);
+
+/*
  * Full-window bidirectional scan, with no cache: the full-sequence
  * (DiffuMamba-style) scan that the paper's block-restricted scan replaces
  * (Sec. 4; Sec. 5.1).
@@ -170,34 +183,39 @@ int bdlm_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
  *
  * desc.block_len is the window length, 0 .. BDLM_MAX_SEQ_LEN; every other argument
  * is as for bdlm_scan_block_step with block_len set to the window (y is
- * [batch][window][nheads][64] fp32, 4-byte aligned).  Two passes over the window in
- * 64-token chunks, the state carried in registers; y is written by the forward pass
- * and updated by the reverse pass.
- * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE, BDLM_E_ALIGN, BDLM_E_LAUNCH.
+ * [batch][window][nheads][64] fp32, 4-byte aligned).
+ * workspace    device memory of at least bdlm_full_window_workspace bytes,
+ *              256-byte aligned (may be NULL when that size is 0); its contents
+ *              are scratch, overwritten by the call.  Calls that share a
+ *              workspace must not run concurrently.
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE, BDLM_E_ALIGN,
+ * BDLM_E_WORKSPACE, BDLM_E_LAUNCH.
  */
 int bdlm_scan_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
                           const float *A, const void *B, const void *C, const float *D,
-                          const float *D_rev, float *y, void *stream);
+                          const float *D_rev, float *y, void *workspace,
+                          int64_t workspace_bytes, void *stream);
 
 /*
  * Chunked prefix prefill: summarise a clean prefix of desc.block_len tokens (any
  * length up to BDLM_MAX_SEQ_LEN) into the cached forward boundary states
  * (Eq. boundary-state), continuing each row's state in place.  Equivalent to
- * committing the prefix block by block, in one launch.
+ * committing the prefix block by block.
  * h_pool, slot_idx  as for bdlm_commit_boundary (slots distinct).
  * n_committed, n_blocks  host bookkeeping: every slot must hold
  *              expected_block_index blocks (negative: unchecked); on success
  *              n_committed += desc.block_len and n_blocks += blocks_in_prefix
  *              (the number of sampler blocks the prefix spans, >= 0).
- * y_fwd        fp32 [batch][len][nheads][64] or NULL: the forward outputs
- *              (skip D) of the prefix tokens.  D_rev is not used.
- * Errors: as bdlm_commit_boundary.
+ * y_fwd        fp32 [batch][len][nheads][64] (4-byte aligned) or NULL: the forward
+ *              outputs (skip D) of the prefix tokens.  D_rev is not used.
+ * workspace    at least bdlm_prefill_workspace bytes, 256-byte aligned; scratch.
+ * Errors: as bdlm_commit_boundary, and BDLM_E_WORKSPACE.
  */
 int bdlm_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
                  const void *B, const void *C, const float *D, float *h_pool, int64_t nslots,
                  const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
                  int64_t expected_block_index, int64_t blocks_in_prefix, float *y_fwd,
-                 void *stream);
+                 void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * State pool layout.  The state of one (slot, head) is the 64 x dstate matrix
@@ -246,12 +264,14 @@ int bdlm_check_commit(const bdlm_desc_t *desc, const void *x, const void *dt, co
                       int64_t expected_block_index);
 int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
                            const float *A, const void *B, const void *C, const float *D,
-                           const float *D_rev, const float *y);
+                           const float *D_rev, const float *y, const void *workspace,
+                           int64_t workspace_bytes);
 int bdlm_check_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
                        const void *B, const void *C, const float *D, const float *h_pool,
                        int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,
                        const int64_t *n_blocks, int64_t expected_block_index,
-                       int64_t blocks_in_prefix);
+                       int64_t blocks_in_prefix, const float *y_fwd, const void *workspace,
+                       int64_t workspace_bytes);
 
 #ifdef __cplusplus
 }

@@ -37,7 +37,8 @@ MAX_SLOT_ROWS = 256
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 
-OK, E_NULL, E_SHAPE, E_DTYPE, E_ALIGN, E_OFFSET, E_SLOT, E_LAUNCH = 0, -1, -2, -3, -4, -5, -6, -7
+OK, E_NULL, E_SHAPE, E_DTYPE, E_ALIGN, E_OFFSET, E_SLOT, E_LAUNCH, E_WORKSPACE = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8
 
 
 class BdlmError(RuntimeError):
@@ -91,16 +92,19 @@ def lib() -> ctypes.CDLL:
         L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
         L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
         L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
-        L.bdlm_check_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp]
-        L.bdlm_scan_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, vp]
+        L.bdlm_full_window_workspace.argtypes = [dp, i64p]
+        L.bdlm_prefill_workspace.argtypes = [dp, i64p]
+        L.bdlm_check_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, vp, i64]
+        L.bdlm_scan_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, vp, i64, vp]
         L.bdlm_check_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p,
-                                         i64, i64]
+                                         i64, i64, fp, vp, i64]
         L.bdlm_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p, i64,
-                                   i64, fp, vp]
+                                   i64, fp, vp, i64, vp]
         for name in ("bdlm_desc_init", "bdlm_check_block_step", "bdlm_check_commit",
                      "bdlm_scan_block_step", "bdlm_commit_boundary", "bdlm_cache_reset",
                      "bdlm_state_pack", "bdlm_state_unpack", "bdlm_check_full_window",
-                     "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill"):
+                     "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill",
+                     "bdlm_full_window_workspace", "bdlm_prefill_workspace"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -262,10 +266,45 @@ def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
     return y_clean
 
 
-def scan_full_window(x, dt, A, B, C, D, D_rev, y=None, stream=None):
+def _workspace_bytes(fn, d) -> int:
+    n = ctypes.c_int64(0)
+    rc = fn(ctypes.byref(d), ctypes.byref(n))
+    if rc != OK:
+        raise BdlmError(rc, fn.__name__)
+    return int(n.value)
+
+
+def _workspace(fn, d, workspace, device):
+    """(pointer, bytes, keep-alive) of the sequence workspace: the caller's tensor, or a
+    fresh one from torch's allocator when none is given."""
+    torch = _torch()
+    need = _workspace_bytes(fn, d)
+    if workspace is None:
+        if need == 0:
+            return None, 0, None
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    if not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size(), workspace
+
+
+def full_window_workspace_bytes(batch, nheads, dstate, window) -> int:
+    d = Desc()
+    lib().bdlm_desc_init(ctypes.byref(d), batch, nheads, HEADDIM, dstate, 1, window, DTYPE_BF16)
+    return _workspace_bytes(lib().bdlm_full_window_workspace, d)
+
+
+def prefill_workspace_bytes(batch, nheads, dstate, length) -> int:
+    d = Desc()
+    lib().bdlm_desc_init(ctypes.byref(d), batch, nheads, HEADDIM, dstate, 1, length, DTYPE_BF16)
+    return _workspace_bytes(lib().bdlm_prefill_workspace, d)
+
+
+def scan_full_window(x, dt, A, B, C, D, D_rev, y=None, stream=None, workspace=None):
     """Full-window bidirectional scan with no cache: forward over the whole window from
     zero plus reverse over the whole window from zero.  x is [B, W, H, 64]; returns y
-    (float32 [B, W, H, 64])."""
+    (float32 [B, W, H, 64]).  ``workspace``: a device tensor of at least
+    :func:`full_window_workspace_bytes` bytes, 256-byte aligned (default: allocated)."""
     torch = _torch()
     d = _desc(x, dt, B, C)
     H = d.nheads
@@ -274,20 +313,24 @@ def scan_full_window(x, dt, A, B, C, D, D_rev, y=None, stream=None):
     elif y.dtype != torch.float32 or not y.is_contiguous() \
             or tuple(y.shape) != (d.batch, d.block_len, H, HEADDIM):
         raise ValueError("y must be a contiguous float32 [B, W, H, 64] tensor")
-    rc = lib().bdlm_scan_full_window(
+    L = lib()
+    wp, wb, keep = _workspace(L.bdlm_full_window_workspace, d, workspace, x.device)
+    rc = L.bdlm_scan_full_window(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
         _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
-        _dev_ptr(y, "y"), _stream_handle(stream))
+        _dev_ptr(y, "y"), wp, wb, _stream_handle(stream))
+    del keep
     if rc != OK:
         raise BdlmError(rc, "bdlm_scan_full_window")
     return y
 
 
 def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_index=-1,
-            blocks_in_prefix=0, slot_idx=None, y_fwd=None, stream=None):
+            blocks_in_prefix=0, slot_idx=None, y_fwd=None, stream=None, workspace=None):
     """Summarise a clean prefix x [B, T, H, 64] (any T) into the cached states, in place.
     Bookkeeping advances by T tokens and ``blocks_in_prefix`` blocks.  ``y_fwd``: None,
-    True (allocate and return) or a float32 tensor for the forward outputs."""
+    True (allocate and return) or a float32 tensor for the forward outputs.
+    ``workspace``: as for :func:`scan_full_window` (:func:`prefill_workspace_bytes`)."""
     torch = _torch()
     d = _desc(x, dt, B, C)
     H, N = d.nheads, d.dstate
@@ -301,13 +344,15 @@ def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_ind
                             device=x.device)
     yp = None if y_fwd is None else _dev_ptr(y_fwd, "y_fwd")
     keep, sp = _slots(slot_idx)
+    L = lib()
+    wp, wb, wkeep = _workspace(L.bdlm_prefill_workspace, d, workspace, x.device)
     i64p = ctypes.POINTER(ctypes.c_int64)
-    rc = lib().bdlm_prefill(
+    rc = L.bdlm_prefill(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
         _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _pool(h_pool, H, N), nslots,
         sp, n_committed.ctypes.data_as(i64p), n_blocks.ctypes.data_as(i64p),
-        int(expected_block_index), int(blocks_in_prefix), yp, _stream_handle(stream))
-    del keep
+        int(expected_block_index), int(blocks_in_prefix), yp, wp, wb, _stream_handle(stream))
+    del keep, wkeep
     if rc != OK:
         raise BdlmError(rc, "bdlm_prefill")
     return y_fwd
@@ -391,9 +436,10 @@ class Cache:
                                self.n_blocks, expected_block_index, slot_idx, y_clean, stream)
 
     def prefill(self, x, dt, A, B, C, D, expected_block_index=-1, blocks_in_prefix=0,
-                slot_idx=None, y_fwd=None, stream=None):
+                slot_idx=None, y_fwd=None, stream=None, workspace=None):
         return prefill(x, dt, A, B, C, D, self.h, self.n_committed, self.n_blocks,
-                       expected_block_index, blocks_in_prefix, slot_idx, y_fwd, stream)
+                       expected_block_index, blocks_in_prefix, slot_idx, y_fwd, stream,
+                       workspace)
 
     def reset(self, slots=None, stream=None):
         cache_reset(self.h, slots, self.n_committed, self.n_blocks, stream)

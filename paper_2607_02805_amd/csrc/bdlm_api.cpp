@@ -14,13 +14,9 @@ bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 int64_t elem_size(int32_t dt) { return dt == BDLM_DTYPE_BF16 ? 2 : 4; }
 
-// Checks shared by a step and a commit.
-// max_len: the longest block_len the entry point accepts.  need_pool: the call
-// reads or writes a state pool (h_pool, nslots and slot_idx are checked).
-int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
-                 const void *B, const void *C, const float *D, const float *D_rev,
-                 const float *h_pool, int64_t nslots, const int32_t *slot_idx,
-                 int64_t max_len = BDLM_MAX_BLOCK_LEN, bool need_pool = true) {
+// Checks of the descriptor alone.  max_len: the longest block_len the entry point
+// accepts.
+int check_desc(const bdlm_desc_t *d, int64_t max_len) {
     if (!d) return BDLM_E_NULL;
     if (d->in_dtype != BDLM_DTYPE_F32 && d->in_dtype != BDLM_DTYPE_BF16) return BDLM_E_DTYPE;
     if (d->reserved != 0) return BDLM_E_DTYPE;
@@ -30,16 +26,28 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
         return BDLM_E_SHAPE;
     if (d->block_len > max_len) return BDLM_E_SHAPE;
     if (d->nheads % d->ngroups != 0) return BDLM_E_SHAPE;
-    if (need_pool && nslots <= 0) return BDLM_E_SHAPE;
-    // grid and 32-bit index limits of the kernels
+    // every launch grid stays within 32 bits
     constexpr int64_t kMaxRows = int64_t(1) << 22;
     if (d->batch > kMaxRows || d->nheads > kMaxRows || d->batch * d->nheads > kMaxRows)
-        return BDLM_E_SHAPE;
-    if (need_pool && nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate))
         return BDLM_E_SHAPE;
     for (int i = 0; i < 3; ++i)
         if (d->x_stride[i] < 0 || d->bc_stride[i] < 0) return BDLM_E_SHAPE;
     if (d->dt_stride[0] < 0 || d->dt_stride[1] < 0) return BDLM_E_SHAPE;
+    return BDLM_OK;
+}
+
+// Checks shared by every entry point that takes activations.
+// need_pool: the call reads or writes a state pool (h_pool, nslots and slot_idx
+// are checked).
+int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                 const void *B, const void *C, const float *D, const float *D_rev,
+                 const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                 int64_t max_len = BDLM_MAX_BLOCK_LEN, bool need_pool = true) {
+    const int rc = check_desc(d, max_len);
+    if (rc != BDLM_OK) return rc;
+    if (need_pool && nslots <= 0) return BDLM_E_SHAPE;
+    if (need_pool && nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate))
+        return BDLM_E_SHAPE;
     if (slot_idx && d->batch > BDLM_MAX_SLOT_ROWS) return BDLM_E_SHAPE;
     // With no token to read, the activation pointers may be NULL (an empty tensor
     // can have no storage).
@@ -115,6 +123,7 @@ const char *bdlm_strerror(int status) {
         case BDLM_E_OFFSET: return "cache slot does not hold the expected number of blocks";
         case BDLM_E_SLOT: return "slot index out of range or repeated in a commit";
         case BDLM_E_LAUNCH: return "HIP launch failed";
+        case BDLM_E_WORKSPACE: return "workspace missing or smaller than required";
         default: return "unknown status";
     }
 }
@@ -175,27 +184,59 @@ int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const
     return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
 }
 
+static int check_workspace(const void *ws, int64_t ws_bytes, int64_t need) {
+    if (ws_bytes < 0) return BDLM_E_SHAPE;
+    if (need == 0) return BDLM_OK;
+    if (!ws) return BDLM_E_WORKSPACE;
+    if (ws_bytes < need) return BDLM_E_WORKSPACE;
+    if (!aligned(ws, 256)) return BDLM_E_ALIGN;
+    return BDLM_OK;
+}
+
+int bdlm_full_window_workspace(const bdlm_desc_t *d, int64_t *bytes) {
+    if (!bytes) return BDLM_E_NULL;
+    const int rc = check_desc(d, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    *bytes = bdlm::full_window_workspace(d->batch, d->nheads, d->dstate, d->block_len);
+    return BDLM_OK;
+}
+
+int bdlm_prefill_workspace(const bdlm_desc_t *d, int64_t *bytes) {
+    if (!bytes) return BDLM_E_NULL;
+    const int rc = check_desc(d, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    *bytes = bdlm::prefill_workspace(d->batch, d->nheads, d->dstate, d->block_len);
+    return BDLM_OK;
+}
+
 int bdlm_check_full_window(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                            const void *B, const void *C, const float *D, const float *D_rev,
-                           const float *y) {
-    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, nullptr, 0, nullptr,
-                                BDLM_MAX_SEQ_LEN, false);
+                           const float *y, const void *workspace, int64_t workspace_bytes) {
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, nullptr, 0, nullptr, BDLM_MAX_SEQ_LEN,
+                          false);
     if (rc != BDLM_OK) return rc;
     if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
     if (!aligned(y, 4)) return BDLM_E_ALIGN;
-    return BDLM_OK;
+    return check_workspace(workspace, workspace_bytes,
+                           bdlm::full_window_workspace(d->batch, d->nheads, d->dstate,
+                                                       d->block_len));
 }
 
 int bdlm_check_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                        const void *B, const void *C, const float *D, const float *h_pool,
                        int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,
                        const int64_t *n_blocks, int64_t expected_block_index,
-                       int64_t blocks_in_prefix) {
+                       int64_t blocks_in_prefix, const float *y_fwd, const void *workspace,
+                       int64_t workspace_bytes) {
     // D_rev is not used by a forward-only pass; D stands in for it in the checks
-    const int rc = check_common(d, x, dt, A, B, C, D, D, h_pool, nslots, slot_idx,
-                                BDLM_MAX_SEQ_LEN, true);
+    int rc = check_common(d, x, dt, A, B, C, D, D, h_pool, nslots, slot_idx, BDLM_MAX_SEQ_LEN,
+                          true);
     if (rc != BDLM_OK) return rc;
     if (blocks_in_prefix < 0) return BDLM_E_SHAPE;
+    if (!aligned(y_fwd, 4)) return BDLM_E_ALIGN;
+    rc = check_workspace(workspace, workspace_bytes,
+                         bdlm::prefill_workspace(d->batch, d->nheads, d->dstate, d->block_len));
+    if (rc != BDLM_OK) return rc;
     return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
 }
 
@@ -236,24 +277,25 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
 
 int bdlm_scan_full_window(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                           const void *B, const void *C, const float *D, const float *D_rev,
-                          float *y, void *stream) {
-    const int rc = bdlm_check_full_window(d, x, dt, A, B, C, D, D_rev, y);
+                          float *y, void *workspace, int64_t workspace_bytes, void *stream) {
+    const int rc =
+        bdlm_check_full_window(d, x, dt, A, B, C, D, D_rev, y, workspace, workspace_bytes);
     if (rc != BDLM_OK) return rc;
     const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D_rev, nullptr, nullptr, y);
-    return bdlm::launch_full_window(a, d->block_len, stream);
+    return bdlm::launch_full_window(a, d->block_len, workspace, stream);
 }
 
 int bdlm_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                  const void *B, const void *C, const float *D, float *h_pool, int64_t nslots,
                  const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
                  int64_t expected_block_index, int64_t blocks_in_prefix, float *y_fwd,
-                 void *stream) {
+                 void *workspace, int64_t workspace_bytes, void *stream) {
     int rc = bdlm_check_prefill(d, x, dt, A, B, C, D, h_pool, nslots, slot_idx, n_committed,
-                                n_blocks, expected_block_index, blocks_in_prefix);
+                                n_blocks, expected_block_index, blocks_in_prefix, y_fwd,
+                                workspace, workspace_bytes);
     if (rc != BDLM_OK) return rc;
-    if (y_fwd && !aligned(y_fwd, 4)) return BDLM_E_ALIGN;
     const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D, h_pool, slot_idx, y_fwd);
-    rc = bdlm::launch_prefill(a, d->block_len, stream);
+    rc = bdlm::launch_prefill(a, d->block_len, workspace, stream);
     if (rc != BDLM_OK) return rc;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;

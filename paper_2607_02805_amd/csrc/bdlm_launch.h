@@ -25,13 +25,49 @@ struct LaunchArgs {
 // Arguments are already validated.  Returns BDLM_OK or BDLM_E_LAUNCH.
 int launch_block(const LaunchArgs &a, bool commit, void *stream);
 
-// Full-window bidirectional scan over T tokens (a.L is ignored): forward pass,
-// then reverse pass adding into a.y.
-int launch_full_window(const LaunchArgs &a, int64_t T, void *stream);
+// How the sequence kernels cut T tokens into segments (one workgroup per batch row,
+// head and segment) and the device workspace they need: per (row, head, segment)
+// `dirs` states of 64 x dstate fp32, then one fp32 log-decay, rounded up to 256
+// bytes.  Segments are sized for about 2048 workgroups, at least 256 tokens each.
+struct SeqPlan {
+    int64_t seg_len, nseg;
+    int32_t dirs;
+    int64_t state_bytes, total_bytes;
+};
+inline SeqPlan seq_plan(int64_t batch, int64_t nheads, int64_t dstate, int64_t T, int32_t dirs) {
+    SeqPlan p;
+    p.dirs = dirs;
+    const int64_t units = batch * nheads;
+    const int64_t want = units >= 2048 ? 1 : (2048 + units - 1) / units;
+    int64_t S = (T + want - 1) / want;
+    S = (S + 63) / 64 * 64;
+    if (S < 256) S = 256;
+    p.seg_len = S;
+    p.nseg = T > 0 ? (T + S - 1) / S : 1;
+    p.state_bytes = units * p.nseg * dirs * int64_t(BDLM_HEADDIM) * dstate * 4;
+    p.total_bytes = p.state_bytes + (units * p.nseg * 4 + 255) / 256 * 256;
+    return p;
+}
+// Workspace bytes of a full window (none when the window is one segment) and of a
+// prefill.
+inline int64_t full_window_workspace(int64_t batch, int64_t nheads, int64_t dstate, int64_t T) {
+    if (batch == 0 || T == 0) return 0;
+    const SeqPlan p = seq_plan(batch, nheads, dstate, T, 2);
+    return p.nseg > 1 ? p.total_bytes : 0;
+}
+inline int64_t prefill_workspace(int64_t batch, int64_t nheads, int64_t dstate, int64_t T) {
+    if (batch == 0 || T == 0) return 0;
+    return seq_plan(batch, nheads, dstate, T, 1).total_bytes;
+}
 
-// Forward chain over T tokens continuing the states in a.h_pool (via a.slots),
+// Full-window bidirectional scan over T tokens (a.L is ignored): forward pass,
+// then reverse pass adding into a.y.  ws: full_window_workspace bytes.
+int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream);
+
+// Forward scan over T tokens continuing the states in a.h_pool (via a.slots),
 // writing them back; a.y (optional) receives the forward outputs.
-int launch_prefill(const LaunchArgs &a, int64_t T, void *stream);
+// ws: prefill_workspace bytes.
+int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream);
 
 // Permute nstates states between row-major [64][dstate] and the pool layout.
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,

@@ -1,0 +1,809 @@
+// bdlm_seq.hip -- gfx950 kernels that run the selective scan along whole sequences:
+// the full-window bidirectional scan (forward over the window from a zero state plus
+// reverse over it from a zero state, Sec. 4 and Sec. 5.1: the full-sequence scan the
+// block-restricted one replaces) and the chunked prefill of a clean prefix into the
+// cached forward states (Eq. boundary-state).
+//
+// The sequence is cut into segments of S tokens (a multiple of the 64-token chunk),
+// and every (batch row, head, segment) is one workgroup:
+//   seg_state    each segment's local states from zero -- forward F_k and, for the
+//                full window, reverse R_k -- and its total log-decay T_k;
+//   seg_combine  per state element, one pass over the segments turns these into the
+//                states entering every segment:
+//                  Sin_0 = s0,  Sin_{k+1} = 2^{T_k} Sin_k + F_k,
+//                  Rin_{K-1} = 0,  Rin_{k-1} = 2^{T_k} Rin_k + R_k,
+//                and for a prefill writes the final state 2^{T_{K-1}} Sin_{K-1} + F_{K-1}
+//                back to the cache;
+//   seg_out      the outputs of each segment in 64-token chunks from its entering state
+//                (the reverse pass adds its outputs to the forward pass's).
+// The reverse direction is the forward scan of the time-reversed sequence (every
+// token keeps its own x, dt, B, C), so seg_out loads each chunk flipped and walks
+// the segment's chunks backwards with the forward arithmetic.
+//
+// Per chunk, with l_i = dt_i A_h log2(e), inclusive sums cs_i and tot = cs_63:
+//   y_i = 2^{cs_i} (C_i . S) + sum_{j<=i} 2^{cs_i - cs_j} dt_j (C_i . B_j) x_j + skip x_i
+//   S  <- 2^{tot} S + sum_j 2^{tot - cs_j} dt_j x_j (outer) B_j
+// Tokens outside the segment load as zeros (dt = 0: decay 1, no input), which
+// changes nothing.
+//
+// Work split: 4 waves, wave w owns head-dim columns 16w .. 16w+15 of the state and
+// of y.  A chunk is staged once in LDS: B and C as row images (MFMA operands over
+// dstate), B and x transposed (operands over tokens), dt and its decay sums.  The
+// decay-weighted Gram tiles C.B^T (10 lower-triangle 16x16 tiles) are shared out
+// over the waves and published in LDS; each wave then forms its columns' y and
+// updates its state rows on bf16 MFMA, with fp32 operands split hi + lo.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bdlm.h"
+#include "bdlm_device.h"
+#include "bdlm_launch.h"
+
+namespace bdlm {
+namespace {
+
+constexpr int kC = 64;           // chunk length (tokens): one token per lane in the scan
+constexpr int kThreads = 256;    // 4 waves
+constexpr int kTiles = 10;       // lower-triangle 16x16 tiles of a 64x64 chunk
+
+struct SeqArgs {
+    const void *x, *dt, *Bm, *Cm;
+    const float *A, *skip;       // skip: D (forward) or D_rev (reverse)
+    float *y;                    // seg_out: outputs; nullptr: none
+    float *ws;                   // segment states [unit][seg][dirs][64 * N] (pool layout)
+    float *tot;                  // segment log2-decays [unit][seg]
+    int64_t xs_b, xs_t, xs_h;
+    int64_t dts_b, dts_t;
+    int64_t bcs_b, bcs_t, bcs_g;
+    int64_t T, S;                // tokens in the sequence; tokens per segment
+    int32_t nseg, dirs;
+    int32_t nheads, heads_per_group;
+    int32_t zero_init;           // seg_out: every segment starts from zero (ws unused)
+    int32_t xcd_remap;           // grid % 8 == 0: keep a (row, segment)'s heads on one XCD
+};
+
+template <int NS, bool F32>
+struct Geo {
+    static constexpr int QN = NS / 16;               // dstate tiles
+    static constexpr int E = F32 ? 4 : 8;            // activations per 16-byte load
+    static constexpr int BCPR = NS / E;              // 16-byte pieces per B / C row
+    static constexpr int BT = 16 * BCPR;             // (token quad, piece) tasks
+    static constexpr int BPT = BT > kThreads ? BT / kThreads : 1;
+    static constexpr int XCPR = kP / E;
+    static constexpr int XROWS = F32 ? 4 : 2;        // token rows per x task
+    static constexpr int XT = (kC / XROWS) * XCPR;
+    static constexpr int XPT = XT > kThreads ? XT / kThreads : 1;
+    static constexpr int IMG = 4 * QN * 64;          // quads of a row image
+    static_assert(BT % kThreads == 0 || BT < kThreads, "B tasks");
+    static_assert(XT % kThreads == 0 || XT < kThreads, "x tasks");
+};
+
+// x transposed in LDS: per (token quad g, column p) the four tokens' values.
+template <bool F32> struct XQuad;
+template <> struct XQuad<false> { using T = uint2; };
+template <> struct XQuad<true> { using T = f32x4; };
+
+__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) {   // a.lo16, b.lo16
+    return (a & 0xffffu) | (b << 16);
+}
+__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {   // a.hi16, b.hi16
+    return (a >> 16) | (b & 0xffff0000u);
+}
+__device__ __forceinline__ float ex2(float v) { return __builtin_amdgcn_exp2f(v); }
+
+// Decode the workgroup into (batch row, segment, head): consecutive units of one
+// (row, segment) share B and C, so they are kept on one XCD.
+struct Unit {
+    int b, seg, h;
+};
+__device__ __forceinline__ Unit decode(const SeqArgs &a) {
+    int u = blockIdx.x;
+    if (a.xcd_remap) u = (u & 7) * (static_cast<int>(gridDim.x) >> 3) + (u >> 3);
+    Unit r;
+    r.h = u % a.nheads;
+    const int rest = u / a.nheads;
+    r.seg = rest % a.nseg;
+    r.b = rest / a.nseg;
+    return r;
+}
+
+// One chunk's global loads into registers and their staging into LDS.
+template <int NS, bool F32, bool REV, bool LOADC>
+struct Stager {
+    using G = Geo<NS, F32>;
+    using AT = typename Act<F32>::T;
+    typedef __attribute__((address_space(1))) const AT g_at;
+
+    const AT *xg, *dtg, *Bg, *Cg;
+    int64_t xs_t, dts_t, bcs_t;
+    int64_t s0, s1;
+    u32x4 rb[G::BPT][4], rc[LOADC ? G::BPT : 1][4], rx[G::XPT][G::XROWS];
+    AT dtraw;
+
+    // global token of local token i of chunk c; false outside the segment
+    __device__ __forceinline__ bool token(int c, int i, int64_t &t) const {
+        const int64_t k = static_cast<int64_t>(c) * kC + i;
+        if constexpr (REV) {
+            t = s1 - 1 - k;
+            return t >= s0;
+        } else {
+            t = s0 + k;
+            return t < s1;
+        }
+    }
+
+    __device__ __forceinline__ void issue(int c, int tid, int wave, int lane) {
+#pragma unroll
+        for (int k = 0; k < G::BPT; ++k) {
+            const int task = tid + kThreads * k;
+            if (task < G::BT) {
+                const int g = task / G::BCPR, pc = task % G::BCPR;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    int64_t t;
+                    const bool ok = token(c, 4 * g + r, t);
+                    const int64_t o = t * bcs_t + pc * G::E;
+                    rb[k][r] = *(ok ? gchunk(Bg + o) : gzero());
+                    if constexpr (LOADC) rc[k][r] = *(ok ? gchunk(Cg + o) : gzero());
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < G::XPT; ++k) {
+            const int task = tid + kThreads * k;
+            if (task < G::XT) {
+                const int g = task / G::XCPR, pc = task % G::XCPR;
+#pragma unroll
+                for (int r = 0; r < G::XROWS; ++r) {
+                    int64_t t;
+                    const bool ok = token(c, G::XROWS * g + r, t);
+                    rx[k][r] = *(ok ? gchunk(xg + t * xs_t + pc * G::E) : gzero());
+                }
+            }
+        }
+        if (wave == 0) {
+            int64_t t;
+            const bool ok = token(c, lane, t);
+            dtraw = *(ok ? (const g_at *)(dtg + t * dts_t) : (const g_at *)(&kZeroChunk));
+        }
+    }
+
+    // Row image of B or C (operand over dstate) from one task's four token rows.
+    template <typename U2>
+    __device__ __forceinline__ static void row_image(const u32x4 (&v)[4], int g, int pc, U2 *hi,
+                                                     U2 *lo) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j = 4 * g + r;
+            if constexpr (F32) {
+                s16x4 h, l;
+                split4(__builtin_bit_cast(f32x4, v[r]), h, l);
+                const int at = img_idx<G::QN, true>(j >> 4, pc >> 2, pc & 3, j & 15);
+                hi[at] = as_u2(h);
+                lo[at] = as_u2(l);
+            } else {
+                const int q0 = 2 * pc, q1 = 2 * pc + 1;
+                hi[img_idx<G::QN, false>(j >> 4, q0 >> 2, q0 & 3, j & 15)] = uint2{v[r].x, v[r].y};
+                hi[img_idx<G::QN, false>(j >> 4, q1 >> 2, q1 & 3, j & 15)] = uint2{v[r].z, v[r].w};
+            }
+        }
+    }
+
+    // Transposed quads: out[g * stride + col] holds the four tokens 4g .. 4g+3 of
+    // column col = piece * E + e.
+    __device__ __forceinline__ static void transpose_bf16(const u32x4 (&v)[4], int base,
+                                                          uint2 *out) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            out[base + 2 * d] = uint2{lo_pair(v[0][d], v[1][d]), lo_pair(v[2][d], v[3][d])};
+            out[base + 2 * d + 1] = uint2{hi_pair(v[0][d], v[1][d]), hi_pair(v[2][d], v[3][d])};
+        }
+    }
+
+    // Write the registers of the current chunk into LDS.  bt / btl: transposed B
+    // (hi / lo), sb / sbl and sc / scl: row images, xt: transposed x.
+    __device__ __forceinline__ void stage(int tid, uint2 *sb, uint2 *sbl, uint2 *sc, uint2 *scl,
+                                          uint2 *bt, uint2 *btl,
+                                          typename XQuad<F32>::T *xt) const {
+#pragma unroll
+        for (int k = 0; k < G::BPT; ++k) {
+            const int task = tid + kThreads * k;
+            if (task < G::BT) {
+                const int g = task / G::BCPR, pc = task % G::BCPR;
+                if constexpr (LOADC) {
+                    row_image(rb[k], g, pc, sb, sbl);
+                    row_image(rc[k], g, pc, sc, scl);
+                }
+                if constexpr (F32) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const f32x4 v = {__uint_as_float(rb[k][0][e]), __uint_as_float(rb[k][1][e]),
+                                         __uint_as_float(rb[k][2][e]), __uint_as_float(rb[k][3][e])};
+                        s16x4 h, l;
+                        split4(v, h, l);
+                        bt[g * NS + pc * 4 + e] = as_u2(h);
+                        btl[g * NS + pc * 4 + e] = as_u2(l);
+                    }
+                } else {
+                    transpose_bf16(rb[k], g * NS + pc * 8, bt);
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < G::XPT; ++k) {
+            const int task = tid + kThreads * k;
+            if (task < G::XT) {
+                const int g = task / G::XCPR, pc = task % G::XCPR;
+                if constexpr (F32) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        xt[g * kP + pc * 4 + e] =
+                            f32x4{__uint_as_float(rx[k][0][e]), __uint_as_float(rx[k][1][e]),
+                                  __uint_as_float(rx[k][2][e]), __uint_as_float(rx[k][3][e])};
+                } else {
+                    // token pair g: half (g & 1) of the quads of token quad g / 2
+                    uint32_t *x32 = reinterpret_cast<uint32_t *>(xt);
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) {
+                        const int at = ((g >> 1) * kP + pc * 8 + 2 * d) * 2 + (g & 1);
+                        x32[at] = lo_pair(rx[k][0][d], rx[k][1][d]);
+                        x32[at + 2] = hi_pair(rx[k][0][d], rx[k][1][d]);
+                    }
+                }
+            }
+        }
+    }
+};
+
+// Wave 0: the chunk's decay sums.  sDt = dt, sCs = cs (inclusive, base 2),
+// sEc = 2^cs, sWs = 2^(tot - cs) dt, sWr = 2^(cs - l) dt (weights of the local
+// reverse state, relative to the chunk start).
+template <bool WITH_WR>
+__device__ __forceinline__ void decay_sums(float dtv, float A2, int lane, float *sDt, float *sCs,
+                                           float *sEc, float *sWs, float *sWr) {
+    const float l2 = dtv * A2;
+    float cs = l2;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const float v = __shfl_up(cs, off, 64);
+        if (lane >= off) cs += v;
+    }
+    const float tot = shfl(cs, 63);
+    sDt[lane] = dtv;
+    sCs[lane] = cs;
+    sEc[lane] = ex2(cs);
+    sWs[lane] = ex2(tot - cs) * dtv;
+    if constexpr (WITH_WR) sWr[lane] = ex2(cs - l2) * dtv;
+}
+
+// Operand quad of x for lane (grp, col): tokens 16jt + 4grp .. +3, column p.
+template <bool F32>
+__device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4 &hi, s16x4 &lo,
+                                          f32x4 &val) {
+    if constexpr (F32) {
+        val = v;
+        split4(v, hi, lo);
+    } else {
+        hi = as_s16x4(v);
+        val = f32x4{bf16_to_f32(hi[0]), bf16_to_f32(hi[1]), bf16_to_f32(hi[2]), bf16_to_f32(hi[3])};
+        lo = s16x4{0, 0, 0, 0};
+    }
+}
+
+// acc += B^T (quads of transposed B for dstate tile q) x (weighted x quads wh + wl):
+// the state update of one 16 x 16 (dstate, column) tile over the chunk's 64 tokens.
+template <int NS, bool F32>
+__device__ __forceinline__ f32x4 state_tile(const uint2 *bt, const uint2 *btl, int q, int grp,
+                                            int col, const s16x4 (&wh)[4], const s16x4 (&wl)[4],
+                                            f32x4 acc) {
+#pragma unroll
+    for (int jt = 0; jt < 4; jt += 2) {
+        const s16x4 a0 = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
+        const s16x4 a1 = as_s16x4(bt[(4 * (jt + 1) + grp) * NS + 16 * q + col]);
+        acc = mma_k32(a0, a1, wh[jt], wh[jt + 1], acc);
+        acc = mma_k32(a0, a1, wl[jt], wl[jt + 1], acc);
+        if constexpr (F32) {
+            const s16x4 l0 = as_s16x4(btl[(4 * jt + grp) * NS + 16 * q + col]);
+            const s16x4 l1 = as_s16x4(btl[(4 * (jt + 1) + grp) * NS + 16 * q + col]);
+            acc = mma_k32(l0, l1, wh[jt], wh[jt + 1], acc);
+        }
+    }
+    return acc;
+}
+
+// State quads of this lane in the pool layout: s[p][16q + 4grp .. +3] at
+// ((4q + grp) * 64 + p) * 4.
+__device__ __forceinline__ int quad_off(int q, int grp, int p) { return ((4 * q + grp) * kP + p) * 4; }
+
+// ------------------------------------------------------------------ seg_state
+// Local forward state F (and, BOTH, reverse state R) of one segment from zero, and
+// the segment's total log2-decay.
+template <int NS, bool F32, bool BOTH>
+__global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(const SeqArgs a) {
+    using G = Geo<NS, F32>;
+    using AT = typename Act<F32>::T;
+    constexpr int QN = G::QN;
+    __shared__ __align__(16) uint2 sBt[16 * NS];
+    __shared__ __align__(16) uint2 sBtl[F32 ? 16 * NS : 1];
+    __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
+    __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC], sWr[kC];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int p = 16 * wave + col;
+    const Unit un = decode(a);
+    const int g = un.h / a.heads_per_group;
+
+    Stager<NS, F32, false, false> st;
+    st.xg = static_cast<const AT *>(a.x) + un.b * a.xs_b + un.h * a.xs_h;
+    st.dtg = static_cast<const AT *>(a.dt) + un.b * a.dts_b + un.h;
+    st.Bg = static_cast<const AT *>(a.Bm) + un.b * a.bcs_b + g * a.bcs_g;
+    st.Cg = nullptr;
+    st.xs_t = a.xs_t;
+    st.dts_t = a.dts_t;
+    st.bcs_t = a.bcs_t;
+    st.s0 = static_cast<int64_t>(un.seg) * a.S;
+    st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
+    const float A2 = a.A[un.h] * kLog2e;
+
+    f32x4 F[QN], R[BOTH ? QN : 1];
+#pragma unroll
+    for (int q = 0; q < QN; ++q) {
+        F[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (BOTH) R[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    float off = 0.f;   // log2-decay of the segment's tokens before the current chunk
+
+    st.issue(0, tid, wave, lane);
+    for (int c = 0; c < nch; ++c) {
+        st.stage(tid, nullptr, nullptr, nullptr, nullptr, sBt, sBtl, sXt);
+        if (wave == 0)
+            decay_sums<BOTH>(Act<F32>::val(st.dtraw), A2, lane, sDt, sCs, sEc, sWs, sWr);
+        __syncthreads();
+        if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
+
+        const float tot = sCs[kC - 1];
+        s16x4 fh[4], fl[4], rh[4], rl[4];
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            s16x4 xh, xl;
+            f32x4 xv;
+            x_operand<F32>(sXt[(4 * jt + grp) * kP + p], xh, xl, xv);
+            const f32x4 wf = *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]);
+            split4(wf * xv, fh[jt], fl[jt]);
+            if constexpr (BOTH) {
+                const f32x4 wr = *reinterpret_cast<const f32x4 *>(&sWr[16 * jt + 4 * grp]);
+                split4(wr * xv * ex2(off), rh[jt], rl[jt]);
+            }
+        }
+        const float keep = ex2(tot);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+            F[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, fh, fl, F[q] * keep);
+            if constexpr (BOTH) R[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, rh, rl, R[q]);
+        }
+        off += tot;
+        __syncthreads();   // LDS is rewritten by the next chunk
+    }
+
+    const int64_t us = (static_cast<int64_t>(un.b) * a.nheads + un.h) * a.nseg + un.seg;
+    float *out = a.ws + us * a.dirs * (kP * NS);
+#pragma unroll
+    for (int q = 0; q < QN; ++q) {
+        *reinterpret_cast<f32x4 *>(out + quad_off(q, grp, p)) = F[q];
+        if constexpr (BOTH) *reinterpret_cast<f32x4 *>(out + kP * NS + quad_off(q, grp, p)) = R[q];
+    }
+    if (tid == 0) a.tot[us] = off;
+}
+
+// ------------------------------------------------------------------ seg_out
+template <int NS, bool F32, bool REV>
+__global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(const SeqArgs a) {
+    using G = Geo<NS, F32>;
+    using AT = typename Act<F32>::T;
+    constexpr int QN = G::QN;
+    constexpr int IMG = G::IMG;
+    __shared__ __align__(16) uint2 sB[IMG], sC[IMG];
+    __shared__ __align__(16) uint2 sBl[F32 ? IMG : 1], sCl[F32 ? IMG : 1];
+    __shared__ __align__(16) uint2 sBt[16 * NS];
+    __shared__ __align__(16) uint2 sBtl[F32 ? 16 * NS : 1];
+    __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
+    __shared__ __align__(16) uint4 sM[kTiles * 64];
+    __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int p = 16 * wave + col;
+    const Unit un = decode(a);
+    const int g = un.h / a.heads_per_group;
+
+    Stager<NS, F32, REV, true> st;
+    st.xg = static_cast<const AT *>(a.x) + un.b * a.xs_b + un.h * a.xs_h;
+    st.dtg = static_cast<const AT *>(a.dt) + un.b * a.dts_b + un.h;
+    st.Bg = static_cast<const AT *>(a.Bm) + un.b * a.bcs_b + g * a.bcs_g;
+    st.Cg = static_cast<const AT *>(a.Cm) + un.b * a.bcs_b + g * a.bcs_g;
+    st.xs_t = a.xs_t;
+    st.dts_t = a.dts_t;
+    st.bcs_t = a.bcs_t;
+    st.s0 = static_cast<int64_t>(un.seg) * a.S;
+    st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
+    const float A2 = a.A[un.h] * kLog2e;
+    const float skip = a.skip[un.h];
+
+    // the state entering the segment (in this direction's scan order)
+    f32x4 S[QN];
+    if (a.zero_init) {
+#pragma unroll
+        for (int q = 0; q < QN; ++q) S[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    } else {
+        const int64_t us = (static_cast<int64_t>(un.b) * a.nheads + un.h) * a.nseg + un.seg;
+        const float *src = a.ws + (us * a.dirs + (REV ? 1 : 0)) * (kP * NS);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
+    }
+    float *ybase = a.y + (static_cast<int64_t>(un.b) * a.T * a.nheads + un.h) * kP + p;
+    const int64_t ytok = static_cast<int64_t>(a.nheads) * kP;
+
+    st.issue(0, tid, wave, lane);
+    for (int c = 0; c < nch; ++c) {
+        st.stage(tid, sB, sBl, sC, sCl, sBt, sBtl, sXt);
+        if (wave == 0)
+            decay_sums<false>(Act<F32>::val(st.dtraw), A2, lane, sDt, sCs, sEc, sWs, nullptr);
+        __syncthreads();
+        if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
+
+        // decay-weighted Gram tiles M[t][j] = 2^{cs_t - cs_j} dt_j (C_t . B_j), j <= t,
+        // held as the transposed product (lane (grp, col): j = 16jt + 4grp + r, t = 16mt + col)
+        for (int k = wave; k < kTiles; k += 4) {
+            const int mt = k < 1 ? 0 : (k < 3 ? 1 : (k < 6 ? 2 : 3));
+            const int jt = k - mt * (mt + 1) / 2;
+            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < QN; q += 2) {
+                const int q1 = q + 1 < QN ? q + 1 : q;
+                const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
+                const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
+                const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
+                if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
+                else gacc = mma_k16(b0, c0, gacc);
+                if constexpr (F32) {
+                    const s16x4 bl0 = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
+                    const s16x4 bl1 = as_s16x4(sBl[img_idx<QN, F32>(jt, q1, grp, col)]);
+                    const s16x4 cl0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                    const s16x4 cl1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q1, grp, col)]);
+                    if (q + 1 < QN) {
+                        gacc = mma_k32(b0, b1, cl0, cl1, gacc);
+                        gacc = mma_k32(bl0, bl1, c0, c1, gacc);
+                    } else {
+                        gacc = mma_k16(b0, cl0, gacc);
+                        gacc = mma_k16(bl0, c0, gacc);
+                    }
+                }
+            }
+            const int t = 16 * mt + col;
+            const float cst = sCs[t];
+            const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
+            const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
+            f32x4 m;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int j = 16 * jt + 4 * grp + r;
+                const float w = ex2(cst - csj[r]) * dtj[r];
+                m[r] = j <= t ? gacc[r] * w : 0.f;
+            }
+            s16x4 mh, ml;
+            split4(m, mh, ml);
+            const uint2 h2 = as_u2(mh), l2 = as_u2(ml);
+            sM[k * 64 + lane] = uint4{h2.x, h2.y, l2.x, l2.y};
+        }
+
+        // prefix term 2^{cs_t} (C_t . S) for this wave's columns; the state is split
+        // into bf16 hi + lo one pair of dstate tiles at a time
+        f32x4 Y[4];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) Y[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < QN; q += 2) {
+            if (q + 1 < QN) {
+                s16x4 h0, l0, h1, l1;
+                split4(S[q], h0, l0);
+                split4(S[q + 1], h1, l1);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                    const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q + 1, grp, col)]);
+                    Y[mt] = mma_k32(c0, c1, h0, h1, Y[mt]);
+                    Y[mt] = mma_k32(c0, c1, l0, l1, Y[mt]);
+                    if constexpr (F32) {
+                        const s16x4 d0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                        const s16x4 d1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q + 1, grp, col)]);
+                        Y[mt] = mma_k32(d0, d1, h0, h1, Y[mt]);
+                    }
+                }
+            } else {
+                s16x4 h0, l0;
+                split4(S[q], h0, l0);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                    Y[mt] = mma_k16(c0, h0, Y[mt]);
+                    Y[mt] = mma_k16(c0, l0, Y[mt]);
+                    if constexpr (F32) {
+                        const s16x4 d0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                        Y[mt] = mma_k16(d0, h0, Y[mt]);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+            Y[mt] *= *reinterpret_cast<const f32x4 *>(&sEc[16 * mt + 4 * grp]);
+        __syncthreads();   // Gram tiles published
+
+        // x operands of this wave's columns (tokens 16jt + 4grp .. +3)
+        s16x4 xh[4], xl[4];
+        f32x4 xvf[F32 ? 4 : 1];   // fp32 storage keeps the values; bf16 re-expands xh
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            f32x4 v;
+            x_operand<F32>(sXt[(4 * jt + grp) * kP + p], xh[jt], xl[jt], v);
+            if constexpr (F32) xvf[jt] = v;
+        }
+        auto xv = [&](int jt) -> f32x4 {
+            if constexpr (F32) return xvf[jt];
+            else return f32x4{bf16_to_f32(xh[jt][0]), bf16_to_f32(xh[jt][1]),
+                              bf16_to_f32(xh[jt][2]), bf16_to_f32(xh[jt][3])};
+        };
+
+        // intra-chunk term: y += M x over j <= t
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+            for (int jt = 0; jt <= mt; jt += 2) {
+                const uint4 v0 = sM[(mt * (mt + 1) / 2 + jt) * 64 + lane];
+                const s16x4 h0 = as_s16x4(uint2{v0.x, v0.y}), l0 = as_s16x4(uint2{v0.z, v0.w});
+                if (jt + 1 <= mt) {
+                    const uint4 v1 = sM[(mt * (mt + 1) / 2 + jt + 1) * 64 + lane];
+                    const s16x4 h1 = as_s16x4(uint2{v1.x, v1.y}), l1 = as_s16x4(uint2{v1.z, v1.w});
+                    Y[mt] = mma_k32(h0, h1, xh[jt], xh[jt + 1], Y[mt]);
+                    Y[mt] = mma_k32(l0, l1, xh[jt], xh[jt + 1], Y[mt]);
+                    if constexpr (F32) Y[mt] = mma_k32(h0, h1, xl[jt], xl[jt + 1], Y[mt]);
+                } else {
+                    Y[mt] = mma_k16(h0, xh[jt], Y[mt]);
+                    Y[mt] = mma_k16(l0, xh[jt], Y[mt]);
+                    if constexpr (F32) Y[mt] = mma_k16(h0, xl[jt], Y[mt]);
+                }
+            }
+        }
+
+        // skip term and store (lane (grp, col): token 16mt + 4grp + r, column p)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const f32x4 out = Y[mt] + skip * xv(mt);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                int64_t t;
+                if (st.token(c, 16 * mt + 4 * grp + r, t)) {
+                    // the reverse pass adds onto the forward pass's outputs in L2
+                    // (one addend per element: the sum is exact fp32 and deterministic)
+                    if constexpr (REV)
+                        __hip_atomic_fetch_add(ybase + t * ytok, out[r], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                    else
+                        __builtin_nontemporal_store(out[r], ybase + t * ytok);
+                }
+            }
+        }
+
+        // carry the state across the chunk
+        const float keep = ex2(sCs[kC - 1]);
+        s16x4 wh[4], wl[4];
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            const f32x4 w = *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]);
+            split4(w * xv(jt), wh[jt], wl[jt]);
+        }
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+            S[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, wh, wl, S[q] * keep);
+            // keep the operand reads of one tile at a time in registers
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __syncthreads();   // LDS is rewritten by the next chunk
+    }
+}
+
+// ------------------------------------------------------------------ seg_combine
+struct CombineArgs {
+    float *ws;
+    const float *tot;
+    float *pool;                 // prefill: initial states read, final states written
+    int64_t units, state_floats; // (row, head) pairs; 64 * N
+    int32_t nseg, dirs, nheads;
+    int32_t use_slots;
+    int32_t slots[BDLM_MAX_SLOT_ROWS];
+};
+
+// One thread per 16-byte quad of a (row, head)'s state: the exclusive scans over
+// the segments in both directions, in place.
+__global__ void __launch_bounds__(256) bdlm_seg_combine_kernel(const CombineArgs c) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t qps = c.state_floats / 4;
+    if (i >= c.units * qps) return;
+    const int64_t unit = i / qps, e = (i % qps) * 4;
+    const float *tot = c.tot + unit * c.nseg;
+    float *base = c.ws + unit * c.nseg * c.dirs * c.state_floats + e;
+    const int64_t seg_stride = c.dirs * c.state_floats;
+
+    float *pst = nullptr;
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    if (c.pool) {
+        const int64_t b = unit / c.nheads, h = unit % c.nheads;
+        const int64_t slot = c.use_slots ? c.slots[b] : b;
+        pst = c.pool + (slot * c.nheads + h) * c.state_floats + e;
+        s = *reinterpret_cast<const f32x4 *>(pst);
+    }
+    for (int k = 0; k < c.nseg; ++k) {
+        f32x4 *f = reinterpret_cast<f32x4 *>(base + k * seg_stride);
+        const f32x4 fk = *f;
+        *f = s;
+        s = s * ex2(tot[k]) + fk;
+    }
+    if (pst) *reinterpret_cast<f32x4 *>(pst) = s;
+    if (c.dirs == 2) {
+        f32x4 r = {0.f, 0.f, 0.f, 0.f};
+        for (int k = c.nseg - 1; k >= 0; --k) {
+            f32x4 *f = reinterpret_cast<f32x4 *>(base + k * seg_stride + c.state_floats);
+            const f32x4 rk = *f;
+            *f = r;
+            r = r * ex2(tot[k]) + rk;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ host side
+template <int NS, bool F32>
+hipError_t state_launch(const SeqArgs &k, bool both, unsigned grid, hipStream_t s) {
+    if (both)
+        hipLaunchKernelGGL((bdlm_seg_state_kernel<NS, F32, true>), dim3(grid), dim3(kThreads), 0, s, k);
+    else
+        hipLaunchKernelGGL((bdlm_seg_state_kernel<NS, F32, false>), dim3(grid), dim3(kThreads), 0, s, k);
+    return hipGetLastError();
+}
+template <int NS, bool F32>
+hipError_t out_launch(const SeqArgs &k, bool rev, unsigned grid, hipStream_t s) {
+    if (rev)
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, true>), dim3(grid), dim3(kThreads), 0, s, k);
+    else
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false>), dim3(grid), dim3(kThreads), 0, s, k);
+    return hipGetLastError();
+}
+
+template <bool F32>
+hipError_t run_state(int ns, const SeqArgs &k, bool both, unsigned grid, hipStream_t s) {
+    switch (ns) {
+        case 16: return state_launch<16, F32>(k, both, grid, s);
+        case 32: return state_launch<32, F32>(k, both, grid, s);
+        case 64: return state_launch<64, F32>(k, both, grid, s);
+        case 128: return state_launch<128, F32>(k, both, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+template <bool F32>
+hipError_t run_out(int ns, const SeqArgs &k, bool rev, unsigned grid, hipStream_t s) {
+    switch (ns) {
+        case 16: return out_launch<16, F32>(k, rev, grid, s);
+        case 32: return out_launch<32, F32>(k, rev, grid, s);
+        case 64: return out_launch<64, F32>(k, rev, grid, s);
+        case 128: return out_launch<128, F32>(k, rev, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+SeqArgs seq_args(const LaunchArgs &a, int64_t T, const SeqPlan &pl, void *ws) {
+    SeqArgs k;
+    k.x = a.x;
+    k.dt = a.dt;
+    k.Bm = a.Bm;
+    k.Cm = a.Cm;
+    k.A = a.A;
+    k.skip = a.D;
+    k.y = a.y;
+    k.ws = static_cast<float *>(ws);
+    k.tot = ws ? static_cast<float *>(ws) + pl.state_bytes / 4 : nullptr;
+    k.xs_b = a.xs_b;
+    k.xs_t = a.xs_t;
+    k.xs_h = a.xs_h;
+    k.dts_b = a.dts_b;
+    k.dts_t = a.dts_t;
+    k.bcs_b = a.bcs_b;
+    k.bcs_t = a.bcs_t;
+    k.bcs_g = a.bcs_g;
+    k.T = T;
+    k.S = pl.seg_len;
+    k.nseg = static_cast<int32_t>(pl.nseg);
+    k.dirs = pl.dirs;
+    k.nheads = a.nheads;
+    k.heads_per_group = a.nheads / a.ngroups;
+    k.zero_init = 1;
+    const int64_t grid = static_cast<int64_t>(a.batch) * a.nheads * pl.nseg;
+    k.xcd_remap = grid % 8 == 0 ? 1 : 0;
+    return k;
+}
+
+hipError_t combine(const LaunchArgs &a, const SeqPlan &pl, const SeqArgs &k, float *pool,
+                   hipStream_t s) {
+    CombineArgs c;
+    c.ws = k.ws;
+    c.tot = k.tot;
+    c.pool = pool;
+    c.units = static_cast<int64_t>(a.batch) * a.nheads;
+    c.state_floats = static_cast<int64_t>(kP) * a.dstate;
+    c.nseg = static_cast<int32_t>(pl.nseg);
+    c.dirs = pl.dirs;
+    c.nheads = a.nheads;
+    c.use_slots = a.slots ? 1 : 0;
+    for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
+        c.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
+    const int64_t threads = c.units * (c.state_floats / 4);
+    const unsigned grid = static_cast<unsigned>((threads + 255) / 256);
+    hipLaunchKernelGGL(bdlm_seg_combine_kernel, dim3(grid), dim3(256), 0, s, c);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
+    if (a.batch == 0 || T == 0) return BDLM_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const SeqPlan pl = seq_plan(a.batch, a.nheads, a.dstate, T, 2);
+    SeqArgs k = seq_args(a, T, pl, pl.nseg > 1 ? ws : nullptr);
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * pl.nseg);
+    const bool f32 = !a.bf16;
+    if (pl.nseg > 1) {
+        // local states, then the states entering every segment
+        if ((f32 ? run_state<true>(a.dstate, k, true, grid, s)
+                 : run_state<false>(a.dstate, k, true, grid, s)) != hipSuccess)
+            return BDLM_E_LAUNCH;
+        if (combine(a, pl, k, nullptr, s) != hipSuccess) return BDLM_E_LAUNCH;
+        k.zero_init = 0;
+    }
+    k.skip = a.D;
+    if ((f32 ? run_out<true>(a.dstate, k, false, grid, s) : run_out<false>(a.dstate, k, false, grid, s)) !=
+        hipSuccess)
+        return BDLM_E_LAUNCH;
+    k.skip = a.D_rev;
+    if ((f32 ? run_out<true>(a.dstate, k, true, grid, s) : run_out<false>(a.dstate, k, true, grid, s)) !=
+        hipSuccess)
+        return BDLM_E_LAUNCH;
+    return BDLM_OK;
+}
+
+int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
+    if (a.batch == 0 || T == 0) return BDLM_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const SeqPlan pl = seq_plan(a.batch, a.nheads, a.dstate, T, 1);
+    SeqArgs k = seq_args(a, T, pl, ws);
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * pl.nseg);
+    const bool f32 = !a.bf16;
+    if ((f32 ? run_state<true>(a.dstate, k, false, grid, s)
+             : run_state<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+        return BDLM_E_LAUNCH;
+    // the cached states enter segment 0; the final states go back to the cache
+    if (combine(a, pl, k, a.h_pool, s) != hipSuccess) return BDLM_E_LAUNCH;
+    if (a.y) {
+        k.zero_init = 0;
+        k.skip = a.D;
+        if ((f32 ? run_out<true>(a.dstate, k, false, grid, s)
+                 : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+            return BDLM_E_LAUNCH;
+    }
+    return BDLM_OK;
+}
+
+}  // namespace bdlm

@@ -61,7 +61,7 @@ def test_exports_every_declared_function(L):
 
 
 def test_strerror(L):
-    for code in (0, -1, -2, -3, -4, -5, -6, -7):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert bd.strerror(code) and bd.strerror(code) != "unknown status"
     assert bd.strerror(12345) == "unknown status"
 
@@ -189,16 +189,28 @@ def test_entry_points_reject_before_launch(L):
     assert L.bdlm_cache_reset(FAKE, 4, 1024, i32p(bad), 1, None, None, None) == bd.E_SLOT
 
 
-def check_window(L, d, p):
+WS = FAKE + 0x100000           # a 256-byte aligned fake workspace
+BIG = 1 << 40                  # "large enough" workspace size
+
+
+def ws_bytes(L, fn, d):
+    n = ctypes.c_int64(-1)
+    assert getattr(L, fn)(ctypes.byref(d), ctypes.byref(n)) == bd.OK
+    return n.value
+
+
+def check_window(L, d, p, ws=WS, wsb=BIG):
     return L.bdlm_check_full_window(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
-                                    p["D"], p["Drev"], p["y"])
+                                    p["D"], p["Drev"], p["y"], ws, wsb)
 
 
-def check_prefill(L, d, p, nslots=4, slots=None, nc=None, nb=None, expect=-1, blocks=0):
+def check_prefill(L, d, p, nslots=4, slots=None, nc=None, nb=None, expect=-1, blocks=0,
+                  yf=None, ws=WS, wsb=BIG):
     nc = np.zeros(nslots, np.int64) if nc is None else nc
     nb = np.zeros(nslots, np.int64) if nb is None else nb
     return L.bdlm_check_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
-                                p["h"], nslots, i32p(slots), i64p(nc), i64p(nb), expect, blocks)
+                                p["h"], nslots, i32p(slots), i64p(nc), i64p(nb), expect, blocks,
+                                yf, ws, wsb)
 
 
 def test_sequence_entry_points_accept_long_sequences(L):
@@ -222,7 +234,7 @@ def test_full_window_checks(L):
     assert check_window(L, desc(), ptrs(x=FAKE + 8)) == bd.E_ALIGN
     assert check_window(L, desc(N=48), ptrs()) == bd.E_SHAPE
     assert L.bdlm_check_full_window(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                    FAKE) == bd.E_NULL
+                                    FAKE, WS, BIG) == bd.E_NULL
 
 
 def test_prefill_checks(L):
@@ -238,7 +250,9 @@ def test_prefill_checks(L):
     assert check_prefill(L, d, ptrs(h=None)) == bd.E_NULL
     assert check_prefill(L, d, ptrs(h=FAKE + 0x7008)) == bd.E_ALIGN
     assert L.bdlm_check_prefill(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4,
-                                None, None, None, -1, 0) == bd.E_NULL
+                                None, None, None, -1, 0, None, WS, BIG) == bd.E_NULL
+    assert check_prefill(L, d, ptrs(), yf=FAKE + 0x9004) == bd.OK
+    assert check_prefill(L, d, ptrs(), yf=FAKE + 0x9002) == bd.E_ALIGN
 
 
 def test_row_limit(L):
@@ -253,13 +267,52 @@ def test_sequence_entry_points_reject_before_launch(L):
     d = desc(batch=2, L=1000)
     p = ptrs(x=None)
     assert L.bdlm_scan_full_window(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
-                                   p["D"], p["Drev"], p["y"], None) == bd.E_NULL
+                                   p["D"], p["Drev"], p["y"], WS, BIG, None) == bd.E_NULL
     nc, nb = np.array([64, 64, 0, 0], np.int64), np.array([2, 2, 0, 0], np.int64)
     p = ptrs()
     rc = L.bdlm_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["h"],
-                        4, None, i64p(nc), i64p(nb), 3, 31, None, None)
+                        4, None, i64p(nc), i64p(nb), 3, 31, None, WS, BIG, None)
     assert rc == bd.E_OFFSET
     assert nc.tolist() == [64, 64, 0, 0] and nb.tolist() == [2, 2, 0, 0]   # untouched
     rc = L.bdlm_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["h"],
-                        4, None, i64p(nc), i64p(nb), 2, 31, FAKE + 2, None)
+                        4, None, i64p(nc), i64p(nb), 2, 31, FAKE + 2, WS, BIG, None)
     assert rc == bd.E_ALIGN
+    rc = L.bdlm_prefill(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"], p["h"],
+                        4, None, i64p(nc), i64p(nb), 2, 31, None, None, 0, None)
+    assert rc == bd.E_WORKSPACE
+    assert nc.tolist() == [64, 64, 0, 0] and nb.tolist() == [2, 2, 0, 0]
+
+
+def test_workspace_sizes(L):
+    """Segments of >= 256 tokens sized for ~2048 workgroups; per (row, head, segment)
+    one state per direction plus one float, rounded up to 256 bytes."""
+    d = desc(batch=4, H=32, N=128, L=65536)
+    nseg = 16                                  # 128 (row, head) pairs -> 16 segments of 4096
+    states = 4 * 32 * nseg * 64 * 128 * 4
+    assert ws_bytes(L, "bdlm_full_window_workspace", d) == 2 * states + (4 * 32 * nseg * 4 + 255) // 256 * 256
+    assert ws_bytes(L, "bdlm_prefill_workspace", d) == states + (4 * 32 * nseg * 4 + 255) // 256 * 256
+    # a window that is one segment needs no workspace; a prefill always does
+    d1 = desc(batch=2, H=3, N=16, L=200)
+    assert ws_bytes(L, "bdlm_full_window_workspace", d1) == 0
+    assert ws_bytes(L, "bdlm_prefill_workspace", d1) == 2 * 3 * 64 * 16 * 4 + 256
+    assert ws_bytes(L, "bdlm_prefill_workspace", desc(batch=0, L=100)) == 0
+    n = ctypes.c_int64(0)
+    assert L.bdlm_full_window_workspace(ctypes.byref(desc(N=48)), ctypes.byref(n)) == bd.E_SHAPE
+    assert L.bdlm_prefill_workspace(ctypes.byref(desc()), None) == bd.E_NULL
+
+
+def test_workspace_checks(L):
+    d = desc(batch=1, H=2, N=32, L=1000)        # several segments
+    need = ws_bytes(L, "bdlm_full_window_workspace", d)
+    assert need > 0
+    assert check_window(L, d, ptrs(), WS, need) == bd.OK
+    assert check_window(L, d, ptrs(), WS, need - 1) == bd.E_WORKSPACE
+    assert check_window(L, d, ptrs(), None, need) == bd.E_WORKSPACE
+    assert check_window(L, d, ptrs(), WS + 16, need) == bd.E_ALIGN
+    assert check_window(L, d, ptrs(), WS, -1) == bd.E_SHAPE
+    d1 = desc(batch=2, H=3, N=16, L=200)        # one segment: no workspace needed
+    assert check_window(L, d1, ptrs(), None, 0) == bd.OK
+    needp = ws_bytes(L, "bdlm_prefill_workspace", d)
+    assert check_prefill(L, d, ptrs(), ws=WS, wsb=needp) == bd.OK
+    assert check_prefill(L, d, ptrs(), ws=WS, wsb=needp - 4) == bd.E_WORKSPACE
+    assert bd.strerror(bd.E_WORKSPACE) != "unknown status"

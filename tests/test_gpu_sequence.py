@@ -1,9 +1,13 @@
-"""GPU parity of the sequence-length kernels against the fp64 oracle:
+"""GPU parity of the sequence entry points against the fp64 oracle:
 
 * bdlm_scan_full_window -- forward over the whole window from zero plus reverse over the
   whole window from zero (the full-sequence contrast);
-* bdlm_prefill -- a clean prefix summarised into the cached states in one launch, which
-  must equal committing it block by block.
+* bdlm_prefill -- a clean prefix summarised into the cached states, which must equal
+  committing it block by block.
+
+Both cut the sequence into segments of >= 256 tokens (one workgroup per row, head and
+segment; the states entering each segment come from a combine pass over the segments'
+local states), so cases span one segment, several segments and a ragged last segment.
 
 Bar: max relative error 2e-3 (tests/gpu_util.py); bookkeeping bit-exact.
 """
@@ -56,6 +60,41 @@ def test_full_window_fp32_storage(N, W):
     y = full_window(d)
     torch.cuda.synchronize()
     assert rel_err(y, oracle.full_window(d)) <= REL_TOL
+
+
+@pytest.mark.parametrize("N", [16, 32, 64, 128])
+@pytest.mark.parametrize("bf16", [True, False])
+def test_full_window_segments(N, bf16):
+    """1 row x 2 heads over 1000 tokens: four segments of 256, the last one ragged."""
+    import paper_2607_02805_amd as bd
+    assert bd.full_window_workspace_bytes(1, 2, N, 1000) > 0
+    w = wl(1, 2, N, 1000, bf16=bf16, seed=9250 + N)
+    d = bi.block_inputs(w, 0)
+    d["D_rev"] = (d["D"] * 0.5).astype(np.float32)
+    say("full window segments", w)
+    y = full_window(d)
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.full_window(d))
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
+def test_full_window_caller_workspace_and_determinism():
+    import paper_2607_02805_amd as bd
+    w = wl(2, 3, 64, 1500, seed=9270)
+    d = bi.block_inputs(w, 0)
+    v = to_dev(d)
+    need = bd.full_window_workspace_bytes(2, 3, 64, 1500)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    args = (v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"])
+    y1 = bd.scan_full_window(*args, workspace=ws)
+    y2 = bd.scan_full_window(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)                       # bitwise, run to run
+    assert rel_err(y1, oracle.full_window(d)) <= REL_TOL
+    with pytest.raises(bd.BdlmError) as ei:
+        bd.scan_full_window(*args, workspace=ws[:need - 256])
+    assert ei.value.code == bd.E_WORKSPACE
 
 
 def test_full_window_groups_and_long():
@@ -155,6 +194,21 @@ def test_prefill_equals_commits():
     assert a.n_committed.tolist() == b.n_committed.tolist() == [2048, 2048]
     ref = oracle.scan_forward(pre)
     assert rel_err(a.states(), ref) <= REL_TOL and rel_err(b.states(), ref) <= REL_TOL
+
+
+def test_prefill_fp32_storage_segments():
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, 3, 64, 32, 1, 32, 1300, False, 1, 9650)
+    pre = bi.prefix_inputs(w)
+    s0 = bi.random_state(w, 2, 4, 0.5)
+    cache = bd.Cache(2, 3, 32)
+    cache.h.copy_(pool_dev(s0))
+    v = to_dev(pre)
+    yf = cache.prefill(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], y_fwd=True)
+    torch.cuda.synchronize()
+    s_ref, y_ref = oracle.scan_forward(pre, s0.astype(np.float64), want_y=True)
+    assert rel_err(from_pool(cache.h), s_ref) <= REL_TOL
+    assert rel_err(yf, y_ref) <= REL_TOL
 
 
 def test_prefill_rejects_wrong_block_index():
