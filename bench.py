@@ -300,9 +300,11 @@ def run_contrast(args, block: dict) -> dict:
     fb = full_window_bytes(w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, w.block_len)
     # per-sequence time of one denoising step: the full window serves w.batch sequences per
     # call; the block step serves 16 per launch, plus the commit once every p steps
-    s = block["shape"]
     t_seq_full = t_full / w.batch
-    t_seq_block = (block["avg_step_us"] + block["avg_commit_us"] / args.denoise) * 1e-6 / s["batch"]
+    t_seq_block = None
+    if block is not None:
+        t_seq_block = (block["avg_step_us"] + block["avg_commit_us"] / args.denoise) * 1e-6 \
+            / block["shape"]["batch"]
     del v, y
     torch.cuda.empty_cache()
     return {
@@ -313,8 +315,9 @@ def run_contrast(args, block: dict) -> dict:
         "achieved_gbs": round(fb / t_full / 1e9, 1),
         "frac": round(fb / t_full / 1e9 / HBM_PEAK_GBS, 4),
         "per_sequence_step_us": {"full_window": round(t_seq_full * 1e6, 3),
-                                 "block_restricted": round(t_seq_block * 1e6, 4)},
-        "ratio": round(t_seq_full / t_seq_block, 1),
+                                 "block_restricted": None if t_seq_block is None
+                                 else round(t_seq_block * 1e6, 4)},
+        "ratio": None if t_seq_block is None else round(t_seq_full / t_seq_block, 1),
     }
 
 
@@ -517,6 +520,8 @@ def main():
                     help="timed block cycles per point of the flatness sweep")
     ap.add_argument("--contrast-reps", type=int, default=3)
     ap.add_argument("--prefill-tokens", type=int, default=16384)
+    ap.add_argument("--sequence-only", action="store_true",
+                    help="only time the full-window contrast and the prefill (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (counter calibration) and exit")
     ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
@@ -544,6 +549,13 @@ def main():
               "(batch, head) with no exchange, so there is no multi-GPU path to time.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.sequence_only:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps({"contrast": run_contrast(args, None), "prefill": run_prefill(args)}),
+              flush=True)
+        return
 
     r = run_gpu(args)
     extras = {}

@@ -184,6 +184,8 @@ int bdlm_prefill_workspace(const bdlm_desc_t *desc, int64_t *bytes);
  * desc.block_len is the window length, 0 .. BDLM_MAX_SEQ_LEN; every other argument
  * is as for bdlm_scan_block_step with block_len set to the window (y is
  * [batch][window][nheads][64] fp32, 4-byte aligned).
+ * Strides: every per-token stride (x, dt, B/C) and nheads * 64 * 4 (y's) at most
+ * 16 MiB, else BDLM_E_SHAPE.
  * workspace    device memory of at least bdlm_full_window_workspace bytes,
  *              256-byte aligned (may be NULL when that size is 0); its contents
  *              are scratch, overwritten by the call.  Calls that share a
@@ -209,6 +211,7 @@ int bdlm_scan_full_window(const bdlm_desc_t *desc, const void *x, const void *dt
  * y_fwd        fp32 [batch][len][nheads][64] (4-byte aligned) or NULL: the forward
  *              outputs (skip D) of the prefix tokens.  D_rev is not used.
  * workspace    at least bdlm_prefill_workspace bytes, 256-byte aligned; scratch.
+ * Strides as for bdlm_scan_full_window.
  * Errors: as bdlm_commit_boundary, and BDLM_E_WORKSPACE.
  */
 int bdlm_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,

@@ -184,6 +184,18 @@ int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const
     return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
 }
 
+// The sequence kernels address a 64-token chunk with 32-bit byte offsets from a
+// per-chunk base: every per-token stride (and y's, nheads x 64 floats) stays below
+// 16 MiB.
+static int check_seq_strides(const bdlm_desc_t *d) {
+    constexpr int64_t kMaxRow = int64_t(1) << 24;
+    const int64_t es = elem_size(d->in_dtype);
+    if (d->x_stride[1] * es > kMaxRow || d->bc_stride[1] * es > kMaxRow ||
+        d->dt_stride[1] * es > kMaxRow || d->nheads * BDLM_HEADDIM * 4 > kMaxRow)
+        return BDLM_E_SHAPE;
+    return BDLM_OK;
+}
+
 static int check_workspace(const void *ws, int64_t ws_bytes, int64_t need) {
     if (ws_bytes < 0) return BDLM_E_SHAPE;
     if (need == 0) return BDLM_OK;
@@ -215,6 +227,8 @@ int bdlm_check_full_window(const bdlm_desc_t *d, const void *x, const void *dt, 
     int rc = check_common(d, x, dt, A, B, C, D, D_rev, nullptr, 0, nullptr, BDLM_MAX_SEQ_LEN,
                           false);
     if (rc != BDLM_OK) return rc;
+    rc = check_seq_strides(d);
+    if (rc != BDLM_OK) return rc;
     if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
     if (!aligned(y, 4)) return BDLM_E_ALIGN;
     return check_workspace(workspace, workspace_bytes,
@@ -231,6 +245,8 @@ int bdlm_check_prefill(const bdlm_desc_t *d, const void *x, const void *dt, cons
     // D_rev is not used by a forward-only pass; D stands in for it in the checks
     int rc = check_common(d, x, dt, A, B, C, D, D, h_pool, nslots, slot_idx, BDLM_MAX_SEQ_LEN,
                           true);
+    if (rc != BDLM_OK) return rc;
+    rc = check_seq_strides(d);
     if (rc != BDLM_OK) return rc;
     if (blocks_in_prefix < 0) return BDLM_E_SHAPE;
     if (!aligned(y_fwd, 4)) return BDLM_E_ALIGN;

@@ -107,44 +107,82 @@ __device__ __forceinline__ Unit decode(const SeqArgs &a) {
     return r;
 }
 
-// One chunk's global loads into registers and their staging into LDS.
+// Buffer resources: chunks are addressed from a per-chunk base (uniform, in scalar
+// registers) plus a fixed per-thread byte offset.  Rows outside the segment get an
+// offset past the resource's range: their loads return zeros and their stores are
+// dropped, with no branch.
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
+                                             0x7fffffff, 0x00020000);
+}
+constexpr int kNT = 2;   // buffer cache policy: nontemporal
+
+// One chunk's global loads into registers and their staging into LDS.  Local token
+// i of chunk c is the segment's token 64c + i (reverse: its 64c + i-th token from
+// the end); row(i) is its position in the chunk's memory window.
 template <int NS, bool F32, bool REV, bool LOADC>
 struct Stager {
     using G = Geo<NS, F32>;
-    using AT = typename Act<F32>::T;
-    typedef __attribute__((address_space(1))) const AT g_at;
+    static constexpr int ES = F32 ? 4 : 2;
 
-    const AT *xg, *dtg, *Bg, *Cg;
-    int64_t xs_t, dts_t, bcs_t;
+    const char *xg, *dtg, *Bg, *Cg;  // this (row, head / group) at token 0
+    int64_t xrow, dtrow, bcrow;      // bytes between consecutive tokens
     int64_t s0, s1;
+    uint32_t ob[G::BPT][4], ox[G::XPT][G::XROWS], odt;   // per-thread byte offsets
     u32x4 rb[G::BPT][4], rc[LOADC ? G::BPT : 1][4], rx[G::XPT][G::XROWS];
-    AT dtraw;
+    uint32_t dtraw;
 
+    __device__ __forceinline__ static int row(int i) { return REV ? kC - 1 - i : i; }
+
+    // first token of chunk c's memory window, and the number of valid local tokens
+    __device__ __forceinline__ int64_t window(int c) const {
+        return REV ? s1 - static_cast<int64_t>(kC) * (c + 1) : s0 + static_cast<int64_t>(kC) * c;
+    }
+    __device__ __forceinline__ int valid(int c) const {
+        const int64_t v = (s1 - s0) - static_cast<int64_t>(kC) * c;
+        return v < kC ? static_cast<int>(v) : kC;
+    }
     // global token of local token i of chunk c; false outside the segment
     __device__ __forceinline__ bool token(int c, int i, int64_t &t) const {
-        const int64_t k = static_cast<int64_t>(c) * kC + i;
-        if constexpr (REV) {
-            t = s1 - 1 - k;
-            return t >= s0;
-        } else {
-            t = s0 + k;
-            return t < s1;
+        t = window(c) + row(i);
+        return i < valid(c);
+    }
+
+    __device__ __forceinline__ void init(int tid, int lane) {
+#pragma unroll
+        for (int k = 0; k < G::BPT; ++k) {
+            const int task = tid + kThreads * k, g = task / G::BCPR, pc = task % G::BCPR;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                ob[k][r] = static_cast<uint32_t>(row(4 * g + r) * bcrow + pc * 16);
         }
+#pragma unroll
+        for (int k = 0; k < G::XPT; ++k) {
+            const int task = tid + kThreads * k, g = task / G::XCPR, pc = task % G::XCPR;
+#pragma unroll
+            for (int r = 0; r < G::XROWS; ++r)
+                ox[k][r] = static_cast<uint32_t>(row(G::XROWS * g + r) * xrow + pc * 16);
+        }
+        odt = static_cast<uint32_t>(row(lane) * dtrow);
     }
 
     __device__ __forceinline__ void issue(int c, int tid, int wave, int lane) {
+        const int64_t w = window(c);
+        const int lim = valid(c);
+        const __amdgpu_buffer_rsrc_t rB = rsrc(Bg + w * bcrow);
+        const __amdgpu_buffer_rsrc_t rC = rsrc(Cg + w * bcrow);
+        const __amdgpu_buffer_rsrc_t rX = rsrc(xg + w * xrow);
 #pragma unroll
         for (int k = 0; k < G::BPT; ++k) {
             const int task = tid + kThreads * k;
             if (task < G::BT) {
-                const int g = task / G::BCPR, pc = task % G::BCPR;
+                const int g = task / G::BCPR;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    int64_t t;
-                    const bool ok = token(c, 4 * g + r, t);
-                    const int64_t o = t * bcs_t + pc * G::E;
-                    rb[k][r] = *(ok ? gchunk(Bg + o) : gzero());
-                    if constexpr (LOADC) rc[k][r] = *(ok ? gchunk(Cg + o) : gzero());
+                    const uint32_t o = 4 * g + r < lim ? ob[k][r] : kOOB;
+                    rb[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rB, o, 0, 0);
+                    if constexpr (LOADC) rc[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rC, o, 0, 0);
                 }
             }
         }
@@ -152,20 +190,24 @@ struct Stager {
         for (int k = 0; k < G::XPT; ++k) {
             const int task = tid + kThreads * k;
             if (task < G::XT) {
-                const int g = task / G::XCPR, pc = task % G::XCPR;
+                const int g = task / G::XCPR;
 #pragma unroll
                 for (int r = 0; r < G::XROWS; ++r) {
-                    int64_t t;
-                    const bool ok = token(c, G::XROWS * g + r, t);
-                    rx[k][r] = *(ok ? gchunk(xg + t * xs_t + pc * G::E) : gzero());
+                    const uint32_t o = G::XROWS * g + r < lim ? ox[k][r] : kOOB;
+                    rx[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rX, o, 0, 0);
                 }
             }
         }
         if (wave == 0) {
-            int64_t t;
-            const bool ok = token(c, lane, t);
-            dtraw = *(ok ? (const g_at *)(dtg + t * dts_t) : (const g_at *)(&kZeroChunk));
+            const __amdgpu_buffer_rsrc_t rD = rsrc(dtg + w * dtrow);
+            const uint32_t o = lane < lim ? odt : kOOB;
+            if constexpr (F32) dtraw = __builtin_amdgcn_raw_buffer_load_b32(rD, o, 0, 0);
+            else dtraw = __builtin_amdgcn_raw_buffer_load_b16(rD, o, 0, 0);
         }
+    }
+
+    __device__ __forceinline__ float dt_value() const {
+        return F32 ? __uint_as_float(dtraw) : __uint_as_float(dtraw << 16);
     }
 
     // Row image of B or C (operand over dstate) from one task's four token rows.
@@ -258,17 +300,31 @@ struct Stager {
 // Wave 0: the chunk's decay sums.  sDt = dt, sCs = cs (inclusive, base 2),
 // sEc = 2^cs, sWs = 2^(tot - cs) dt, sWr = 2^(cs - l) dt (weights of the local
 // reverse state, relative to the chunk start).
+// Inclusive sum over the 64 lanes of a wave on DPP, without LDS: shifts by 1, 2, 4, 8
+// within each row of 16 lanes (lanes shifted in from outside the row read 0), then
+// row 0's total into row 1 (and row 2's into row 3), then the total of rows 0-1 into
+// rows 2-3.
+template <int CTRL, int ROW_MASK, bool BOUND_ZERO>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf,
+                                                      BOUND_ZERO));
+}
+__device__ __forceinline__ float wave_inclusive_sum(float v) {
+    v += dpp<0x111, 0xf, true>(v);   // row_shr:1
+    v += dpp<0x112, 0xf, true>(v);   // row_shr:2
+    v += dpp<0x114, 0xf, true>(v);   // row_shr:4
+    v += dpp<0x118, 0xf, true>(v);   // row_shr:8
+    v += dpp<0x142, 0xa, false>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp<0x143, 0xc, false>(v);  // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 template <bool WITH_WR>
 __device__ __forceinline__ void decay_sums(float dtv, float A2, int lane, float *sDt, float *sCs,
                                            float *sEc, float *sWs, float *sWr) {
     const float l2 = dtv * A2;
-    float cs = l2;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const float v = __shfl_up(cs, off, 64);
-        if (lane >= off) cs += v;
-    }
-    const float tot = shfl(cs, 63);
+    const float cs = wave_inclusive_sum(l2);
+    const float tot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cs), 63));
     sDt[lane] = dtv;
     sCs[lane] = cs;
     sEc[lane] = ex2(cs);
@@ -290,23 +346,30 @@ __device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4
     }
 }
 
-// acc += B^T (quads of transposed B for dstate tile q) x (weighted x quads wh + wl):
-// the state update of one 16 x 16 (dstate, column) tile over the chunk's 64 tokens.
+// The transposed-B operand quads of dstate tile q (tokens 16jt + 4grp .. +3,
+// column 16q + col) and the state update of one 16 x 16 (dstate, column) tile over
+// the chunk's 64 tokens: acc += B^T (wh + wl), wh + wl the weighted x quads.
+template <bool F32>
+struct BtOps {
+    s16x4 h[4], l[F32 ? 4 : 1];
+};
 template <int NS, bool F32>
-__device__ __forceinline__ f32x4 state_tile(const uint2 *bt, const uint2 *btl, int q, int grp,
-                                            int col, const s16x4 (&wh)[4], const s16x4 (&wl)[4],
-                                            f32x4 acc) {
+__device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, const uint2 *btl, int q,
+                                        int grp, int col) {
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+        o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
+        if constexpr (F32) o.l[jt] = as_s16x4(btl[(4 * jt + grp) * NS + 16 * q + col]);
+    }
+}
+template <bool F32>
+__device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const s16x4 (&wh)[4],
+                                        const s16x4 (&wl)[4], f32x4 acc) {
 #pragma unroll
     for (int jt = 0; jt < 4; jt += 2) {
-        const s16x4 a0 = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
-        const s16x4 a1 = as_s16x4(bt[(4 * (jt + 1) + grp) * NS + 16 * q + col]);
-        acc = mma_k32(a0, a1, wh[jt], wh[jt + 1], acc);
-        acc = mma_k32(a0, a1, wl[jt], wl[jt + 1], acc);
-        if constexpr (F32) {
-            const s16x4 l0 = as_s16x4(btl[(4 * jt + grp) * NS + 16 * q + col]);
-            const s16x4 l1 = as_s16x4(btl[(4 * (jt + 1) + grp) * NS + 16 * q + col]);
-            acc = mma_k32(l0, l1, wh[jt], wh[jt + 1], acc);
-        }
+        acc = mma_k32(o.h[jt], o.h[jt + 1], wh[jt], wh[jt + 1], acc);
+        acc = mma_k32(o.h[jt], o.h[jt + 1], wl[jt], wl[jt + 1], acc);
+        if constexpr (F32) acc = mma_k32(o.l[jt], o.l[jt + 1], wh[jt], wh[jt + 1], acc);
     }
     return acc;
 }
@@ -314,6 +377,23 @@ __device__ __forceinline__ f32x4 state_tile(const uint2 *bt, const uint2 *btl, i
 // State quads of this lane in the pool layout: s[p][16q + 4grp .. +3] at
 // ((4q + grp) * 64 + p) * 4.
 __device__ __forceinline__ int quad_off(int q, int grp, int p) { return ((4 * q + grp) * kP + p) * 4; }
+
+// Point a stager at workgroup (row, head, segment)'s inputs.
+template <class ST>
+__device__ __forceinline__ void setup(ST &st, const SeqArgs &a, const Unit &un, int g, int tid,
+                                      int lane) {
+    constexpr int ES = ST::ES;
+    st.xg = static_cast<const char *>(a.x) + (un.b * a.xs_b + un.h * a.xs_h) * ES;
+    st.dtg = static_cast<const char *>(a.dt) + (un.b * a.dts_b + un.h) * ES;
+    st.Bg = static_cast<const char *>(a.Bm) + (un.b * a.bcs_b + g * a.bcs_g) * ES;
+    st.Cg = a.Cm ? static_cast<const char *>(a.Cm) + (un.b * a.bcs_b + g * a.bcs_g) * ES : nullptr;
+    st.xrow = a.xs_t * ES;
+    st.dtrow = a.dts_t * ES;
+    st.bcrow = a.bcs_t * ES;
+    st.s0 = static_cast<int64_t>(un.seg) * a.S;
+    st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    st.init(tid, lane);
+}
 
 // ------------------------------------------------------------------ seg_state
 // Local forward state F (and, BOTH, reverse state R) of one segment from zero, and
@@ -336,15 +416,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
     const int g = un.h / a.heads_per_group;
 
     Stager<NS, F32, false, false> st;
-    st.xg = static_cast<const AT *>(a.x) + un.b * a.xs_b + un.h * a.xs_h;
-    st.dtg = static_cast<const AT *>(a.dt) + un.b * a.dts_b + un.h;
-    st.Bg = static_cast<const AT *>(a.Bm) + un.b * a.bcs_b + g * a.bcs_g;
-    st.Cg = nullptr;
-    st.xs_t = a.xs_t;
-    st.dts_t = a.dts_t;
-    st.bcs_t = a.bcs_t;
-    st.s0 = static_cast<int64_t>(un.seg) * a.S;
-    st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    setup(st, a, un, g, tid, lane);
     const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
     const float A2 = a.A[un.h] * kLog2e;
 
@@ -360,7 +432,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
     for (int c = 0; c < nch; ++c) {
         st.stage(tid, nullptr, nullptr, nullptr, nullptr, sBt, sBtl, sXt);
         if (wave == 0)
-            decay_sums<BOTH>(Act<F32>::val(st.dtraw), A2, lane, sDt, sCs, sEc, sWs, sWr);
+            decay_sums<BOTH>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, sWr);
         __syncthreads();
         if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
 
@@ -379,10 +451,15 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
             }
         }
         const float keep = ex2(tot);
+        BtOps<F32> cur, nxt;
+        bt_read<NS, F32>(cur, sBt, sBtl, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
-            F[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, fh, fl, F[q] * keep);
-            if constexpr (BOTH) R[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, rh, rl, R[q]);
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, sBtl, q + 1, grp, col);
+            F[q] = bt_mma<F32>(cur, fh, fl, F[q] * keep);
+            if constexpr (BOTH) R[q] = bt_mma<F32>(cur, rh, rl, R[q]);
+            if (q + 1 < QN) cur = nxt;
+            __builtin_amdgcn_sched_barrier(0);
         }
         off += tot;
         __syncthreads();   // LDS is rewritten by the next chunk
@@ -421,15 +498,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
     const int g = un.h / a.heads_per_group;
 
     Stager<NS, F32, REV, true> st;
-    st.xg = static_cast<const AT *>(a.x) + un.b * a.xs_b + un.h * a.xs_h;
-    st.dtg = static_cast<const AT *>(a.dt) + un.b * a.dts_b + un.h;
-    st.Bg = static_cast<const AT *>(a.Bm) + un.b * a.bcs_b + g * a.bcs_g;
-    st.Cg = static_cast<const AT *>(a.Cm) + un.b * a.bcs_b + g * a.bcs_g;
-    st.xs_t = a.xs_t;
-    st.dts_t = a.dts_t;
-    st.bcs_t = a.bcs_t;
-    st.s0 = static_cast<int64_t>(un.seg) * a.S;
-    st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    setup(st, a, un, g, tid, lane);
     const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
     const float A2 = a.A[un.h] * kLog2e;
     const float skip = a.skip[un.h];
@@ -445,50 +514,46 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
     }
-    float *ybase = a.y + (static_cast<int64_t>(un.b) * a.T * a.nheads + un.h) * kP + p;
-    const int64_t ytok = static_cast<int64_t>(a.nheads) * kP;
+    // y of this (row, head) at token 0, bytes between tokens, and this lane's offset of
+    // local token 4grp within a chunk's memory window (tokens 16mt + r further on)
+    const float *ybase = a.y + (static_cast<int64_t>(un.b) * a.T * a.nheads + un.h) * kP;
+    const int64_t ytokB = static_cast<int64_t>(a.nheads) * kP * 4;
+    const uint32_t oy = static_cast<uint32_t>(Stager<NS, F32, REV, true>::row(4 * grp) * ytokB + p * 4);
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
         st.stage(tid, sB, sBl, sC, sCl, sBt, sBtl, sXt);
         if (wave == 0)
-            decay_sums<false>(Act<F32>::val(st.dtraw), A2, lane, sDt, sCs, sEc, sWs, nullptr);
+            decay_sums<false>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, nullptr);
         __syncthreads();
         if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
 
         // decay-weighted Gram tiles M[t][j] = 2^{cs_t - cs_j} dt_j (C_t . B_j), j <= t,
         // held as the transposed product (lane (grp, col): j = 16jt + 4grp + r, t = 16mt + col)
+        // (wave w: tiles w, w + 4, w + 8; all operands of a tile are read before its MFMAs)
         for (int k = wave; k < kTiles; k += 4) {
             const int mt = k < 1 ? 0 : (k < 3 ? 1 : (k < 6 ? 2 : 3));
             const int jt = k - mt * (mt + 1) / 2;
-            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+            s16x4 bq[QN], cq[QN], blq[F32 ? QN : 1], clq[F32 ? QN : 1];
 #pragma unroll
-            for (int q = 0; q < QN; q += 2) {
-                const int q1 = q + 1 < QN ? q + 1 : q;
-                const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
-                const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
-                const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-                const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
-                if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
-                else gacc = mma_k16(b0, c0, gacc);
+            for (int q = 0; q < QN; ++q) {
+                bq[q] = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
+                cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
                 if constexpr (F32) {
-                    const s16x4 bl0 = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
-                    const s16x4 bl1 = as_s16x4(sBl[img_idx<QN, F32>(jt, q1, grp, col)]);
-                    const s16x4 cl0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                    const s16x4 cl1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q1, grp, col)]);
-                    if (q + 1 < QN) {
-                        gacc = mma_k32(b0, b1, cl0, cl1, gacc);
-                        gacc = mma_k32(bl0, bl1, c0, c1, gacc);
-                    } else {
-                        gacc = mma_k16(b0, cl0, gacc);
-                        gacc = mma_k16(bl0, c0, gacc);
-                    }
+                    blq[q] = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
+                    clq[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
                 }
             }
             const int t = 16 * mt + col;
             const float cst = sCs[t];
             const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
             const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
+            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+            gacc = mma_quads<QN>(bq, cq, gacc);
+            if constexpr (F32) {
+                gacc = mma_quads<QN>(bq, clq, gacc);
+                gacc = mma_quads<QN>(blq, cq, gacc);
+            }
             f32x4 m;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -510,20 +575,24 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int q = 0; q < QN; q += 2) {
             if (q + 1 < QN) {
+                s16x4 c0[4], c1[4], d0[F32 ? 4 : 1], d1[F32 ? 4 : 1];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    c0[mt] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                    c1[mt] = as_s16x4(sC[img_idx<QN, F32>(mt, q + 1, grp, col)]);
+                    if constexpr (F32) {
+                        d0[mt] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                        d1[mt] = as_s16x4(sCl[img_idx<QN, F32>(mt, q + 1, grp, col)]);
+                    }
+                }
                 s16x4 h0, l0, h1, l1;
                 split4(S[q], h0, l0);
                 split4(S[q + 1], h1, l1);
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
-                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-                    const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q + 1, grp, col)]);
-                    Y[mt] = mma_k32(c0, c1, h0, h1, Y[mt]);
-                    Y[mt] = mma_k32(c0, c1, l0, l1, Y[mt]);
-                    if constexpr (F32) {
-                        const s16x4 d0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                        const s16x4 d1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q + 1, grp, col)]);
-                        Y[mt] = mma_k32(d0, d1, h0, h1, Y[mt]);
-                    }
+                    Y[mt] = mma_k32(c0[mt], c1[mt], h0, h1, Y[mt]);
+                    Y[mt] = mma_k32(c0[mt], c1[mt], l0, l1, Y[mt]);
+                    if constexpr (F32) Y[mt] = mma_k32(d0[mt], d1[mt], h0, h1, Y[mt]);
                 }
             } else {
                 s16x4 h0, l0;
@@ -539,6 +608,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     }
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
@@ -582,20 +652,24 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         }
 
         // skip term and store (lane (grp, col): token 16mt + 4grp + r, column p)
+        {
+            const __amdgpu_buffer_rsrc_t rY = rsrc(ybase + st.window(c) * (ytokB / 4));
+            const int lim = st.valid(c);
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const f32x4 out = Y[mt] + skip * xv(mt);
+            for (int mt = 0; mt < 4; ++mt) {
+                const f32x4 out = Y[mt] + skip * xv(mt);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                int64_t t;
-                if (st.token(c, 16 * mt + 4 * grp + r, t)) {
-                    // the reverse pass adds onto the forward pass's outputs in L2
-                    // (one addend per element: the sum is exact fp32 and deterministic)
+                for (int r = 0; r < 4; ++r) {
+                    const int i = 16 * mt + r;   // + 4grp: this lane's local token
+                    const uint32_t o = 16 * mt + 4 * grp + r < lim
+                                           ? oy + static_cast<uint32_t>((REV ? -i : i) * ytokB)
+                                           : kOOB;
+                    // the reverse pass adds onto the forward pass's outputs in L2 (one
+                    // addend per element: the sum is exact fp32 and deterministic)
                     if constexpr (REV)
-                        __hip_atomic_fetch_add(ybase + t * ytok, out[r], __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(out[r], rY, o, 0, 0);
                     else
-                        __builtin_nontemporal_store(out[r], ybase + t * ytok);
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(out[r]), rY, o, 0, kNT);
                 }
             }
         }
@@ -608,10 +682,14 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             const f32x4 w = *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]);
             split4(w * xv(jt), wh[jt], wl[jt]);
         }
+        BtOps<F32> cur, nxt;
+        bt_read<NS, F32>(cur, sBt, sBtl, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
-            S[q] = state_tile<NS, F32>(sBt, sBtl, q, grp, col, wh, wl, S[q] * keep);
-            // keep the operand reads of one tile at a time in registers
+            // the next tile's operands are read while this tile's MFMAs run
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, sBtl, q + 1, grp, col);
+            S[q] = bt_mma<F32>(cur, wh, wl, S[q] * keep);
+            if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();   // LDS is rewritten by the next chunk

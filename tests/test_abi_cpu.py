@@ -316,3 +316,15 @@ def test_workspace_checks(L):
     assert check_prefill(L, d, ptrs(), ws=WS, wsb=needp) == bd.OK
     assert check_prefill(L, d, ptrs(), ws=WS, wsb=needp - 4) == bd.E_WORKSPACE
     assert bd.strerror(bd.E_WORKSPACE) != "unknown status"
+
+
+def test_sequence_stride_limit(L):
+    """Chunks are addressed with 32-bit offsets: per-token strides up to 16 MiB."""
+    d = desc(batch=1, H=4, L=1000)
+    d.x_stride[1] = (1 << 23)                   # bf16: 16 MiB per token
+    d.x_stride[0] = d.x_stride[1] * 1000
+    assert check_window(L, d, ptrs()) == bd.OK
+    d.x_stride[1] = (1 << 23) + 8
+    assert check_window(L, d, ptrs()) == bd.E_SHAPE
+    assert check_prefill(L, d, ptrs()) == bd.E_SHAPE
+    assert check_step(L, desc(), ptrs()) == bd.OK   # the block entry points are not limited

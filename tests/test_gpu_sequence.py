@@ -97,6 +97,31 @@ def test_full_window_caller_workspace_and_determinism():
     assert ei.value.code == bd.E_WORKSPACE
 
 
+@pytest.mark.parametrize("B,H,N,W", [(2, 256, 16, 64), (8, 256, 128, 64), (4, 64, 64, 3000)])
+def test_full_window_many_workgroups(B, H, N, W):
+    """More workgroups than CUs, so CUs run several in turn: the result must not depend
+    on that (bitwise equal across calls, y pre-filled differently) and must match the
+    oracle on sampled heads."""
+    import paper_2607_02805_amd as bd
+    w = wl(B, H, N, W, seed=9280 + H + W)
+    d = bi.block_inputs(w, 0)
+    v = to_dev(d)
+    args = (v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"])
+    y1 = torch.zeros((B, W, H, 64), device=DEV)
+    y2 = torch.full((B, W, H, 64), float("nan"), device=DEV)
+    bd.scan_full_window(*args, y=y1)
+    bd.scan_full_window(*args, y=y2)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    for b, h in ((0, 0), (B - 1, H - 1), (B // 2, H // 3)):
+        sub = {"x": d["x"][b:b + 1, :, h:h + 1], "dt": d["dt"][b:b + 1, :, h:h + 1],
+               "B": d["B"][b:b + 1], "C": d["C"][b:b + 1],
+               "A": d["A"][h:h + 1], "D": d["D"][h:h + 1], "D_rev": d["D_rev"][h:h + 1]}
+        e = rel_err(y1[b:b + 1, :, h:h + 1], oracle.full_window(sub))
+        say("  (b, h) =", (b, h), "rel err", e)
+        assert e <= REL_TOL
+
+
 def test_full_window_groups_and_long():
     w = wl(2, 4, 64, 2000, G=2, seed=9300)
     d = bi.block_inputs(w, 0)
