@@ -459,10 +459,10 @@ def summarize_trace(stats_csv: str) -> str:
 
 
 def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
-                      copy_bytes=256 << 20) -> dict:
-    """Per-launch HBM bytes of the step and commit kernels from FETCH_SIZE / WRITE_SIZE
-    (KiB per dispatch), each scaled by the same counter's reading for a plain copy of
-    known size."""
+                      copy_bytes=256 << 20, kernels=None) -> dict:
+    """Per-launch HBM bytes of kernels (default: the block step and the commit; else a
+    {tag: name substring} map) from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each
+    scaled by the same counter's reading for a plain copy of known size."""
     import statistics as st
 
     def per_kernel(path, counter):
@@ -479,7 +479,8 @@ def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
     f_scale = copy_bytes / 1024 / copy_kib(copy_fetch_csv, "FETCH_SIZE")
     w_scale = copy_bytes / 1024 / copy_kib(copy_write_csv, "WRITE_SIZE")
     res = {"fetch_scale": f_scale, "write_scale": w_scale}
-    for tag, key in (("step", STEP_KERNEL), ("commit", COMMIT_KERNEL)):
+    kernels = kernels or {"step": STEP_KERNEL, "commit": COMMIT_KERNEL}
+    for tag, key in kernels.items():
         fk = [v for k, vs in per_kernel(fetch_csv, "FETCH_SIZE").items() if key in k for v in vs]
         wk = [v for k, vs in per_kernel(write_csv, "WRITE_SIZE").items() if key in k for v in vs]
         res[tag] = {"fetch_kib_median": st.median(fk), "write_kib_median": st.median(wk),
@@ -529,6 +530,8 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=4,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
+    ap.add_argument("--traffic-kernels", metavar="TAG=NAME,...",
+                    help="with --summarize-traffic: kernels to report (name substrings)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
@@ -537,7 +540,10 @@ def main():
         print(summarize_trace(args.summarize_trace))
         return
     if args.summarize_traffic:
-        r = summarize_traffic(*args.summarize_traffic)
+        kern = None
+        if args.traffic_kernels:
+            kern = dict(kv.split("=", 1) for kv in args.traffic_kernels.split(";"))
+        r = summarize_traffic(*args.summarize_traffic, kernels=kern)
         r["kernel_source_sha256_16"] = kernel_source_sha()
         r["step_alg_bytes"] = step_bytes(16, 32, 64, 128, 1, 32)
         r["commit_alg_bytes"] = commit_bytes(16, 32, 64, 128, 1, 32)
