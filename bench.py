@@ -353,6 +353,56 @@ def run_prefill(args) -> dict:
             "achieved_gbs": round(nbytes / t / 1e9, 1)}
 
 
+def run_all_block(args) -> dict:
+    """The all-block training forward of one Mamba layer (Fig. 1): an 8,192-token window
+    at the 350M layer shape, batch 8 (a 64-sequence global batch over 8 GPUs), blocks of
+    32 tokens.  Clean stream: the states entering all 256 blocks and its forward outputs;
+    noised stream: every block stepped from its clean prefix's state (one batched block
+    step over 2,048 block rows).  Inputs drawn on the GPU."""
+    import torch
+
+    import bdlm_inputs as bi
+    import paper_2607_02805_amd as bd
+    dev = "cuda:0"
+    w = bi.Workload("350m-train-window", 8, 32, 64, 128, 1, 32, 8192, True, 1, 5000)
+    T, L, K = w.prefix, w.block_len, w.prefix // w.block_len
+    c = bi.tokens_device(w, T, w.base_seed + 1, dev)
+    n = bi.tokens_device(w, T, w.base_seed + 10, dev)
+    hp = {k: torch.from_numpy(a).to(dev) for k, a in bi.head_params(w).items()}
+    stream = torch.cuda.Stream()
+    reps = 3
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+
+    def once():
+        return bd.all_block_forward((c["x"], c["dt"], c["B"], c["C"]), (n["x"], n["dt"], n["B"], n["C"]),
+                                    hp["A"], hp["D"], hp["D_rev"], L, want_clean_y=True,
+                                    stream=stream)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        out = once()                                 # warm-up (and the allocations)
+        del out
+        ev[0].record(stream)
+        for r in range(reps):
+            out = once()
+            ev[r + 1].record(stream)
+            del out
+    torch.cuda.synchronize()
+    ms = [ev[r].elapsed_time(ev[r + 1]) for r in range(reps)]
+    t = float(np.median(ms)) * 1e-3
+    Bsz, H, P, N = w.batch, w.nheads, w.headdim, w.dstate
+    inputs = Bsz * T * (H * P + H + 2 * N) * 2      # x, dt, B, C of one stream (bf16)
+    y = Bsz * T * H * P * 4
+    states = Bsz * K * H * P * N * 4
+    nbytes = 2 * inputs + 2 * y + 2 * states        # both streams; states written, read
+    del c, n
+    torch.cuda.empty_cache()
+    return {"workload": "350m-mamba-layer-b8-window8192-L32-allblock", "blocks": K,
+            "ms": round(t * 1e3, 3), "ms_all": [round(m, 3) for m in ms],
+            "tokens_per_s": round(2 * Bsz * T / t, 1), "alg_bytes": nbytes,
+            "achieved_gbs": round(nbytes / t / 1e9, 1),
+            "frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def run_copy_reference(nbytes: int, nbuf: int = 32, reps: int = 20) -> dict:
     """A plain device copy moving ``nbytes`` in total (half read, half written) per launch,
     over a ring of ``nbuf`` buffers so that every launch misses the Infinity Cache,
@@ -559,8 +609,8 @@ def main():
     if args.sequence_only:
         import torch
         torch.cuda.set_device(0)
-        print(json.dumps({"contrast": run_contrast(args, None), "prefill": run_prefill(args)}),
-              flush=True)
+        print(json.dumps({"contrast": run_contrast(args, None), "prefill": run_prefill(args),
+                          "all_block": run_all_block(args)}), flush=True)
         return
 
     r = run_gpu(args)
@@ -570,6 +620,7 @@ def main():
         extras["flatness"] = run_flatness(args)
         extras["contrast"] = run_contrast(args, r)
         extras["prefill"] = run_prefill(args)
+        extras["all_block"] = run_all_block(args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, args.cpu_budget)
     s = r["shape"]
     line = {

@@ -221,6 +221,33 @@ int bdlm_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const f
                  void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
+ * All-block states of a clean sequence (the training computation of Fig. 1: every
+ * block of a training window is denoised from the forward boundary state of its
+ * clean prefix, Eq. prefix-cache-loss).  The clean sequence is n_blocks blocks of
+ * desc.block_len (1 .. 64) tokens: x [batch][n_blocks * block_len][nheads][64] etc.
+ * with desc's strides.
+ * s_init       device fp32, batch x nheads states in the pool layout (the states
+ *              before block 0), or NULL for zero states.
+ * s_out        device fp32, batch * n_blocks * nheads states in the pool layout:
+ *              state (row * n_blocks + k) * nheads + head is the forward state after
+ *              blocks 0 .. k-1 of that row (k = 0: s_init).  16-byte aligned.
+ * y_fwd        fp32 [batch][n_blocks * block_len][nheads][64] or NULL: the forward
+ *              outputs (skip D) of the clean sequence.  C is read only for these.
+ * workspace    at least bdlm_boundary_states_workspace bytes (one float per row,
+ *              head and block), 256-byte aligned.
+ * The noised blocks are then one bdlm_scan_block_step with batch batch * n_blocks
+ * over s_out (slot_idx NULL): a contiguous [batch][n_blocks * block_len][...] tensor
+ * is the same memory as [batch * n_blocks][block_len][...].
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE (also batch * nheads * n_blocks > 2^30),
+ * BDLM_E_DTYPE, BDLM_E_ALIGN, BDLM_E_WORKSPACE, BDLM_E_LAUNCH.
+ */
+int bdlm_boundary_states_workspace(const bdlm_desc_t *desc, int64_t n_blocks, int64_t *bytes);
+int bdlm_block_boundary_states(const bdlm_desc_t *desc, int64_t n_blocks, const void *x,
+                               const void *dt, const float *A, const void *B, const void *C,
+                               const float *D, const float *s_init, float *s_out, float *y_fwd,
+                               void *workspace, int64_t workspace_bytes, void *stream);
+
+/*
  * State pool layout.  The state of one (slot, head) is the 64 x dstate matrix
  * s[p][n] of the recurrence.  In a pool, state k = slot * nheads + head starts
  * at float offset k * 64 * dstate and stores s[p][n] at
@@ -269,6 +296,11 @@ int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *d
                            const float *A, const void *B, const void *C, const float *D,
                            const float *D_rev, const float *y, const void *workspace,
                            int64_t workspace_bytes);
+int bdlm_check_block_boundary_states(const bdlm_desc_t *desc, int64_t n_blocks, const void *x,
+                                     const void *dt, const float *A, const void *B,
+                                     const void *C, const float *D, const float *s_init,
+                                     const float *s_out, const float *y_fwd,
+                                     const void *workspace, int64_t workspace_bytes);
 int bdlm_check_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
                        const void *B, const void *C, const float *D, const float *h_pool,
                        int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,

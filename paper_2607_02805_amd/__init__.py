@@ -92,6 +92,11 @@ def lib() -> ctypes.CDLL:
         L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
         L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
         L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
+        L.bdlm_boundary_states_workspace.argtypes = [dp, i64, i64p]
+        L.bdlm_check_block_boundary_states.argtypes = [dp, i64, vp, vp, fp, vp, vp, fp, fp, fp,
+                                                       fp, vp, i64]
+        L.bdlm_block_boundary_states.argtypes = [dp, i64, vp, vp, fp, vp, vp, fp, fp, fp, fp, vp,
+                                                 i64, vp]
         L.bdlm_full_window_workspace.argtypes = [dp, i64p]
         L.bdlm_prefill_workspace.argtypes = [dp, i64p]
         L.bdlm_check_full_window.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, vp, i64]
@@ -104,7 +109,9 @@ def lib() -> ctypes.CDLL:
                      "bdlm_scan_block_step", "bdlm_commit_boundary", "bdlm_cache_reset",
                      "bdlm_state_pack", "bdlm_state_unpack", "bdlm_check_full_window",
                      "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill",
-                     "bdlm_full_window_workspace", "bdlm_prefill_workspace"):
+                     "bdlm_full_window_workspace", "bdlm_prefill_workspace",
+                     "bdlm_boundary_states_workspace", "bdlm_check_block_boundary_states",
+                     "bdlm_block_boundary_states"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -356,6 +363,71 @@ def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_ind
     if rc != OK:
         raise BdlmError(rc, "bdlm_prefill")
     return y_fwd
+
+
+def block_boundary_states(x, dt, A, B, C, D, block_len, s_init=None, s_out=None, y_fwd=None,
+                          stream=None, workspace=None):
+    """States entering every block of a clean sequence x [B, K * block_len, H, 64]:
+    returns ``s_out`` (float32, pool layout, [B * K, H, N/4, 64, 4]; state b * K + k is
+    the forward state after blocks 0 .. k-1 of row b, k = 0 being ``s_init`` or zero)
+    and, if ``y_fwd`` is True or a tensor, the forward outputs of the sequence."""
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    T, H, N = d.block_len, d.nheads, d.dstate
+    if block_len <= 0 or T % block_len != 0:
+        raise ValueError("the sequence length must be a whole number of blocks")
+    K = T // block_len
+    d.block_len = block_len
+    if s_out is None:
+        s_out = torch.empty(pool_shape(d.batch * K, H, N), dtype=torch.float32, device=x.device)
+    elif s_out.dtype != torch.float32 or not s_out.is_contiguous() \
+            or s_out.numel() != d.batch * K * H * HEADDIM * N:
+        raise ValueError(f"s_out must be a contiguous float32 tensor of {d.batch * K * H} states")
+    if s_init is not None and (s_init.dtype != torch.float32 or not s_init.is_contiguous()
+                               or s_init.numel() != d.batch * H * HEADDIM * N):
+        raise ValueError(f"s_init must be a contiguous float32 tensor of {d.batch * H} states")
+    if y_fwd is True:
+        y_fwd = torch.empty((d.batch, T, H, HEADDIM), dtype=torch.float32, device=x.device)
+    L = lib()
+    need = ctypes.c_int64(0)
+    rc = L.bdlm_boundary_states_workspace(ctypes.byref(d), K, ctypes.byref(need))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_boundary_states_workspace")
+    if workspace is None and need.value > 0:
+        workspace = torch.empty(need.value, dtype=torch.uint8, device=x.device)
+    wp = None if workspace is None else workspace.data_ptr()
+    wb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = L.bdlm_block_boundary_states(
+        ctypes.byref(d), K, _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"),
+        None if s_init is None else _dev_ptr(s_init, "s_init"), _dev_ptr(s_out, "s_out"),
+        None if y_fwd is None else _dev_ptr(y_fwd, "y_fwd"), wp, wb, _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_block_boundary_states")
+    return (s_out, y_fwd) if y_fwd is not None else s_out
+
+
+def all_block_forward(clean, noised, A, D, D_rev, block_len, s_init=None, want_clean_y=False,
+                      stream=None):
+    """The all-block training forward of one Mamba layer: ``clean`` and ``noised`` are
+    (x, dt, B, C) of the same window [B, K * block_len, ...]; every noised block k is
+    stepped (forward from the clean prefix's state before block k, reverse inside the
+    block) in one batched block step.  Returns (y_noised [B, K * block_len, H, 64],
+    s_out[, y_clean_forward])."""
+    xc, dtc, Bc, Cc = clean
+    xn, dtn, Bn, Cn = noised
+    bsz, T = xn.shape[0], xn.shape[1]
+    K = T // block_len
+    out = block_boundary_states(xc, dtc, A, Bc, Cc, D, block_len, s_init=s_init,
+                                y_fwd=True if want_clean_y else None, stream=stream)
+    s_out = out[0] if want_clean_y else out
+
+    def blocks(t):   # [B, K * L, ...] -> [B * K, L, ...] (a view when contiguous)
+        return t.reshape(bsz * K, block_len, *t.shape[2:])
+    y = scan_block_step(blocks(xn), blocks(dtn), A, blocks(Bn), blocks(Cn), D, D_rev, s_out,
+                        stream=stream)
+    y = y.reshape(bsz, T, *y.shape[2:])
+    return (y, s_out, out[1]) if want_clean_y else (y, s_out)
 
 
 def cache_reset(h_pool, slots=None, n_committed=None, n_blocks=None, stream=None):

@@ -256,6 +256,54 @@ int bdlm_check_prefill(const bdlm_desc_t *d, const void *x, const void *dt, cons
     return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
 }
 
+int bdlm_boundary_states_workspace(const bdlm_desc_t *d, int64_t n_blocks, int64_t *bytes) {
+    if (!bytes) return BDLM_E_NULL;
+    const int rc = check_desc(d, BDLM_MAX_BLOCK_LEN);
+    if (rc != BDLM_OK) return rc;
+    if (n_blocks < 0) return BDLM_E_SHAPE;
+    *bytes = (d->batch == 0 || d->block_len == 0) ? 0
+                                                  : bdlm::boundary_workspace(d->batch, d->nheads,
+                                                                             n_blocks);
+    return BDLM_OK;
+}
+
+int bdlm_check_block_boundary_states(const bdlm_desc_t *d, int64_t n_blocks, const void *x,
+                                     const void *dt, const float *A, const void *B,
+                                     const void *C, const float *D, const float *s_init,
+                                     const float *s_out, const float *y_fwd,
+                                     const void *workspace, int64_t workspace_bytes) {
+    // the whole clean sequence is n_blocks * block_len tokens; check it as such
+    if (!d) return BDLM_E_NULL;
+    if (n_blocks < 0) return BDLM_E_SHAPE;
+    if (d->block_len > BDLM_MAX_BLOCK_LEN || d->block_len < 0) return BDLM_E_SHAPE;
+    if (d->block_len > 0 && n_blocks > BDLM_MAX_SEQ_LEN / d->block_len) return BDLM_E_SHAPE;
+    bdlm_desc_t seq = *d;
+    seq.block_len = d->block_len * n_blocks;
+    // C is read only for the forward outputs
+    int rc = check_common(&seq, x, dt, A, B, y_fwd ? C : B, D, D, nullptr, 0, nullptr,
+                          BDLM_MAX_SEQ_LEN, false);
+    if (rc != BDLM_OK) return rc;
+    rc = check_seq_strides(&seq);
+    if (rc != BDLM_OK) return rc;
+    if (d->batch * d->nheads * n_blocks > (int64_t(1) << 30)) return BDLM_E_SHAPE;
+    const bool empty = d->batch == 0 || seq.block_len == 0;
+    if (!s_out && !empty) return BDLM_E_NULL;
+    if (!aligned(s_out, 16) || !aligned(s_init, 16) || !aligned(y_fwd, 4)) return BDLM_E_ALIGN;
+    return check_workspace(workspace, workspace_bytes,
+                           empty ? 0 : bdlm::boundary_workspace(d->batch, d->nheads, n_blocks));
+}
+
+int bdlm_block_boundary_states(const bdlm_desc_t *d, int64_t n_blocks, const void *x,
+                               const void *dt, const float *A, const void *B, const void *C,
+                               const float *D, const float *s_init, float *s_out, float *y_fwd,
+                               void *workspace, int64_t workspace_bytes, void *stream) {
+    const int rc = bdlm_check_block_boundary_states(d, n_blocks, x, dt, A, B, C, D, s_init, s_out,
+                                                    y_fwd, workspace, workspace_bytes);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D, nullptr, nullptr, y_fwd);
+    return bdlm::launch_boundary_states(a, n_blocks, s_init, s_out, workspace, stream);
+}
+
 int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                          const void *B, const void *C, const float *D, const float *D_rev,
                          const float *h_pool, int64_t nslots, const int32_t *slot_idx, float *y,

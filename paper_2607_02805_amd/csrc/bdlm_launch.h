@@ -69,6 +69,17 @@ int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream);
 // ws: prefill_workspace bytes.
 int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream);
 
+// States entering every block of a clean sequence of nblocks blocks of a.L tokens:
+// s_out[(row * nblocks + k) * nheads + head] (pool layout) = the forward state after
+// blocks 0 .. k-1, starting from s_init[row * nheads + head] (nullptr: zero).  a.y
+// (optional) receives the forward outputs of the sequence.  ws: boundary_workspace
+// bytes (one log-decay per row, head and block).
+int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_init,
+                           float *s_out, void *ws, void *stream);
+inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t nblocks) {
+    return (batch * nheads * nblocks * 4 + 255) / 256 * 256;
+}
+
 // Permute nstates states between row-major [64][dstate] and the pool layout.
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream);

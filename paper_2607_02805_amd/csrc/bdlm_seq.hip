@@ -60,7 +60,16 @@ struct SeqArgs {
     int32_t nheads, heads_per_group;
     int32_t zero_init;           // seg_out: every segment starts from zero (ws unused)
     int32_t xcd_remap;           // grid % 8 == 0: keep a (row, segment)'s heads on one XCD
+    int32_t blk_major;           // states of (row, head, segment) at slot (row * nseg + segment)
+                                 // * nheads + head (a pool of per-block states); else
+                                 // (row * nheads + head) * nseg + segment
 };
+
+// Slot of workgroup (row, head, segment)'s states in ws (times dirs states each).
+__device__ __forceinline__ int64_t state_slot(const SeqArgs &a, int b, int h, int seg) {
+    return a.blk_major ? (static_cast<int64_t>(b) * a.nseg + seg) * a.nheads + h
+                       : (static_cast<int64_t>(b) * a.nheads + h) * a.nseg + seg;
+}
 
 template <int NS, bool F32>
 struct Geo {
@@ -465,14 +474,13 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         __syncthreads();   // LDS is rewritten by the next chunk
     }
 
-    const int64_t us = (static_cast<int64_t>(un.b) * a.nheads + un.h) * a.nseg + un.seg;
-    float *out = a.ws + us * a.dirs * (kP * NS);
+    float *out = a.ws + state_slot(a, un.b, un.h, un.seg) * a.dirs * (kP * NS);
 #pragma unroll
     for (int q = 0; q < QN; ++q) {
         *reinterpret_cast<f32x4 *>(out + quad_off(q, grp, p)) = F[q];
         if constexpr (BOTH) *reinterpret_cast<f32x4 *>(out + kP * NS + quad_off(q, grp, p)) = R[q];
     }
-    if (tid == 0) a.tot[us] = off;
+    if (tid == 0) a.tot[(static_cast<int64_t>(un.b) * a.nheads + un.h) * a.nseg + un.seg] = off;
 }
 
 // ------------------------------------------------------------------ seg_out
@@ -509,8 +517,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = f32x4{0.f, 0.f, 0.f, 0.f};
     } else {
-        const int64_t us = (static_cast<int64_t>(un.b) * a.nheads + un.h) * a.nseg + un.seg;
-        const float *src = a.ws + (us * a.dirs + (REV ? 1 : 0)) * (kP * NS);
+        const float *src =
+            a.ws + (state_slot(a, un.b, un.h, un.seg) * a.dirs + (REV ? 1 : 0)) * (kP * NS);
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
     }
@@ -700,9 +708,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 struct CombineArgs {
     float *ws;
     const float *tot;
-    float *pool;                 // prefill: initial states read, final states written
+    float *pool;                 // states entering segment 0 (slot per row), or nullptr: zero
     int64_t units, state_floats; // (row, head) pairs; 64 * N
     int32_t nseg, dirs, nheads;
+    int32_t write_final;         // prefill: the final states go back to pool
+    int32_t blk_major;           // ws slots as in SeqArgs::blk_major
     int32_t use_slots;
     int32_t slots[BDLM_MAX_SLOT_ROWS];
 };
@@ -714,29 +724,31 @@ __global__ void __launch_bounds__(256) bdlm_seg_combine_kernel(const CombineArgs
     const int64_t qps = c.state_floats / 4;
     if (i >= c.units * qps) return;
     const int64_t unit = i / qps, e = (i % qps) * 4;
+    const int64_t b = unit / c.nheads, h = unit % c.nheads;
     const float *tot = c.tot + unit * c.nseg;
-    float *base = c.ws + unit * c.nseg * c.dirs * c.state_floats + e;
-    const int64_t seg_stride = c.dirs * c.state_floats;
+    auto seg = [&](int k) {
+        const int64_t slot = c.blk_major ? (b * c.nseg + k) * c.nheads + h : unit * c.nseg + k;
+        return reinterpret_cast<f32x4 *>(c.ws + slot * c.dirs * c.state_floats + e);
+    };
 
     float *pst = nullptr;
     f32x4 s = {0.f, 0.f, 0.f, 0.f};
     if (c.pool) {
-        const int64_t b = unit / c.nheads, h = unit % c.nheads;
         const int64_t slot = c.use_slots ? c.slots[b] : b;
         pst = c.pool + (slot * c.nheads + h) * c.state_floats + e;
         s = *reinterpret_cast<const f32x4 *>(pst);
     }
     for (int k = 0; k < c.nseg; ++k) {
-        f32x4 *f = reinterpret_cast<f32x4 *>(base + k * seg_stride);
+        f32x4 *f = seg(k);
         const f32x4 fk = *f;
         *f = s;
         s = s * ex2(tot[k]) + fk;
     }
-    if (pst) *reinterpret_cast<f32x4 *>(pst) = s;
+    if (c.write_final) *reinterpret_cast<f32x4 *>(pst) = s;
     if (c.dirs == 2) {
         f32x4 r = {0.f, 0.f, 0.f, 0.f};
         for (int k = c.nseg - 1; k >= 0; --k) {
-            f32x4 *f = reinterpret_cast<f32x4 *>(base + k * seg_stride + c.state_floats);
+            f32x4 *f = seg(k) + c.state_floats / 4;
             const f32x4 rk = *f;
             *f = r;
             r = r * ex2(tot[k]) + rk;
@@ -809,17 +821,20 @@ SeqArgs seq_args(const LaunchArgs &a, int64_t T, const SeqPlan &pl, void *ws) {
     k.nheads = a.nheads;
     k.heads_per_group = a.nheads / a.ngroups;
     k.zero_init = 1;
+    k.blk_major = 0;
     const int64_t grid = static_cast<int64_t>(a.batch) * a.nheads * pl.nseg;
     k.xcd_remap = grid % 8 == 0 ? 1 : 0;
     return k;
 }
 
 hipError_t combine(const LaunchArgs &a, const SeqPlan &pl, const SeqArgs &k, float *pool,
-                   hipStream_t s) {
+                   bool write_final, hipStream_t s) {
     CombineArgs c;
     c.ws = k.ws;
     c.tot = k.tot;
     c.pool = pool;
+    c.write_final = write_final && pool ? 1 : 0;
+    c.blk_major = k.blk_major;
     c.units = static_cast<int64_t>(a.batch) * a.nheads;
     c.state_floats = static_cast<int64_t>(kP) * a.dstate;
     c.nseg = static_cast<int32_t>(pl.nseg);
@@ -848,7 +863,7 @@ int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
         if ((f32 ? run_state<true>(a.dstate, k, true, grid, s)
                  : run_state<false>(a.dstate, k, true, grid, s)) != hipSuccess)
             return BDLM_E_LAUNCH;
-        if (combine(a, pl, k, nullptr, s) != hipSuccess) return BDLM_E_LAUNCH;
+        if (combine(a, pl, k, nullptr, false, s) != hipSuccess) return BDLM_E_LAUNCH;
         k.zero_init = 0;
     }
     k.skip = a.D;
@@ -873,7 +888,37 @@ int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
              : run_state<false>(a.dstate, k, false, grid, s)) != hipSuccess)
         return BDLM_E_LAUNCH;
     // the cached states enter segment 0; the final states go back to the cache
-    if (combine(a, pl, k, a.h_pool, s) != hipSuccess) return BDLM_E_LAUNCH;
+    if (combine(a, pl, k, a.h_pool, true, s) != hipSuccess) return BDLM_E_LAUNCH;
+    if (a.y) {
+        k.zero_init = 0;
+        k.skip = a.D;
+        if ((f32 ? run_out<true>(a.dstate, k, false, grid, s)
+                 : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+            return BDLM_E_LAUNCH;
+    }
+    return BDLM_OK;
+}
+
+int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_init,
+                           float *s_out, void *ws, void *stream) {
+    if (a.batch == 0 || nblocks == 0) return BDLM_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // one segment per block; the block states live in s_out, the segment decays in ws
+    SeqPlan pl;
+    pl.seg_len = a.L;
+    pl.nseg = nblocks;
+    pl.dirs = 1;
+    pl.state_bytes = 0;
+    pl.total_bytes = 0;
+    SeqArgs k = seq_args(a, nblocks * a.L, pl, s_out);
+    k.tot = static_cast<float *>(ws);
+    k.blk_major = 1;
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * nblocks);
+    const bool f32 = !a.bf16;
+    if ((f32 ? run_state<true>(a.dstate, k, false, grid, s)
+             : run_state<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+        return BDLM_E_LAUNCH;
+    if (combine(a, pl, k, const_cast<float *>(s_init), false, s) != hipSuccess) return BDLM_E_LAUNCH;
     if (a.y) {
         k.zero_init = 0;
         k.skip = a.D;

@@ -328,3 +328,39 @@ def test_sequence_stride_limit(L):
     assert check_window(L, d, ptrs()) == bd.E_SHAPE
     assert check_prefill(L, d, ptrs()) == bd.E_SHAPE
     assert check_step(L, desc(), ptrs()) == bd.OK   # the block entry points are not limited
+
+
+def check_bstates(L, d, K=4, p=None, s_init=FAKE + 0xA000, s_out=FAKE + 0xB000, yf=None,
+                  ws=WS, wsb=BIG):
+    p = ptrs() if p is None else p
+    return L.bdlm_check_block_boundary_states(ctypes.byref(d), K, p["x"], p["dt"], p["A"], p["B"],
+                                              p["C"], p["D"], s_init, s_out, yf, ws, wsb)
+
+
+def test_boundary_states_checks(L):
+    d = desc(batch=2, H=4, N=32, L=32)
+    assert check_bstates(L, d) == bd.OK
+    assert check_bstates(L, d, s_init=None) == bd.OK                  # zero initial states
+    assert check_bstates(L, d, p=ptrs(C=None)) == bd.OK               # C only for y_fwd
+    assert check_bstates(L, d, p=ptrs(C=None), yf=FAKE + 0xC000) == bd.E_NULL
+    assert check_bstates(L, d, K=-1) == bd.E_SHAPE
+    assert check_bstates(L, d, s_out=None) == bd.E_NULL
+    assert check_bstates(L, d, s_out=FAKE + 0xB008) == bd.E_ALIGN
+    assert check_bstates(L, d, s_init=FAKE + 0xA004) == bd.E_ALIGN
+    assert check_bstates(L, desc(L=65)) == bd.E_SHAPE                 # blocks of at most 64
+    assert check_bstates(L, d, K=(2 ** 31) // 32 + 1) == bd.E_SHAPE   # sequence too long
+    assert check_bstates(L, desc(batch=1 << 10, H=1 << 10), K=2 ** 11) == bd.E_SHAPE   # grid
+    need = ws_bytes_b(L, d, 4)
+    assert need == (2 * 4 * 4 * 4 + 255) // 256 * 256
+    assert check_bstates(L, d, ws=WS, wsb=need) == bd.OK
+    assert check_bstates(L, d, ws=WS, wsb=need - 4) == bd.E_WORKSPACE
+    assert check_bstates(L, d, ws=None, wsb=need) == bd.E_WORKSPACE
+    assert check_bstates(L, d, K=0, ws=None, wsb=0) == bd.OK          # empty: nothing to do
+    assert L.bdlm_block_boundary_states(None, 4, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                        FAKE, None, WS, BIG, None) == bd.E_NULL
+
+
+def ws_bytes_b(L, d, K):
+    n = ctypes.c_int64(-1)
+    assert L.bdlm_boundary_states_workspace(ctypes.byref(d), K, ctypes.byref(n)) == bd.OK
+    return n.value
