@@ -403,6 +403,82 @@ def run_all_block(args) -> dict:
             "frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4)}
 
 
+def _graph_time(fn, nlayers, reps=10):
+    """Per-call time of fn(layer) over a ring of layers captured in one HIP graph."""
+    import torch
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for li in range(nlayers):
+            fn(li)
+    stream.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        for li in range(nlayers):
+            fn(li)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        g.replay()
+        e0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / (reps * nlayers)
+
+
+def run_variants(args) -> dict:
+    """Block-step variants, each over a ring of 24 layers' states (cold reads):
+    the paper's 350M geometry (d_inner 1664: 26 heads of 64, dstate 128) with its block
+    length 256 at batch 16 (step and commit, on the sequence kernels), and the step with
+    separate reverse-direction inputs at the 350M layer shape (32 heads, L 32)."""
+    import torch
+
+    import bdlm_inputs as bi
+    import paper_2607_02805_amd as bd
+    dev = "cuda:0"
+    nl = 24
+    out = {}
+    # paper geometry, L = 256
+    w = bi.Workload("350m-paper-geometry", 16, 26, 64, 128, 1, 256, 0, True, 1, 6000)
+    d = to_dev(bi.block_inputs(w, 0), dev)
+    c = to_dev(bi.commit_inputs(w), dev)
+    pools = [torch.zeros(bd.pool_shape(16, 26, 128), device=dev) for _ in range(nl)]
+    y = torch.empty((16, 256, 26, 64), device=dev)
+    yc = torch.empty_like(y)
+    nc, nb = np.zeros(16, np.int64), np.zeros(16, np.int64)
+    t_step = _graph_time(lambda li: bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"],
+                                                       d["D"], d["D_rev"], pools[li], y=y), nl)
+    t_commit = _graph_time(lambda li: bd.commit_boundary(c["x"], c["dt"], c["A"], c["B"], c["C"],
+                                                         c["D"], c["D_rev"], pools[li], nc.copy(),
+                                                         nb.copy(), -1, y_clean=yc), nl)
+    sb = step_bytes(16, 26, 64, 128, 1, 256)
+    out["paper_geometry_L256"] = {
+        "workload": "350m-paper-geometry-b16-h26-L256", "step_us": round(t_step * 1e6, 2),
+        "commit_us": round(t_commit * 1e6, 2), "step_bytes": sb,
+        "step_gbs": round(sb / t_step / 1e9, 1),
+        "active_tokens_per_s": round(16 * 256 / t_step, 1)}
+    del pools, y, yc
+    # separate reverse-direction inputs, L = 32
+    w = bi.WORKLOADS[3]
+    f = to_dev(bi.block_inputs(w, 0), dev)
+    r = to_dev(bi.block_inputs(w, 1), dev)
+    pools = [torch.zeros(bd.pool_shape(16, 32, 128), device=dev) for _ in range(nl)]
+    y = torch.empty((16, 32, 32, 64), device=dev)
+    t_sep = _graph_time(lambda li: bd.scan_block_step_sep(
+        (f["x"], f["dt"], f["A"], f["B"], f["C"], f["D"]),
+        (r["x"], r["dt"], r["A"], r["B"], r["C"], r["D_rev"]), pools[li], y=y), nl)
+    sb = step_bytes(16, 32, 64, 128, 1, 32) + (step_bytes(16, 32, 64, 128, 1, 32)
+                                               - 16 * 32 * 64 * 128 * 4 - 16 * 32 * 32 * 64 * 4)
+    out["separate_reverse_L32"] = {
+        "workload": "350m-mamba-layer-b16-L32-separate-reverse-inputs",
+        "step_us": round(t_sep * 1e6, 2), "step_bytes": sb,
+        "step_gbs": round(sb / t_sep / 1e9, 1)}
+    del pools, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_copy_reference(nbytes: int, nbuf: int = 32, reps: int = 20) -> dict:
     """A plain device copy moving ``nbytes`` in total (half read, half written) per launch,
     over a ring of ``nbuf`` buffers so that every launch misses the Infinity Cache,
@@ -610,7 +686,8 @@ def main():
         import torch
         torch.cuda.set_device(0)
         print(json.dumps({"contrast": run_contrast(args, None), "prefill": run_prefill(args),
-                          "all_block": run_all_block(args)}), flush=True)
+                          "all_block": run_all_block(args), "variants": run_variants(args)}),
+              flush=True)
         return
 
     r = run_gpu(args)
@@ -621,6 +698,7 @@ def main():
         extras["contrast"] = run_contrast(args, r)
         extras["prefill"] = run_prefill(args)
         extras["all_block"] = run_all_block(args)
+        extras["variants"] = run_variants(args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, args.cpu_budget)
     s = r["shape"]
     line = {

@@ -31,9 +31,12 @@
  *     error nothing is enqueued and nothing is modified.  The return value is
  *     BDLM_OK or a negative BDLM_E_* code.  No entry point aborts.
  *   - Sizes: headdim P == 64; dstate N in {16, 32, 64, 128}; block_len L in
- *     [0, 64] (the sequence entry points: up to BDLM_MAX_SEQ_LEN); nheads % ngroups
- *     == 0; batch >= 0; batch * nheads <= 2^22 (one or two workgroups per
- *     (row, head), within the 32-bit grid of a launch).
+ *     [0, BDLM_MAX_SEQ_LEN]; nheads % ngroups == 0; batch >= 0; batch * nheads
+ *     <= 2^22 (within the 32-bit grid of a launch).  A block step or commit with
+ *     L <= BDLM_MAX_BLOCK_LEN is one fused launch; longer blocks (e.g. the paper's
+ *     256) run on the sequence kernels as a forward launch from the cached state and
+ *     a reverse launch adding into y, and then need per-token strides (and
+ *     nheads * 64 * 4) of at most 16 MiB.
  *   - Activation storage (x, dt, B, C) is fp32 or bf16 (desc.in_dtype).  All
  *     arithmetic, states and outputs are fp32.
  */
@@ -174,6 +177,22 @@ int bdlm_full_window_workspace(const bdlm_desc_t *desc, int64_t *bytes);
 int bdlm_prefill_workspace(const bdlm_desc_t *desc, int64_t *bytes);
 
 /*
+ * One denoising step with separate reverse-direction inputs (Eq. partial-reverse with
+ * F_theta,<- carrying its own projections): the forward branch runs on (x, dt, A, B,
+ * C) from the cached state with skip D, the reverse branch on (x_rev, dt_rev, A_rev,
+ * B_rev, C_rev) from zero with skip D_rev, and y is their sum.  Both input sets share
+ * desc's shapes and strides; everything else as bdlm_scan_block_step (any block
+ * length; two launches: forward, then reverse adding into y).
+ * Errors: as bdlm_scan_block_step.
+ */
+int bdlm_scan_block_step_sep(const bdlm_desc_t *desc, const void *x, const void *dt,
+                             const float *A, const void *B, const void *C, const float *D,
+                             const void *x_rev, const void *dt_rev, const float *A_rev,
+                             const void *B_rev, const void *C_rev, const float *D_rev,
+                             const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                             float *y, void *stream);
+
+/*
  * Full-window bidirectional scan, with no cache: the full-sequence
  * (DiffuMamba-style) scan that the paper's block-restricted scan replaces
  * (Sec. 4; Sec. 5.1).
@@ -292,6 +311,12 @@ int bdlm_check_commit(const bdlm_desc_t *desc, const void *x, const void *dt, co
                       const float *h_pool, int64_t nslots, const int32_t *slot_idx,
                       const int64_t *n_committed, const int64_t *n_blocks,
                       int64_t expected_block_index);
+int bdlm_check_block_step_sep(const bdlm_desc_t *desc, const void *x, const void *dt,
+                              const float *A, const void *B, const void *C, const float *D,
+                              const void *x_rev, const void *dt_rev, const float *A_rev,
+                              const void *B_rev, const void *C_rev, const float *D_rev,
+                              const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                              const float *y);
 int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
                            const float *A, const void *B, const void *C, const float *D,
                            const float *D_rev, const float *y, const void *workspace,

@@ -92,6 +92,10 @@ def lib() -> ctypes.CDLL:
         L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
         L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
         L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
+        L.bdlm_check_block_step_sep.argtypes = [dp, vp, vp, fp, vp, vp, fp, vp, vp, fp, vp, vp,
+                                                fp, fp, i64, i32p, fp]
+        L.bdlm_scan_block_step_sep.argtypes = [dp, vp, vp, fp, vp, vp, fp, vp, vp, fp, vp, vp, fp,
+                                               fp, i64, i32p, fp, vp]
         L.bdlm_boundary_states_workspace.argtypes = [dp, i64, i64p]
         L.bdlm_check_block_boundary_states.argtypes = [dp, i64, vp, vp, fp, vp, vp, fp, fp, fp,
                                                        fp, vp, i64]
@@ -111,7 +115,8 @@ def lib() -> ctypes.CDLL:
                      "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill",
                      "bdlm_full_window_workspace", "bdlm_prefill_workspace",
                      "bdlm_boundary_states_workspace", "bdlm_check_block_boundary_states",
-                     "bdlm_block_boundary_states"):
+                     "bdlm_block_boundary_states", "bdlm_check_block_step_sep",
+                     "bdlm_scan_block_step_sep"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -232,6 +237,35 @@ def scan_block_step(x, dt, A, B, C, D, D_rev, h_pool, y=None, slot_idx=None, str
     del keep
     if rc != OK:
         raise BdlmError(rc, "bdlm_scan_block_step")
+    return y
+
+
+def scan_block_step_sep(fwd, rev, h_pool, y=None, slot_idx=None, stream=None):
+    """A denoising step whose reverse branch has its own inputs: ``fwd`` and ``rev`` are
+    (x, dt, A, B, C, skip) tuples of the same shapes and strides; the forward branch
+    continues the cached state with skip ``fwd[5]`` (D), the reverse branch runs inside
+    the block from zero with skip ``rev[5]`` (D_rev).  Returns y (float32 [B, L, H, 64])."""
+    torch = _torch()
+    x, dt, A, B, C, D = fwd
+    xr, dtr, Ar, Br, Cr, Dr = rev
+    d = _desc(x, dt, B, C)
+    dr = _desc(xr, dtr, Br, Cr)
+    if (list(d.x_stride), list(d.dt_stride), list(d.bc_stride), d.in_dtype) != \
+            (list(dr.x_stride), list(dr.dt_stride), list(dr.bc_stride), dr.in_dtype):
+        raise ValueError("forward and reverse inputs must share shapes, strides and dtype")
+    H, N = d.nheads, d.dstate
+    if y is None:
+        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
+    keep, sp = _slots(slot_idx)
+    rc = lib().bdlm_scan_block_step_sep(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _dev_ptr(xr, "x_rev"),
+        _dev_ptr(dtr, "dt_rev"), _f32_vec(Ar, H, "A_rev"), _dev_ptr(Br, "B_rev"),
+        _dev_ptr(Cr, "C_rev"), _f32_vec(Dr, H, "D_rev"), _pool(h_pool, H, N), h_pool.shape[0],
+        sp, _dev_ptr(y, "y"), _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_scan_block_step_sep")
     return y
 
 

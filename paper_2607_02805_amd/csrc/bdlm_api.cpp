@@ -76,6 +76,18 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     return BDLM_OK;
 }
 
+// The sequence kernels address a 64-token chunk with 32-bit byte offsets from a
+// per-chunk base: every per-token stride (and y's, nheads x 64 floats) stays below
+// 16 MiB.
+int check_seq_strides(const bdlm_desc_t *d) {
+    constexpr int64_t kMaxRow = int64_t(1) << 24;
+    const int64_t es = elem_size(d->in_dtype);
+    if (d->x_stride[1] * es > kMaxRow || d->bc_stride[1] * es > kMaxRow ||
+        d->dt_stride[1] * es > kMaxRow || d->nheads * BDLM_HEADDIM * 4 > kMaxRow)
+        return BDLM_E_SHAPE;
+    return BDLM_OK;
+}
+
 bdlm::LaunchArgs make_args(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                            const void *B, const void *C, const float *D, const float *D_rev,
                            float *h_pool, const int32_t *slot_idx, float *y) {
@@ -150,11 +162,20 @@ int bdlm_desc_init(bdlm_desc_t *d, int64_t batch, int64_t nheads, int64_t headdi
     return BDLM_OK;
 }
 
+// Blocks longer than BDLM_MAX_BLOCK_LEN run on the sequence kernels: their strides
+// are limited as for the sequence entry points.
+static int check_long_block(const bdlm_desc_t *d) {
+    return d->block_len > BDLM_MAX_BLOCK_LEN ? check_seq_strides(d) : BDLM_OK;
+}
+
 int bdlm_check_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                           const void *B, const void *C, const float *D, const float *D_rev,
                           const float *h_pool, int64_t nslots, const int32_t *slot_idx,
                           const float *y) {
-    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx,
+                          BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    rc = check_long_block(d);
     if (rc != BDLM_OK) return rc;
     if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
     if (!aligned(y, 16)) return BDLM_E_ALIGN;
@@ -179,21 +200,12 @@ int bdlm_check_commit(const bdlm_desc_t *d, const void *x, const void *dt, const
                       const float *h_pool, int64_t nslots, const int32_t *slot_idx,
                       const int64_t *n_committed, const int64_t *n_blocks,
                       int64_t expected_block_index) {
-    const int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx,
+                          BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    rc = check_long_block(d);
     if (rc != BDLM_OK) return rc;
     return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
-}
-
-// The sequence kernels address a 64-token chunk with 32-bit byte offsets from a
-// per-chunk base: every per-token stride (and y's, nheads x 64 floats) stays below
-// 16 MiB.
-static int check_seq_strides(const bdlm_desc_t *d) {
-    constexpr int64_t kMaxRow = int64_t(1) << 24;
-    const int64_t es = elem_size(d->in_dtype);
-    if (d->x_stride[1] * es > kMaxRow || d->bc_stride[1] * es > kMaxRow ||
-        d->dt_stride[1] * es > kMaxRow || d->nheads * BDLM_HEADDIM * 4 > kMaxRow)
-        return BDLM_E_SHAPE;
-    return BDLM_OK;
 }
 
 static int check_workspace(const void *ws, int64_t ws_bytes, int64_t need) {
@@ -315,7 +327,41 @@ int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, co
     // argument block as a commit, with the state update compiled out.
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
+    if (d->block_len > BDLM_MAX_BLOCK_LEN) return bdlm::launch_block_long(a, a, false, true, stream);
     return bdlm::launch_block(a, false, stream);
+}
+
+int bdlm_check_block_step_sep(const bdlm_desc_t *d, const void *x, const void *dt,
+                              const float *A, const void *B, const void *C, const float *D,
+                              const void *x_rev, const void *dt_rev, const float *A_rev,
+                              const void *B_rev, const void *C_rev, const float *D_rev,
+                              const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                              const float *y) {
+    int rc = check_common(d, x, dt, A, B, C, D, D, h_pool, nslots, slot_idx, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    rc = check_common(d, x_rev, dt_rev, A_rev, B_rev, C_rev, D_rev, D_rev, nullptr, 0, nullptr,
+                      BDLM_MAX_SEQ_LEN, false);
+    if (rc != BDLM_OK) return rc;
+    rc = check_seq_strides(d);
+    if (rc != BDLM_OK) return rc;
+    if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
+    if (!aligned(y, 4)) return BDLM_E_ALIGN;
+    return BDLM_OK;
+}
+
+int bdlm_scan_block_step_sep(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                             const void *B, const void *C, const float *D, const void *x_rev,
+                             const void *dt_rev, const float *A_rev, const void *B_rev,
+                             const void *C_rev, const float *D_rev, const float *h_pool,
+                             int64_t nslots, const int32_t *slot_idx, float *y, void *stream) {
+    const int rc = bdlm_check_block_step_sep(d, x, dt, A, B, C, D, x_rev, dt_rev, A_rev, B_rev,
+                                             C_rev, D_rev, h_pool, nslots, slot_idx, y);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs f =
+        make_args(d, x, dt, A, B, C, D, D, const_cast<float *>(h_pool), slot_idx, y);
+    const bdlm::LaunchArgs r =
+        make_args(d, x_rev, dt_rev, A_rev, B_rev, C_rev, D_rev, D_rev, nullptr, slot_idx, y);
+    return bdlm::launch_block_long(f, r, false, true, stream);
 }
 
 int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
@@ -329,7 +375,9 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
     if (y_clean && !aligned(y_clean, 16)) return BDLM_E_ALIGN;
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
-    rc = bdlm::launch_block(a, true, stream);
+    rc = d->block_len > BDLM_MAX_BLOCK_LEN
+             ? bdlm::launch_block_long(a, a, true, y_clean != nullptr, stream)
+             : bdlm::launch_block(a, true, stream);
     if (rc != BDLM_OK) return rc;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;

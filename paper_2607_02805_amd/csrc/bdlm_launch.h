@@ -80,6 +80,13 @@ inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t nblocks
     return (batch * nheads * nblocks * 4 + 255) / 256 * 256;
 }
 
+// A block of any length (a.L) as one segment per row: the forward branch from the
+// cached state (fwd's inputs, skip fwd.D) and, if want_y, the reverse branch from zero
+// (rev's inputs, skip rev.D_rev) added into fwd.y.  commit: the final forward state is
+// written back to fwd.h_pool in place.  fwd and rev share shapes and slots.
+int launch_block_long(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
+                      void *stream);
+
 // Permute nstates states between row-major [64][dstate] and the pool layout.
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream);

@@ -63,6 +63,11 @@ struct SeqArgs {
     int32_t blk_major;           // states of (row, head, segment) at slot (row * nseg + segment)
                                  // * nheads + head (a pool of per-block states); else
                                  // (row * nheads + head) * nseg + segment
+    // seg_out with one segment per row (a block step or commit of any length):
+    const float *pool_in;        // the entering state from the cache (slot per row)
+    float *pool_out;             // the final state written back to the cache (in place)
+    int32_t use_slots;
+    int32_t slots[BDLM_MAX_SLOT_ROWS];
 };
 
 // Slot of workgroup (row, head, segment)'s states in ws (times dirs states each).
@@ -513,7 +518,12 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 
     // the state entering the segment (in this direction's scan order)
     f32x4 S[QN];
-    if (a.zero_init) {
+    const int64_t cslot = a.use_slots ? a.slots[un.b] : un.b;
+    if (a.pool_in) {
+        const float *src = a.pool_in + (cslot * a.nheads + un.h) * (kP * NS);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
+    } else if (a.zero_init) {
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = f32x4{0.f, 0.f, 0.f, 0.f};
     } else {
@@ -538,8 +548,10 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 
         // decay-weighted Gram tiles M[t][j] = 2^{cs_t - cs_j} dt_j (C_t . B_j), j <= t,
         // held as the transposed product (lane (grp, col): j = 16jt + 4grp + r, t = 16mt + col)
-        // (wave w: tiles w, w + 4, w + 8; all operands of a tile are read before its MFMAs)
-        for (int k = wave; k < kTiles; k += 4) {
+        // (wave w: tiles w, w + 4, w + 8; all operands of a tile are read before its MFMAs;
+        // no outputs wanted, e.g. a commit without y: nothing to do)
+        const int ntiles = a.y ? kTiles : 0;
+        for (int k = wave; k < ntiles; k += 4) {
             const int mt = k < 1 ? 0 : (k < 3 ? 1 : (k < 6 ? 2 : 3));
             const int jt = k - mt * (mt + 1) / 2;
             s16x4 bq[QN], cq[QN], blq[F32 ? QN : 1], clq[F32 ? QN : 1];
@@ -580,6 +592,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         f32x4 Y[4];
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) Y[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (a.y) {
 #pragma unroll
         for (int q = 0; q < QN; q += 2) {
             if (q + 1 < QN) {
@@ -621,6 +634,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
             Y[mt] *= *reinterpret_cast<const f32x4 *>(&sEc[16 * mt + 4 * grp]);
+        }
         __syncthreads();   // Gram tiles published
 
         // x operands of this wave's columns (tokens 16jt + 4grp .. +3)
@@ -638,6 +652,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                               bf16_to_f32(xh[jt][2]), bf16_to_f32(xh[jt][3])};
         };
 
+        if (a.y) {
         // intra-chunk term: y += M x over j <= t
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
@@ -681,8 +696,10 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 }
             }
         }
+        }
 
-        // carry the state across the chunk
+        // carry the state across the chunk (not after the last one unless it is kept)
+        if (c + 1 == nch && !a.pool_out) break;
         const float keep = ex2(sCs[kC - 1]);
         s16x4 wh[4], wl[4];
 #pragma unroll
@@ -701,6 +718,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();   // LDS is rewritten by the next chunk
+    }
+    if (a.pool_out) {
+        float *dst = a.pool_out + (cslot * a.nheads + un.h) * (kP * NS);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) *reinterpret_cast<f32x4 *>(dst + quad_off(q, grp, p)) = S[q];
     }
 }
 
@@ -822,6 +844,11 @@ SeqArgs seq_args(const LaunchArgs &a, int64_t T, const SeqPlan &pl, void *ws) {
     k.heads_per_group = a.nheads / a.ngroups;
     k.zero_init = 1;
     k.blk_major = 0;
+    k.pool_in = nullptr;
+    k.pool_out = nullptr;
+    k.use_slots = a.slots ? 1 : 0;
+    for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
+        k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
     const int64_t grid = static_cast<int64_t>(a.batch) * a.nheads * pl.nseg;
     k.xcd_remap = grid % 8 == 0 ? 1 : 0;
     return k;
@@ -926,6 +953,45 @@ int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_
                  : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
             return BDLM_E_LAUNCH;
     }
+    return BDLM_OK;
+}
+
+// One segment per row: a block of any length from the cached state.
+static SeqArgs block_args(const LaunchArgs &a) {
+    SeqPlan pl;
+    pl.seg_len = a.L;
+    pl.nseg = 1;
+    pl.dirs = 1;
+    pl.state_bytes = 0;
+    pl.total_bytes = 0;
+    return seq_args(a, a.L, pl, nullptr);
+}
+
+int launch_block_long(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
+                      void *stream) {
+    if (fwd.batch == 0 || fwd.L == 0) return BDLM_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(fwd.batch) * fwd.nheads);
+    const bool f32 = !fwd.bf16;
+    // forward from the cached state (a commit writes the final state back in place)
+    SeqArgs k = block_args(fwd);
+    k.pool_in = fwd.h_pool;
+    k.pool_out = commit ? fwd.h_pool : nullptr;
+    k.y = want_y ? fwd.y : nullptr;
+    k.skip = fwd.D;
+    if (k.y || k.pool_out) {
+        if ((f32 ? run_out<true>(fwd.dstate, k, false, grid, s)
+                 : run_out<false>(fwd.dstate, k, false, grid, s)) != hipSuccess)
+            return BDLM_E_LAUNCH;
+    }
+    if (!want_y) return BDLM_OK;
+    // reverse inside the block from zero, added onto y
+    SeqArgs r = block_args(rev);
+    r.y = fwd.y;
+    r.skip = rev.D_rev;
+    if ((f32 ? run_out<true>(rev.dstate, r, true, grid, s)
+             : run_out<false>(rev.dstate, r, true, grid, s)) != hipSuccess)
+        return BDLM_E_LAUNCH;
     return BDLM_OK;
 }
 

@@ -99,7 +99,7 @@ def test_null_desc_and_meta(L):
 
 @pytest.mark.parametrize("mut,code", [
     (dict(headdim=32), bd.E_SHAPE), (dict(dstate=48), bd.E_SHAPE), (dict(dstate=256), bd.E_SHAPE),
-    (dict(block_len=65), bd.E_SHAPE), (dict(block_len=-1), bd.E_SHAPE),
+    (dict(block_len=2 ** 31), bd.E_SHAPE), (dict(block_len=-1), bd.E_SHAPE),
     (dict(nheads=6, ngroups=4), bd.E_SHAPE), (dict(ngroups=0), bd.E_SHAPE),
     (dict(nheads=0), bd.E_SHAPE), (dict(batch=-1), bd.E_SHAPE),
     (dict(in_dtype=7), bd.E_DTYPE), (dict(reserved=1), bd.E_DTYPE),
@@ -221,7 +221,18 @@ def test_sequence_entry_points_accept_long_sequences(L):
         assert check_prefill(L, desc(L=T), ptrs(), blocks=T // 32) == bd.OK
     assert check_window(L, desc(L=2 ** 31), ptrs()) == bd.E_SHAPE
     assert check_prefill(L, desc(L=2 ** 31), ptrs()) == bd.E_SHAPE
-    assert check_step(L, desc(L=65), ptrs()) == bd.E_SHAPE
+    # blocks longer than 64 run on the sequence kernels (the paper's block length 256)
+    assert check_step(L, desc(L=65), ptrs()) == bd.OK
+    assert check_step(L, desc(L=256), ptrs()) == bd.OK
+    assert check_commit(L, desc(L=256), ptrs()) == bd.OK
+    d = desc(L=256)
+    d.x_stride[1] = (1 << 23) + 8                # too large a token stride for that path
+    d.x_stride[0] = d.x_stride[1] * 256
+    assert check_step(L, d, ptrs()) == bd.E_SHAPE
+    d = desc(L=64)
+    d.x_stride[1] = (1 << 23) + 8                # the fused block kernel has no such limit
+    d.x_stride[0] = d.x_stride[1] * 64
+    assert check_step(L, d, ptrs()) == bd.OK
 
 
 def test_full_window_checks(L):
@@ -364,3 +375,27 @@ def ws_bytes_b(L, d, K):
     n = ctypes.c_int64(-1)
     assert L.bdlm_boundary_states_workspace(ctypes.byref(d), K, ctypes.byref(n)) == bd.OK
     return n.value
+
+
+def check_sep(L, d, p=None, q=None, slots=None, nslots=4):
+    p = ptrs() if p is None else p
+    q = ptrs(x=FAKE + 0x20000, dt=FAKE + 0x21000, A=FAKE + 0x22000, B=FAKE + 0x23000,
+             C=FAKE + 0x24000, D=FAKE + 0x25000) if q is None else q
+    return L.bdlm_check_block_step_sep(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                       p["D"], q["x"], q["dt"], q["A"], q["B"], q["C"], q["D"],
+                                       p["h"], nslots, i32p(slots), p["y"])
+
+
+def test_block_step_sep_checks(L):
+    d = desc(batch=2, L=32)
+    assert check_sep(L, d) == bd.OK
+    assert check_sep(L, desc(batch=2, L=256)) == bd.OK
+    for field in ("x", "dt", "A", "B", "C", "D"):
+        q = ptrs(x=FAKE + 0x20000, dt=FAKE + 0x21000, A=FAKE + 0x22000, B=FAKE + 0x23000,
+                 C=FAKE + 0x24000, D=FAKE + 0x25000)
+        q[field] = None
+        assert check_sep(L, d, q=q) == bd.E_NULL, field
+    q = ptrs(x=FAKE + 0x20008)
+    assert check_sep(L, d, q=q) == bd.E_ALIGN
+    assert check_sep(L, d, p=ptrs(h=None)) == bd.E_NULL
+    assert check_sep(L, d, slots=np.array([5, 0], np.int32)) == bd.E_SLOT

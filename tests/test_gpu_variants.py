@@ -1,0 +1,117 @@
+"""GPU parity of the block-step variants against the fp64 oracle:
+
+* blocks longer than 64 tokens (the paper's block length 256, ragged lengths), at the
+  paper's layer widths (d_inner 896 and 1664: 14 and 26 heads of 64): step and commit;
+* separate reverse-direction inputs (the reverse branch with its own projections and
+  A, D): the oracle's forward part on the forward inputs plus its reverse part on the
+  reverse inputs.
+
+Bar: max relative error 2e-3 (tests/gpu_util.py); bookkeeping bit-exact.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import bdlm_inputs as bi
+import oracle
+from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[gpu-variants]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("H,N,L", [(14, 128, 256), (26, 128, 256), (4, 64, 65), (3, 16, 300),
+                                   (8, 128, 128)])
+def test_long_block_step(H, N, L):
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 3, H, 64, N, 1, L, 0, True, 1, 10000 + H + L)
+    d = bi.block_inputs(w, 0)
+    d["D_rev"] = (d["D"] * 0.75).astype(np.float32)
+    pool = bi.random_state(w, 5, 3, 0.5).astype(np.float64)
+    slots = [4, 1, 4]
+    v = to_dev(d)
+    say("long step", dict(H=H, N=N, L=L))
+    y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"],
+                           pool_dev(pool), slot_idx=slots)
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.block_step(d, pool, slot_idx=slots))
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
+@pytest.mark.parametrize("H,N,L,want_y", [(26, 128, 256, True), (14, 64, 256, False),
+                                          (4, 32, 100, True)])
+def test_long_block_commit(H, N, L, want_y):
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, H, 64, N, 1, L, 0, True, 1, 10100 + H + L)
+    d = bi.commit_inputs(w)
+    pool = bi.random_state(w, 3, 5, 0.5).astype(np.float64)
+    slots = [2, 0]
+    nb = np.array([3, 1, 3], np.int64)
+    nc = nb * L
+    ref_pool, ref_nc, ref_nb = pool.copy(), nc.copy(), nb.copy()
+    rc, y_ref = oracle.commit(d, ref_pool, ref_nc, ref_nb, slot_idx=slots, expected_block_index=3,
+                              want_y=True)
+    assert rc == 0
+    v = to_dev(d)
+    h = pool_dev(pool)
+    yc = True if want_y else None
+    out = bd.commit_boundary(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], h, nc, nb,
+                             3, slot_idx=slots, y_clean=yc)
+    torch.cuda.synchronize()
+    assert nc.tolist() == ref_nc.tolist() and nb.tolist() == ref_nb.tolist()
+    got = from_pool(h)
+    assert rel_err(got[slots], ref_pool[slots]) <= REL_TOL
+    np.testing.assert_array_equal(got[1], pool[1].astype(np.float32))     # untouched slot
+    if want_y:
+        assert rel_err(out, y_ref) <= REL_TOL
+
+
+def sep_inputs(w, seed):
+    """Forward inputs and independent reverse inputs (own x, dt, B, C, A, D)."""
+    fwd = bi.block_inputs(w, 0)
+    rev = bi.tokens(w, w.block_len, seed)
+    rp = bi.head_params(w, seed + 1)
+    rev.update({"A": rp["A"], "D": rp["D"], "D_rev": rp["D"]})
+    return fwd, rev
+
+
+@pytest.mark.parametrize("H,N,L,bf16", [(32, 128, 32, True), (4, 64, 256, True), (3, 16, 50, False),
+                                        (8, 128, 64, True)])
+def test_step_separate_reverse_inputs(H, N, L, bf16):
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, H, 64, N, 1, L, 0, bf16, 1, 10200 + H + L)
+    fwd, rev = sep_inputs(w, 10300 + L)
+    pool = bi.random_state(w, 2, 7, 0.5).astype(np.float64)
+    vf, vr = to_dev(fwd), to_dev(rev)
+    say("separate reverse inputs", dict(H=H, N=N, L=L, bf16=bf16))
+    y = bd.scan_block_step_sep((vf["x"], vf["dt"], vf["A"], vf["B"], vf["C"], vf["D"]),
+                               (vr["x"], vr["dt"], vr["A"], vr["B"], vr["C"], vr["D_rev"]),
+                               pool_dev(pool))
+    torch.cuda.synchronize()
+    _, yf, _ = oracle.block_step(fwd, pool, parts=True)
+    _, _, yr = oracle.block_step(rev, np.zeros_like(pool), parts=True)
+    e = rel_err(y, yf + yr)
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
+def test_step_separate_with_shared_inputs_equals_step():
+    """With the same inputs in both branches the variant is the ordinary step."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 4, 32, 64, 128, 1, 32, 0, True, 1, 10400)
+    d = bi.block_inputs(w, 0)
+    pool = pool_dev(bi.random_state(w, 4, 9, 0.5))
+    v = to_dev(d)
+    y1 = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], pool)
+    y2 = bd.scan_block_step_sep((v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"]),
+                                (v["x"], v["dt"], v["A"], v["B"], v["C"], v["D_rev"]), pool)
+    torch.cuda.synchronize()
+    ref = oracle.block_step(d, from_pool(pool).astype(np.float64))
+    assert rel_err(y1, ref) <= REL_TOL and rel_err(y2, ref) <= REL_TOL
