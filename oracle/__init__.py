@@ -16,6 +16,9 @@ C function follows are cited in that file:
 * ``scan_forward`` -- Eq. boundary-state: a clean prefix summarised by the forward scan.
 * ``full_window``  -- the full-sequence bidirectional (DiffuMamba-style) scan the paper
   contrasts against (Sec. 4; Sec. 5.1).
+* ``conv``         -- the convolution part of the Mamba boundary state (Sec. 2, Sec. 4;
+  App. C: width 4): forward continued from the cached last three input rows, reverse
+  zero-padded inside the block, SiLU; a commit keeps the last three rows.
 
 Inputs are the exact stored bytes the GPU reads: activations as fp32 or bf16
 (numpy ``uint16`` holding the bf16 bit pattern), ``A``/``D``/``D_rev`` fp32.
@@ -35,6 +38,7 @@ _LIB = os.path.join(_HERE, "liboracle_bdlm.so")
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+DTYPE_F64 = 2      # already-decoded values (e.g. convolution outputs)
 
 OK = 0
 ERR_ARG = -1
@@ -101,7 +105,9 @@ def _act(a: np.ndarray) -> tuple[np.ndarray, int]:
         return np.ascontiguousarray(a), DTYPE_BF16
     if a.dtype == np.float32:
         return np.ascontiguousarray(a), DTYPE_F32
-    raise TypeError(f"activation dtype must be float32 or uint16 (bf16 bits), got {a.dtype}")
+    if a.dtype == np.float64:
+        return np.ascontiguousarray(a), DTYPE_F64
+    raise TypeError(f"activation dtype must be float32, float64 or uint16 (bf16 bits), got {a.dtype}")
 
 
 def _shape(inp: dict) -> tuple[_Shape, dict]:
@@ -220,3 +226,43 @@ def decode(a: np.ndarray) -> np.ndarray:
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     return a.astype(np.float64)
+
+
+def conv(inp: dict, w: np.ndarray, bias: np.ndarray, cache: np.ndarray, slot_idx=None,
+         commit: bool = False):
+    """Width-4 depthwise causal convolution + SiLU over the x, B, C channels of a block
+    (``inp`` holds the pre-convolution x, B, C; channels x head-major, then B, then C).
+
+    ``w`` fp32 [channels, 4] (``w[:, 3]`` multiplies the current token), ``bias`` fp32
+    [channels], ``cache`` float64 [nslots, 3, channels] (row 0 the oldest input).
+    Returns ``(fwd, rev)``: dicts of float64 x, B, C -- the forward branch continues from
+    the cached rows, the reverse branch is zero-padded past the block end.  With
+    ``commit`` the cache rows become the last three rows of (cache rows ++ block).
+    """
+    x, dty = _act(inp["x"])
+    Bm, d2 = _act(inp["B"])
+    Cm, d3 = _act(inp["C"])
+    if len({dty, d2, d3}) != 1:
+        raise TypeError("x, B and C must share one storage dtype")
+    bsz, L, H, P = x.shape
+    _, _, G, N = Bm.shape
+    s = _Shape(bsz, H, P, N, G, L, dty)
+    ch = H * P + 2 * G * N
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    bias = np.ascontiguousarray(bias, dtype=np.float32)
+    if w.shape != (ch, 4) or bias.shape != (ch,) or cache.dtype != np.float64 \
+            or not cache.flags.c_contiguous or cache.shape[1:] != (3, ch):
+        raise ValueError("conv weights [channels, 4], bias [channels], cache float64 [n, 3, channels]")
+    out = [np.zeros(a.shape, np.float64) for a in (x, Bm, Cm, x, Bm, Cm)]
+    si = None if slot_idx is None else np.ascontiguousarray(slot_idx, dtype=np.int32)
+    L_ = lib()
+    L_.bdlm_oracle_conv.restype = ctypes.c_int
+    rc = L_.bdlm_oracle_conv(ctypes.byref(s), _v(x), _v(Bm), _v(Cm), _p(w, ctypes.c_float),
+                             _p(bias, ctypes.c_float), _p(cache, ctypes.c_double),
+                             ctypes.c_int64(cache.shape[0]), _p(si, ctypes.c_int32),
+                             ctypes.c_int(1 if commit else 0),
+                             *[_p(o, ctypes.c_double) for o in out])
+    if rc != OK:
+        raise ValueError(f"oracle conv failed: {rc}")
+    return dict(x=out[0], B=out[1], C=out[2]), dict(x=out[3], B=out[4], C=out[5])
+

@@ -20,6 +20,12 @@
  *     cache                                               (Sec. 3 BDLM cache; Sec. 4.1)
  *   - full-window bidirectional scan (DiffuMamba-style contrast: forward and
  *     reverse over the whole window, both from zero)      (Sec. 4, Sec. 5.1)
+ *   - the convolution part of the Mamba boundary state: a width-4 depthwise
+ *     causal convolution with SiLU over the x, B, C channels (App. C: Mamba
+ *     convolution width 4), continued from the cached last three input rows in
+ *     the forward branch and zero-padded inside the block in the reverse branch
+ *     (Sec. 2 and Sec. 4: the cached boundary state includes the convolution
+ *     state; the reverse scan is local to the active block)
  *
  * Every function takes the same stored bytes the GPU reads (fp32 or bf16
  * activations, fp32 per-head A / D / D_rev) and decodes them exactly to
@@ -45,6 +51,7 @@
 
 #define OR_DTYPE_F32 0
 #define OR_DTYPE_BF16 1
+#define OR_DTYPE_F64 2   /* already-decoded values, e.g. convolution outputs */
 
 #define OR_OK 0
 #define OR_ERR_ARG (-1)
@@ -65,6 +72,7 @@ static double rd(const void *base, int64_t i, int dtype)
         memcpy(&f, &bits, sizeof f);
         return (double)f;
     }
+    if (dtype == OR_DTYPE_F64) return ((const double *)base)[i];
     return (double)((const float *)base)[i];
 }
 
@@ -73,7 +81,9 @@ static int shape_ok(const or_shape *s)
     if (s->batch < 0 || s->len < 0) return 0;
     if (s->nheads <= 0 || s->headdim <= 0 || s->dstate <= 0 || s->ngroups <= 0) return 0;
     if (s->nheads % s->ngroups) return 0;
-    if (s->in_dtype != OR_DTYPE_F32 && s->in_dtype != OR_DTYPE_BF16) return 0;
+    if (s->in_dtype != OR_DTYPE_F32 && s->in_dtype != OR_DTYPE_BF16 &&
+        s->in_dtype != OR_DTYPE_F64)
+        return 0;
     return 1;
 }
 
@@ -280,6 +290,86 @@ int bdlm_oracle_full_window(const or_shape *s, const void *x, const void *dt, co
                                     y, NULL, NULL, NULL);
     free(zero);
     return rc;
+}
+
+/*
+ * The convolution of the Mamba mixer over one block, per batch row b and channel c
+ * of xBC (channels: x head-major h*headdim + p, then B g*dstate + n, then C), with
+ * pre-convolution inputs u[t] (decoded from the stored bytes), weights w[c][0..3]
+ * (w[c][3] multiplies the current token) and bias bc[c]:
+ *
+ *   forward  xf[t] = silu(bc + sum_k w[k] u[t - 3 + k]),  u[-3..-1] = cache rows 0..2
+ *   reverse  xr[t] = silu(bc + sum_k w[k] u[t + 3 - k]),  u[L..L+2] = 0
+ *
+ * The reverse line is the causal convolution of the flipped block from zeros,
+ * flipped back: the reverse branch stays inside the block.  silu(v) = v / (1 + e^-v).
+ * cache   [nslots][3][channels] double, row 0 the oldest input; with commit != 0
+ *         the rows become the last three rows of (cache rows ++ block).
+ * Outputs (double, layouts of x / B / C): xf, bf, cf (forward), xr, br, cr (reverse);
+ * any may be NULL.  slot_idx as for bdlm_oracle_block_step; with commit the slots
+ * must be distinct.
+ */
+static double silu(double v) { return v / (1.0 + exp(-v)); }
+
+int bdlm_oracle_conv(const or_shape *s, const void *x, const void *Bm, const void *Cm,
+                     const float *w, const float *bias, double *cache, int64_t nslots,
+                     const int32_t *slot_idx, int commit, double *xf, double *bf, double *cf,
+                     double *xr, double *br, double *cr)
+{
+    if (!shape_ok(s) || !w || !bias || !cache || nslots <= 0) return OR_ERR_ARG;
+    const int64_t L = s->len, HP = s->nheads * s->headdim, GN = s->ngroups * s->dstate;
+    const int64_t ch = HP + 2 * GN;
+    for (int64_t b = 0; b < s->batch; ++b) {
+        const int64_t sl = slot_idx ? slot_idx[b] : b;
+        if (sl < 0 || sl >= nslots) return OR_ERR_SLOT;
+        if (commit && slot_idx)
+            for (int64_t b2 = 0; b2 < b; ++b2)
+                if (slot_idx[b2] == sl) return OR_ERR_SLOT;
+    }
+    double *u = malloc((size_t)(L + 6) * sizeof(double));
+    if (!u) return OR_ERR_ARG;
+    for (int64_t b = 0; b < s->batch; ++b) {
+        const int64_t sl = slot_idx ? slot_idx[b] : b;
+        double *crow = cache + sl * 3 * ch;
+        for (int64_t c = 0; c < ch; ++c) {
+            /* u[0..2] cache rows, u[3..L+2] the block, u[L+3..L+5] zeros */
+            for (int k = 0; k < 3; ++k) u[k] = crow[k * ch + c];
+            double *of, *orv;
+            int64_t oi;
+            const void *src;
+            if (c < HP) {
+                const int64_t h = c / s->headdim, p = c % s->headdim;
+                src = x;
+                of = xf;
+                orv = xr;
+                oi = ix_x(s, b, 0, h, p);
+                for (int64_t t = 0; t < L; ++t) u[3 + t] = rd(x, ix_x(s, b, t, h, p), s->in_dtype);
+            } else {
+                const int64_t j = (c - HP) % GN, g = j / s->dstate, n = j % s->dstate;
+                src = c < HP + GN ? Bm : Cm;
+                of = c < HP + GN ? bf : cf;
+                orv = c < HP + GN ? br : cr;
+                oi = ix_bc(s, b, 0, g, n);
+                for (int64_t t = 0; t < L; ++t) u[3 + t] = rd(src, ix_bc(s, b, t, g, n), s->in_dtype);
+            }
+            for (int k = 0; k < 3; ++k) u[L + 3 + k] = 0.0;
+            /* token stride of this channel's output layout */
+            const int64_t ts = c < HP ? s->nheads * s->headdim : s->ngroups * s->dstate;
+            for (int64_t t = 0; t < L; ++t) {
+                double vf = bias[c], vr = bias[c];
+                for (int k = 0; k < 4; ++k) {
+                    vf += (double)w[c * 4 + k] * u[3 + t - 3 + k];
+                    vr += (double)w[c * 4 + k] * u[3 + t + 3 - k];
+                }
+                if (of) of[oi + t * ts] = silu(vf);
+                if (orv) orv[oi + t * ts] = silu(vr);
+            }
+            if (commit)
+                for (int k = 0; k < 3; ++k) crow[k * ch + c] = u[L + k];
+        }
+    }
+    free(u);
+    return OR_OK;
 }
 
 int bdlm_oracle_num_threads(void)

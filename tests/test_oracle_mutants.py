@@ -88,3 +88,45 @@ def test_mutant_is_caught(tmp_path, name, old, new, monkeypatch):
         except (AssertionError, ValueError):
             caught.append(i)
     assert caught, f"no pin catches mutant {name}"
+
+
+# Mutants of the convolution part (oracle.conv), caught by the convolution pins.
+import tests.test_oracle_conv as cpins  # noqa: E402
+
+CONV_MUTANTS = [
+    ("conv-kernel-reversed", "vf += (double)w[c * 4 + k] * u[3 + t - 3 + k];",
+     "vf += (double)w[c * 4 + 3 - k] * u[3 + t - 3 + k];"),
+    ("conv-no-silu", "if (of) of[oi + t * ts] = silu(vf);", "if (of) of[oi + t * ts] = vf;"),
+    ("conv-bias-dropped", "double vf = bias[c], vr = bias[c];", "double vf = 0.0, vr = bias[c];"),
+    ("conv-reverse-reads-cache", "for (int k = 0; k < 3; ++k) u[L + 3 + k] = 0.0;",
+     "for (int k = 0; k < 3; ++k) u[L + 3 + k] = u[k];"),
+    ("conv-reverse-window-shifted", "vr += (double)w[c * 4 + k] * u[3 + t + 3 - k];",
+     "vr += (double)w[c * 4 + k] * u[3 + t + 2 - k];"),
+    ("conv-cache-rows-reversed", "for (int k = 0; k < 3; ++k) u[k] = crow[k * ch + c];",
+     "for (int k = 0; k < 3; ++k) u[k] = crow[(2 - k) * ch + c];"),
+    ("conv-commit-keeps-first-rows", "for (int k = 0; k < 3; ++k) crow[k * ch + c] = u[L + k];",
+     "for (int k = 0; k < 3; ++k) crow[k * ch + c] = u[3 + k];"),
+]
+
+CONV_PINS = [
+    lambda: cpins.test_identity_kernel_gives_silu_of_the_input(),
+    lambda: cpins.test_against_numpy_correlate(5),
+    lambda: cpins.test_against_numpy_correlate(1),
+    lambda: cpins.test_reverse_is_flip_of_forward_from_zero(),
+    lambda: cpins.test_cache_continuation_equals_one_pass(),
+    lambda: cpins.test_commit_keeps_last_three_rows(1),
+    lambda: cpins.test_commit_keeps_last_three_rows(6),
+]
+
+
+@pytest.mark.parametrize("name,old,new", CONV_MUTANTS, ids=[m[0] for m in CONV_MUTANTS])
+def test_conv_mutant_is_caught(tmp_path, name, old, new, monkeypatch):
+    mut = _load_mutant(tmp_path, name, old, new)
+    monkeypatch.setattr(oracle, "_lib", mut)
+    caught = []
+    for i, pin in enumerate(CONV_PINS):
+        try:
+            pin()
+        except (AssertionError, ValueError):
+            caught.append(i)
+    assert caught, f"no pin catches mutant {name}"
