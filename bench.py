@@ -475,6 +475,31 @@ def run_variants(args) -> dict:
         "step_us": round(t_sep * 1e6, 2), "step_bytes": sb,
         "step_gbs": round(sb / t_sep / 1e9, 1)}
     del pools, y
+    # with the mixer's convolution (pre-convolution inputs, cached convolution rows)
+    ch = bd.conv_channels(32, 1, 128)
+    rng = np.random.Generator(np.random.PCG64(7000))
+    cw = torch.from_numpy((rng.standard_normal((ch, 4)) * 0.5).astype(np.float32)).to(dev)
+    cb = torch.from_numpy((rng.standard_normal(ch) * 0.1).astype(np.float32)).to(dev)
+    pools = [torch.zeros(bd.pool_shape(16, 32, 128), device=dev) for _ in range(nl)]
+    convs = [torch.zeros((16, 3, ch), device=dev) for _ in range(nl)]
+    y = torch.empty((16, 32, 32, 64), device=dev)
+    ws = torch.empty(bd._workspace_bytes(bd.lib().bdlm_conv_workspace,
+                                         bd._desc(f["x"], f["dt"], f["B"], f["C"])),
+                     dtype=torch.uint8, device=dev)
+    nc, nb = np.zeros(16, np.int64), np.zeros(16, np.int64)
+    t_cs = _graph_time(lambda li: bd.conv_block_step(f["x"], f["dt"], f["A"], f["B"], f["C"], f["D"],
+                                                     f["D_rev"], cw, cb, convs[li], pools[li], y=y,
+                                                     workspace=ws), nl)
+    t_cc = _graph_time(lambda li: bd.conv_commit_boundary(f["x"], f["dt"], f["A"], f["B"], f["C"],
+                                                          f["D"], f["D_rev"], cw, cb, convs[li],
+                                                          pools[li], nc.copy(), nb.copy(), -1,
+                                                          y_clean=y, workspace=ws), nl)
+    sb = step_bytes(16, 32, 64, 128, 1, 32) + 16 * 3 * ch * 4 + ch * 5 * 4
+    out["conv_L32"] = {
+        "workload": "350m-mamba-layer-b16-L32-with-conv-state",
+        "step_us": round(t_cs * 1e6, 2), "commit_us": round(t_cc * 1e6, 2), "step_bytes": sb,
+        "step_gbs": round(sb / t_cs / 1e9, 1)}
+    del pools, convs, y, ws
     torch.cuda.empty_cache()
     return out
 

@@ -193,6 +193,42 @@ int bdlm_scan_block_step_sep(const bdlm_desc_t *desc, const void *x, const void 
                              float *y, void *stream);
 
 /*
+ * Block step and commit with the convolution part of the Mamba boundary state
+ * (Sec. 2 and Sec. 4: the cached state includes the convolution state; App. C:
+ * convolution width 4).  x, B and C are the block's inputs BEFORE the mixer's
+ * depthwise causal convolution; per batch row b, channel c of xBC (x head-major
+ * h * 64 + p, then B g * dstate + n, then C), with weights conv_w[c][0..3]
+ * (conv_w[c][3] on the current token) and bias conv_b[c]:
+ *   forward branch  xf[t] = silu(conv_b[c] + sum_k conv_w[c][k] u[t - 3 + k]), u[-3..-1]
+ *                   the cached rows conv_pool[slot][0..2][c] (row 0 the oldest);
+ *   reverse branch  xr[t] = silu(conv_b[c] + sum_k conv_w[c][k] u[t + 3 - k]), zero past
+ *                   the block's end (the reverse branch stays inside the block);
+ * then the step of bdlm_scan_block_step_sep with the forward branch on (xf, dt, A, Bf,
+ * Cf, D) from the cached state and the reverse branch on (xr, dt, A, Br, Cr, D_rev)
+ * from zero.  A commit also replaces the slot's conv_pool rows by the last three rows
+ * of (cached rows ++ block) and updates h_pool from the forward branch.
+ * conv_w       device fp32 [channels][4], 16-byte aligned; conv_b fp32 [channels].
+ * conv_pool    device fp32 [nslots][3][channels] (same slots as h_pool).
+ * workspace    at least bdlm_conv_workspace bytes (the convolved inputs, fp32),
+ *              256-byte aligned.
+ * Any block length; two or three launches.  Errors: as bdlm_scan_block_step /
+ * bdlm_commit_boundary, and BDLM_E_WORKSPACE.
+ */
+int bdlm_conv_workspace(const bdlm_desc_t *desc, int64_t *bytes);
+int bdlm_conv_block_step(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, const float *D_rev,
+                         const float *conv_w, const float *conv_b, const float *conv_pool,
+                         const float *h_pool, int64_t nslots, const int32_t *slot_idx, float *y,
+                         void *workspace, int64_t workspace_bytes, void *stream);
+int bdlm_conv_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
+                              const float *A, const void *B, const void *C, const float *D,
+                              const float *D_rev, const float *conv_w, const float *conv_b,
+                              float *conv_pool, float *h_pool, int64_t nslots,
+                              const int32_t *slot_idx, int64_t *n_committed, int64_t *n_blocks,
+                              int64_t expected_block_index, float *y_clean, void *workspace,
+                              int64_t workspace_bytes, void *stream);
+
+/*
  * Full-window bidirectional scan, with no cache: the full-sequence
  * (DiffuMamba-style) scan that the paper's block-restricted scan replaces
  * (Sec. 4; Sec. 5.1).
@@ -317,6 +353,19 @@ int bdlm_check_block_step_sep(const bdlm_desc_t *desc, const void *x, const void
                               const void *B_rev, const void *C_rev, const float *D_rev,
                               const float *h_pool, int64_t nslots, const int32_t *slot_idx,
                               const float *y);
+int bdlm_check_conv_block_step(const bdlm_desc_t *desc, const void *x, const void *dt,
+                               const float *A, const void *B, const void *C, const float *D,
+                               const float *D_rev, const float *conv_w, const float *conv_b,
+                               const float *conv_pool, const float *h_pool, int64_t nslots,
+                               const int32_t *slot_idx, const float *y, const void *workspace,
+                               int64_t workspace_bytes);
+int bdlm_check_conv_commit(const bdlm_desc_t *desc, const void *x, const void *dt,
+                           const float *A, const void *B, const void *C, const float *D,
+                           const float *D_rev, const float *conv_w, const float *conv_b,
+                           const float *conv_pool, const float *h_pool, int64_t nslots,
+                           const int32_t *slot_idx, const int64_t *n_committed,
+                           const int64_t *n_blocks, int64_t expected_block_index,
+                           const float *y_clean, const void *workspace, int64_t workspace_bytes);
 int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
                            const float *A, const void *B, const void *C, const float *D,
                            const float *D_rev, const float *y, const void *workspace,

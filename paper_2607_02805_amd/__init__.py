@@ -92,6 +92,15 @@ def lib() -> ctypes.CDLL:
         L.bdlm_cache_reset.argtypes = [fp, i64, i64, i32p, i64, i64p, i64p, vp]
         L.bdlm_state_pack.argtypes = [fp, fp, i64, i64, vp]
         L.bdlm_state_unpack.argtypes = [fp, fp, i64, i64, vp]
+        L.bdlm_conv_workspace.argtypes = [dp, i64p]
+        L.bdlm_check_conv_block_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, fp, fp, fp, i64,
+                                                 i32p, fp, vp, i64]
+        L.bdlm_conv_block_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, fp, fp, fp, i64, i32p,
+                                           fp, vp, i64, vp]
+        L.bdlm_check_conv_commit.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, fp, fp, fp, i64, i32p,
+                                             i64p, i64p, i64, fp, vp, i64]
+        L.bdlm_conv_commit_boundary.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, fp, fp, fp, fp, i64,
+                                                i32p, i64p, i64p, i64, fp, vp, i64, vp]
         L.bdlm_check_block_step_sep.argtypes = [dp, vp, vp, fp, vp, vp, fp, vp, vp, fp, vp, vp,
                                                 fp, fp, i64, i32p, fp]
         L.bdlm_scan_block_step_sep.argtypes = [dp, vp, vp, fp, vp, vp, fp, vp, vp, fp, vp, vp, fp,
@@ -116,7 +125,9 @@ def lib() -> ctypes.CDLL:
                      "bdlm_full_window_workspace", "bdlm_prefill_workspace",
                      "bdlm_boundary_states_workspace", "bdlm_check_block_boundary_states",
                      "bdlm_block_boundary_states", "bdlm_check_block_step_sep",
-                     "bdlm_scan_block_step_sep"):
+                     "bdlm_scan_block_step_sep", "bdlm_conv_workspace",
+                     "bdlm_check_conv_block_step", "bdlm_conv_block_step",
+                     "bdlm_check_conv_commit", "bdlm_conv_commit_boundary"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -267,6 +278,83 @@ def scan_block_step_sep(fwd, rev, h_pool, y=None, slot_idx=None, stream=None):
     if rc != OK:
         raise BdlmError(rc, "bdlm_scan_block_step_sep")
     return y
+
+
+def conv_channels(nheads, ngroups, dstate) -> int:
+    """Channels of the mixer's convolution: x (nheads * 64), then B and C (ngroups * dstate)."""
+    return nheads * HEADDIM + 2 * ngroups * dstate
+
+
+def _conv_args(d, conv_w, conv_b, conv_pool, workspace, device):
+    torch = _torch()
+    ch = conv_channels(d.nheads, d.ngroups, d.dstate)
+    if conv_w.dtype != torch.float32 or tuple(conv_w.shape) != (ch, 4) or not conv_w.is_contiguous():
+        raise ValueError(f"conv_w must be a contiguous float32 [{ch}, 4] tensor")
+    if conv_b.dtype != torch.float32 or tuple(conv_b.shape) != (ch,) or not conv_b.is_contiguous():
+        raise ValueError(f"conv_b must be a contiguous float32 [{ch}] tensor")
+    if conv_pool.dtype != torch.float32 or conv_pool.dim() != 3 or \
+            tuple(conv_pool.shape[1:]) != (3, ch) or not conv_pool.is_contiguous():
+        raise ValueError(f"conv_pool must be a contiguous float32 [nslots, 3, {ch}] tensor")
+    wp, wb, keep = _workspace(lib().bdlm_conv_workspace, d, workspace, device)
+    return wp, wb, keep
+
+
+def conv_block_step(x, dt, A, B, C, D, D_rev, conv_w, conv_b, conv_pool, h_pool, y=None,
+                    slot_idx=None, stream=None, workspace=None):
+    """A denoising step with the mixer's convolution: x, B, C are pre-convolution inputs;
+    the forward branch's convolution continues from ``conv_pool`` (read only), the
+    reverse branch's is zero-padded inside the block.  Returns y (float32 [B, L, H, 64])."""
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    if y is None:
+        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
+    if conv_pool.shape[0] != h_pool.shape[0]:
+        raise ValueError("conv_pool and h_pool must have the same slots")
+    wp, wb, wkeep = _conv_args(d, conv_w, conv_b, conv_pool, workspace, x.device)
+    keep, sp = _slots(slot_idx)
+    rc = lib().bdlm_conv_block_step(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _dev_ptr(conv_w, "conv_w"), _dev_ptr(conv_b, "conv_b"), _dev_ptr(conv_pool, "conv_pool"),
+        _pool(h_pool, H, N), h_pool.shape[0], sp, _dev_ptr(y, "y"), wp, wb, _stream_handle(stream))
+    del keep, wkeep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_conv_block_step")
+    return y
+
+
+def conv_commit_boundary(x, dt, A, B, C, D, D_rev, conv_w, conv_b, conv_pool, h_pool, n_committed,
+                         n_blocks, expected_block_index=-1, slot_idx=None, y_clean=None,
+                         stream=None, workspace=None):
+    """Commit with the mixer's convolution: the SSM states advance over the forward
+    branch's convolved block and ``conv_pool`` keeps the last three pre-convolution rows."""
+    torch = _torch()
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    nslots = h_pool.shape[0]
+    if conv_pool.shape[0] != nslots:
+        raise ValueError("conv_pool and h_pool must have the same slots")
+    for a in (n_committed, n_blocks):
+        if not isinstance(a, np.ndarray) or a.dtype != np.int64 or a.shape != (nslots,):
+            raise ValueError(f"n_committed / n_blocks must be numpy int64 [{nslots}]")
+    if y_clean is True:
+        y_clean = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
+                              device=x.device)
+    wp, wb, wkeep = _conv_args(d, conv_w, conv_b, conv_pool, workspace, x.device)
+    keep, sp = _slots(slot_idx)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_conv_commit_boundary(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _dev_ptr(conv_w, "conv_w"), _dev_ptr(conv_b, "conv_b"), _dev_ptr(conv_pool, "conv_pool"),
+        _pool(h_pool, H, N), nslots, sp, n_committed.ctypes.data_as(i64p),
+        n_blocks.ctypes.data_as(i64p), int(expected_block_index),
+        None if y_clean is None else _dev_ptr(y_clean, "y_clean"), wp, wb, _stream_handle(stream))
+    del keep, wkeep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_conv_commit_boundary")
+    return y_clean
 
 
 def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
@@ -526,12 +614,29 @@ class Cache:
     per slot).  :meth:`states` returns the states as row-major [nslots, nheads, 64, dstate].
     """
 
-    def __init__(self, nslots: int, nheads: int, dstate: int, device="cuda"):
+    def __init__(self, nslots: int, nheads: int, dstate: int, device="cuda", ngroups: int = 0):
+        """``ngroups`` > 0 also keeps the mixer's convolution rows (``conv``, float32
+        [nslots, 3, channels]) for :meth:`conv_step` / :meth:`conv_commit`."""
         torch = _torch()
         self.h = torch.zeros(pool_shape(nslots, nheads, dstate), dtype=torch.float32,
                              device=device)
+        self.conv = None
+        if ngroups > 0:
+            self.conv = torch.zeros((nslots, 3, conv_channels(nheads, ngroups, dstate)),
+                                    dtype=torch.float32, device=device)
         self.n_committed = np.zeros(nslots, np.int64)
         self.n_blocks = np.zeros(nslots, np.int64)
+
+    def conv_step(self, x, dt, A, B, C, D, D_rev, conv_w, conv_b, y=None, slot_idx=None,
+                  stream=None):
+        return conv_block_step(x, dt, A, B, C, D, D_rev, conv_w, conv_b, self.conv, self.h, y,
+                               slot_idx, stream)
+
+    def conv_commit(self, x, dt, A, B, C, D, D_rev, conv_w, conv_b, expected_block_index=-1,
+                    slot_idx=None, y_clean=None, stream=None):
+        return conv_commit_boundary(x, dt, A, B, C, D, D_rev, conv_w, conv_b, self.conv, self.h,
+                                    self.n_committed, self.n_blocks, expected_block_index,
+                                    slot_idx, y_clean, stream)
 
     def step(self, x, dt, A, B, C, D, D_rev, y=None, slot_idx=None, stream=None):
         return scan_block_step(x, dt, A, B, C, D, D_rev, self.h, y, slot_idx, stream)
@@ -549,6 +654,8 @@ class Cache:
 
     def reset(self, slots=None, stream=None):
         cache_reset(self.h, slots, self.n_committed, self.n_blocks, stream)
+        if self.conv is not None:
+            cache_reset(self.conv, slots, stream=stream)
 
     def states(self, stream=None):
         """The cached states as a row-major [nslots, nheads, 64, dstate] tensor."""
@@ -560,12 +667,17 @@ class Cache:
 
     def state_dict(self) -> dict:
         """Checkpoint: the states (on the host) and the bookkeeping."""
-        return {"h": self.h.detach().cpu(), "n_committed": self.n_committed.copy(),
-                "n_blocks": self.n_blocks.copy()}
+        sd = {"h": self.h.detach().cpu(), "n_committed": self.n_committed.copy(),
+              "n_blocks": self.n_blocks.copy()}
+        if self.conv is not None:
+            sd["conv"] = self.conv.detach().cpu()
+        return sd
 
     def load_state_dict(self, sd: dict) -> None:
         if tuple(sd["h"].shape) != tuple(self.h.shape):
             raise ValueError("checkpoint shape does not match this cache")
         self.h.copy_(sd["h"])
+        if self.conv is not None:
+            self.conv.copy_(sd["conv"])
         self.n_committed[:] = sd["n_committed"]
         self.n_blocks[:] = sd["n_blocks"]

@@ -387,6 +387,90 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
     return BDLM_OK;
 }
 
+int bdlm_conv_workspace(const bdlm_desc_t *d, int64_t *bytes) {
+    if (!bytes) return BDLM_E_NULL;
+    const int rc = check_desc(d, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    *bytes = bdlm::conv_workspace(d->batch, d->block_len, d->nheads, d->ngroups, d->dstate);
+    return BDLM_OK;
+}
+
+static int check_conv(const bdlm_desc_t *d, const float *conv_w, const float *conv_b,
+                      const float *conv_pool, const void *ws, int64_t ws_bytes) {
+    if (!conv_w || !conv_b || !conv_pool) return BDLM_E_NULL;
+    if (!aligned(conv_w, 16) || !aligned(conv_b, 4) || !aligned(conv_pool, 4)) return BDLM_E_ALIGN;
+    // the convolved inputs are scanned from the (fp32, contiguous) workspace
+    if (d->nheads * BDLM_HEADDIM * 4 > (int64_t(1) << 24)) return BDLM_E_SHAPE;
+    return check_workspace(ws, ws_bytes,
+                           bdlm::conv_workspace(d->batch, d->block_len, d->nheads, d->ngroups,
+                                                d->dstate));
+}
+
+int bdlm_check_conv_block_step(const bdlm_desc_t *d, const void *x, const void *dt,
+                               const float *A, const void *B, const void *C, const float *D,
+                               const float *D_rev, const float *conv_w, const float *conv_b,
+                               const float *conv_pool, const float *h_pool, int64_t nslots,
+                               const int32_t *slot_idx, const float *y, const void *workspace,
+                               int64_t workspace_bytes) {
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    if (!y && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
+    if (!aligned(y, 4)) return BDLM_E_ALIGN;
+    return check_conv(d, conv_w, conv_b, conv_pool, workspace, workspace_bytes);
+}
+
+int bdlm_conv_block_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, const float *D_rev,
+                         const float *conv_w, const float *conv_b, const float *conv_pool,
+                         const float *h_pool, int64_t nslots, const int32_t *slot_idx, float *y,
+                         void *workspace, int64_t workspace_bytes, void *stream) {
+    const int rc = bdlm_check_conv_block_step(d, x, dt, A, B, C, D, D_rev, conv_w, conv_b,
+                                              conv_pool, h_pool, nslots, slot_idx, y, workspace,
+                                              workspace_bytes);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs a =
+        make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
+    return bdlm::launch_conv_block(a, conv_w, conv_b, const_cast<float *>(conv_pool), false,
+                                   workspace, stream);
+}
+
+int bdlm_check_conv_commit(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                           const void *B, const void *C, const float *D, const float *D_rev,
+                           const float *conv_w, const float *conv_b, const float *conv_pool,
+                           const float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                           const int64_t *n_committed, const int64_t *n_blocks,
+                           int64_t expected_block_index, const float *y_clean,
+                           const void *workspace, int64_t workspace_bytes) {
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx, BDLM_MAX_SEQ_LEN);
+    if (rc != BDLM_OK) return rc;
+    if (!aligned(y_clean, 4)) return BDLM_E_ALIGN;
+    rc = check_conv(d, conv_w, conv_b, conv_pool, workspace, workspace_bytes);
+    if (rc != BDLM_OK) return rc;
+    return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
+}
+
+int bdlm_conv_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                              const void *B, const void *C, const float *D, const float *D_rev,
+                              const float *conv_w, const float *conv_b, float *conv_pool,
+                              float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                              int64_t *n_committed, int64_t *n_blocks,
+                              int64_t expected_block_index, float *y_clean, void *workspace,
+                              int64_t workspace_bytes, void *stream) {
+    int rc = bdlm_check_conv_commit(d, x, dt, A, B, C, D, D_rev, conv_w, conv_b, conv_pool, h_pool,
+                                    nslots, slot_idx, n_committed, n_blocks, expected_block_index,
+                                    y_clean, workspace, workspace_bytes);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
+    rc = bdlm::launch_conv_block(a, conv_w, conv_b, conv_pool, true, workspace, stream);
+    if (rc != BDLM_OK) return rc;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        n_committed[s] += d->block_len;
+        n_blocks[s] += 1;
+    }
+    return BDLM_OK;
+}
+
 int bdlm_scan_full_window(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
                           const void *B, const void *C, const float *D, const float *D_rev,
                           float *y, void *workspace, int64_t workspace_bytes, void *stream) {

@@ -1,0 +1,178 @@
+// bdlm_conv.hip -- the convolution part of the Mamba boundary state on gfx950: a
+// width-4 depthwise causal convolution with SiLU over the x, B and C channels of the
+// active block (the Mamba-2 mixer's convolution, App. C), in two versions -- the
+// forward branch continues from the cached last three input rows, the reverse branch
+// (local to the block, Sec. 4) is zero-padded past the block's end -- and, for a
+// commit, the cache rows replaced by the last three rows of (cache ++ block).
+//
+// One thread per (batch row, channel); channels are contiguous across threads, so a
+// token's row is one coalesced read.  Each thread runs a three-row shift register up
+// the block (forward) and down it (reverse); after the forward pass the register holds
+// exactly the rows the cache must keep.  Outputs are fp32 in the scan's input layouts
+// (plus dt widened to fp32), consumed by the sequence kernels.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bdlm.h"
+#include "bdlm_launch.h"
+
+namespace bdlm {
+namespace {
+
+struct ConvArgs {
+    const void *x, *Bm, *Cm, *dt;
+    int64_t xs_b, xs_t, xs_h, dts_b, dts_t, bcs_b, bcs_t, bcs_g;
+    const float *w, *bias;      // [channels][4] (w[c][3] on the current token), [channels]
+    float *cache;               // [nslots][3][channels], row 0 the oldest input
+    float *out;                 // fp32: xf, bf, cf, xr, br, cr, dtf (see conv_workspace)
+    int32_t batch, L, nheads, ngroups, dstate, bf16, commit, use_slots;
+    int32_t slots[BDLM_MAX_SLOT_ROWS];
+};
+
+__device__ __forceinline__ float load_act(const void *p, int64_t i, int bf16) {
+    if (bf16)
+        return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t *>(p)[i]) << 16);
+    return static_cast<const float *>(p)[i];
+}
+__device__ __forceinline__ float silu(float v) { return v / (1.f + expf(-v)); }
+
+__global__ void __launch_bounds__(256) bdlm_conv_kernel(const ConvArgs a) {
+    const int HP = a.nheads * 64, GN = a.ngroups * a.dstate, CH = HP + 2 * GN;
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int b = blockIdx.y;
+    if (c >= CH) return;
+    const int64_t L = a.L;
+    const int64_t BL = static_cast<int64_t>(a.batch) * L;
+
+    // where this channel lives: input element offset of token 0, token stride, and
+    // the fp32 output plane / row width
+    const void *src;
+    int64_t in0, in_t;
+    int plane;            // 0 x, 1 B, 2 C
+    int64_t o0, o_t;      // output offset of token 0 and token stride within the plane
+    if (c < HP) {
+        const int h = c / 64, p = c % 64;
+        src = a.x;
+        in0 = b * a.xs_b + h * a.xs_h + p;
+        in_t = a.xs_t;
+        plane = 0;
+        o0 = b * L * HP + c;
+        o_t = HP;
+    } else {
+        const int j = (c - HP) % GN, g = j / a.dstate, n = j % a.dstate;
+        plane = c < HP + GN ? 1 : 2;
+        src = plane == 1 ? a.Bm : a.Cm;
+        in0 = b * a.bcs_b + g * a.bcs_g + n;
+        in_t = a.bcs_t;
+        o0 = b * L * GN + j;
+        o_t = GN;
+    }
+    // output planes: [xf | bf | cf | xr | br | cr | dtf]
+    float *planes[6];
+    planes[0] = a.out;
+    planes[1] = planes[0] + BL * HP;
+    planes[2] = planes[1] + BL * GN;
+    planes[3] = planes[2] + BL * GN;
+    planes[4] = planes[3] + BL * HP;
+    planes[5] = planes[4] + BL * GN;
+    float *dtf = planes[5] + BL * GN;
+    float *of = planes[plane] + o0, *orv = planes[3 + plane] + o0;
+
+    const float4 wv = *reinterpret_cast<const float4 *>(a.w + static_cast<int64_t>(c) * 4);
+    const float bc = a.bias[c];
+    const int64_t slot = a.use_slots ? a.slots[b] : b;
+    float *crow = a.cache + slot * 3 * CH + c;
+
+    // forward: u[t-3], u[t-2], u[t-1] in p0, p1, p2 (the cached rows before token 0)
+    float p0 = crow[0], p1 = crow[CH], p2 = crow[2 * CH];
+    for (int64_t t = 0; t < L; ++t) {
+        const float u = load_act(src, in0 + t * in_t, a.bf16);
+        of[t * o_t] = silu(bc + wv.x * p0 + wv.y * p1 + wv.z * p2 + wv.w * u);
+        p0 = p1;
+        p1 = p2;
+        p2 = u;
+    }
+    // reverse: u[t+1], u[t+2], u[t+3] in n1, n2, n3 (zeros past the block's end)
+    float n1 = 0.f, n2 = 0.f, n3 = 0.f;
+    for (int64_t t = L - 1; t >= 0; --t) {
+        const float u = load_act(src, in0 + t * in_t, a.bf16);
+        orv[t * o_t] = silu(bc + wv.x * n3 + wv.y * n2 + wv.z * n1 + wv.w * u);
+        n3 = n2;
+        n2 = n1;
+        n1 = u;
+    }
+    if (a.commit) {   // the last three rows of (cache ++ block)
+        crow[0] = p0;
+        crow[CH] = p1;
+        crow[2 * CH] = p2;
+    }
+    // dt widened to fp32 (one thread per head)
+    if (c < a.nheads)
+        for (int64_t t = 0; t < L; ++t)
+            dtf[(b * L + t) * a.nheads + c] = load_act(a.dt, b * a.dts_b + t * a.dts_t + c, a.bf16);
+}
+
+}  // namespace
+
+int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, float *conv_pool,
+                      bool commit, void *ws, void *stream) {
+    if (a.batch == 0 || a.L == 0) return BDLM_OK;
+    ConvArgs k;
+    k.x = a.x;
+    k.Bm = a.Bm;
+    k.Cm = a.Cm;
+    k.dt = a.dt;
+    k.xs_b = a.xs_b;
+    k.xs_t = a.xs_t;
+    k.xs_h = a.xs_h;
+    k.dts_b = a.dts_b;
+    k.dts_t = a.dts_t;
+    k.bcs_b = a.bcs_b;
+    k.bcs_t = a.bcs_t;
+    k.bcs_g = a.bcs_g;
+    k.w = w;
+    k.bias = bias;
+    k.cache = conv_pool;
+    k.out = static_cast<float *>(ws);
+    k.batch = a.batch;
+    k.L = a.L;
+    k.nheads = a.nheads;
+    k.ngroups = a.ngroups;
+    k.dstate = a.dstate;
+    k.bf16 = a.bf16;
+    k.commit = commit ? 1 : 0;
+    k.use_slots = a.slots ? 1 : 0;
+    for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
+        k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
+    const int ch = a.nheads * 64 + 2 * a.ngroups * a.dstate;
+    hipLaunchKernelGGL(bdlm_conv_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), k);
+    if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
+
+    // the scan over the convolved inputs: fp32, contiguous, in the workspace
+    const int64_t BL = static_cast<int64_t>(a.batch) * a.L;
+    const int64_t HP = a.nheads * 64, GN = static_cast<int64_t>(a.ngroups) * a.dstate;
+    float *base = static_cast<float *>(ws);
+    LaunchArgs f = a, r = a;
+    for (LaunchArgs *p : {&f, &r}) {
+        p->bf16 = 0;
+        p->xs_b = a.L * HP;
+        p->xs_t = HP;
+        p->xs_h = 64;
+        p->dts_b = static_cast<int64_t>(a.L) * a.nheads;
+        p->dts_t = a.nheads;
+        p->bcs_b = a.L * GN;
+        p->bcs_t = GN;
+        p->bcs_g = a.dstate;
+        p->dt = base + 2 * BL * (HP + 2 * GN);
+    }
+    f.x = base;
+    f.Bm = base + BL * HP;
+    f.Cm = base + BL * (HP + GN);
+    r.x = base + BL * (HP + 2 * GN);
+    r.Bm = base + BL * (2 * HP + 2 * GN);
+    r.Cm = base + BL * (2 * HP + 3 * GN);
+    return launch_block_long(f, r, commit, a.y != nullptr, stream);
+}
+
+}  // namespace bdlm

@@ -87,6 +87,18 @@ inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t nblocks
 int launch_block_long(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
                       void *stream);
 
+// The convolution part of the boundary state, then the block step (commit: the
+// commit) on the convolved inputs: a.x / a.Bm / a.Cm are the pre-convolution inputs,
+// conv_pool [nslots][3][channels] the cached input rows (a commit replaces them).
+// ws: conv_workspace bytes (fp32 convolved x, B, C for both branches and dt).
+int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, float *conv_pool,
+                      bool commit, void *ws, void *stream);
+inline int64_t conv_workspace(int64_t batch, int64_t L, int64_t nheads, int64_t ngroups,
+                              int64_t dstate) {
+    const int64_t HP = nheads * BDLM_HEADDIM, GN = ngroups * dstate;
+    return (batch * L * (2 * HP + 4 * GN + nheads) * 4 + 255) / 256 * 256;
+}
+
 // Permute nstates states between row-major [64][dstate] and the pool layout.
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream);

@@ -31,7 +31,10 @@
 // dstate), B and x transposed (operands over tokens), dt and its decay sums.  The
 // decay-weighted Gram tiles C.B^T (10 lower-triangle 16x16 tiles) are shared out
 // over the waves and published in LDS; each wave then forms its columns' y and
-// updates its state rows on bf16 MFMA, with fp32 operands split hi + lo.
+// updates its state rows on MFMA: bf16 storage on bf16 MFMA (fp32 operands such as
+// states and decay-weighted tiles split hi + lo, the bf16 activations exact), fp32
+// storage on fp32 MFMA (every operand fp32, e.g. convolution outputs, which would lose
+// accuracy in a two-term bf16 split).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -104,6 +107,19 @@ __device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {   // a.hi1
     return (a >> 16) | (b & 0xffff0000u);
 }
 __device__ __forceinline__ float ex2(float v) { return __builtin_amdgcn_exp2f(v); }
+
+// c += a b over one quad on fp32 MFMA: instruction r contracts lane group g's value
+// r, i.e. index 4g + r of the quad layout.
+__device__ __forceinline__ f32x4 mma_f32q(f32x4 a, f32x4 b, f32x4 c) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r], b[r], c, 0, 0, 0);
+    return c;
+}
+// The LDS operand images hold bf16 quads (uint2) for bf16 storage and fp32 quads
+// (f32x4, in the same arrays at twice the size) for fp32 storage.
+__device__ __forceinline__ f32x4 f32q(const uint2 *img, int i) {
+    return reinterpret_cast<const f32x4 *>(img)[i];
+}
 
 // Decode the workgroup into (batch row, segment, head): consecutive units of one
 // (row, segment) share B and C, so they are kept on one XCD.
@@ -225,18 +241,14 @@ struct Stager {
     }
 
     // Row image of B or C (operand over dstate) from one task's four token rows.
-    template <typename U2>
-    __device__ __forceinline__ static void row_image(const u32x4 (&v)[4], int g, int pc, U2 *hi,
-                                                     U2 *lo) {
+    __device__ __forceinline__ static void row_image(const u32x4 (&v)[4], int g, int pc,
+                                                     uint2 *hi) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int j = 4 * g + r;
             if constexpr (F32) {
-                s16x4 h, l;
-                split4(__builtin_bit_cast(f32x4, v[r]), h, l);
                 const int at = img_idx<G::QN, true>(j >> 4, pc >> 2, pc & 3, j & 15);
-                hi[at] = as_u2(h);
-                lo[at] = as_u2(l);
+                reinterpret_cast<f32x4 *>(hi)[at] = __builtin_bit_cast(f32x4, v[r]);
             } else {
                 const int q0 = 2 * pc, q1 = 2 * pc + 1;
                 hi[img_idx<G::QN, false>(j >> 4, q0 >> 2, q0 & 3, j & 15)] = uint2{v[r].x, v[r].y};
@@ -256,10 +268,9 @@ struct Stager {
         }
     }
 
-    // Write the registers of the current chunk into LDS.  bt / btl: transposed B
-    // (hi / lo), sb / sbl and sc / scl: row images, xt: transposed x.
-    __device__ __forceinline__ void stage(int tid, uint2 *sb, uint2 *sbl, uint2 *sc, uint2 *scl,
-                                          uint2 *bt, uint2 *btl,
+    // Write the registers of the current chunk into LDS.  bt: transposed B, sb and sc:
+    // row images, xt: transposed x.
+    __device__ __forceinline__ void stage(int tid, uint2 *sb, uint2 *sc, uint2 *bt,
                                           typename XQuad<F32>::T *xt) const {
 #pragma unroll
         for (int k = 0; k < G::BPT; ++k) {
@@ -267,19 +278,15 @@ struct Stager {
             if (task < G::BT) {
                 const int g = task / G::BCPR, pc = task % G::BCPR;
                 if constexpr (LOADC) {
-                    row_image(rb[k], g, pc, sb, sbl);
-                    row_image(rc[k], g, pc, sc, scl);
+                    row_image(rb[k], g, pc, sb);
+                    row_image(rc[k], g, pc, sc);
                 }
                 if constexpr (F32) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const f32x4 v = {__uint_as_float(rb[k][0][e]), __uint_as_float(rb[k][1][e]),
-                                         __uint_as_float(rb[k][2][e]), __uint_as_float(rb[k][3][e])};
-                        s16x4 h, l;
-                        split4(v, h, l);
-                        bt[g * NS + pc * 4 + e] = as_u2(h);
-                        btl[g * NS + pc * 4 + e] = as_u2(l);
-                    }
+                    for (int e = 0; e < 4; ++e)
+                        reinterpret_cast<f32x4 *>(bt)[g * NS + pc * 4 + e] =
+                            f32x4{__uint_as_float(rb[k][0][e]), __uint_as_float(rb[k][1][e]),
+                                  __uint_as_float(rb[k][2][e]), __uint_as_float(rb[k][3][e])};
                 } else {
                     transpose_bf16(rb[k], g * NS + pc * 8, bt);
                 }
@@ -352,7 +359,7 @@ __device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4
                                           f32x4 &val) {
     if constexpr (F32) {
         val = v;
-        split4(v, hi, lo);
+        hi = lo = s16x4{0, 0, 0, 0};
     } else {
         hi = as_s16x4(v);
         val = f32x4{bf16_to_f32(hi[0]), bf16_to_f32(hi[1]), bf16_to_f32(hi[2]), bf16_to_f32(hi[3])};
@@ -363,27 +370,37 @@ __device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4
 // The transposed-B operand quads of dstate tile q (tokens 16jt + 4grp .. +3,
 // column 16q + col) and the state update of one 16 x 16 (dstate, column) tile over
 // the chunk's 64 tokens: acc += B^T (wh + wl), wh + wl the weighted x quads.
+template <bool F32> struct BtOps;
+template <> struct BtOps<false> { s16x4 h[4]; };
+template <> struct BtOps<true> { f32x4 f[4]; };
+// weighted x quads: bf16 hi + lo (bf16 storage) or fp32 (fp32 storage)
+template <bool F32> struct WOps;
+template <> struct WOps<false> { s16x4 h[4], l[4]; };
+template <> struct WOps<true> { f32x4 f[4]; };
 template <bool F32>
-struct BtOps {
-    s16x4 h[4], l[F32 ? 4 : 1];
-};
+__device__ __forceinline__ void w_set(WOps<F32> &o, int jt, f32x4 v) {
+    if constexpr (F32) o.f[jt] = v;
+    else split4(v, o.h[jt], o.l[jt]);
+}
 template <int NS, bool F32>
-__device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, const uint2 *btl, int q,
-                                        int grp, int col) {
+__device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, int q, int grp, int col) {
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
-        o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
-        if constexpr (F32) o.l[jt] = as_s16x4(btl[(4 * jt + grp) * NS + 16 * q + col]);
+        if constexpr (F32) o.f[jt] = f32q(bt, (4 * jt + grp) * NS + 16 * q + col);
+        else o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
     }
 }
 template <bool F32>
-__device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const s16x4 (&wh)[4],
-                                        const s16x4 (&wl)[4], f32x4 acc) {
+__device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const WOps<F32> &w, f32x4 acc) {
+    if constexpr (F32) {
 #pragma unroll
-    for (int jt = 0; jt < 4; jt += 2) {
-        acc = mma_k32(o.h[jt], o.h[jt + 1], wh[jt], wh[jt + 1], acc);
-        acc = mma_k32(o.h[jt], o.h[jt + 1], wl[jt], wl[jt + 1], acc);
-        if constexpr (F32) acc = mma_k32(o.l[jt], o.l[jt + 1], wh[jt], wh[jt + 1], acc);
+        for (int jt = 0; jt < 4; ++jt) acc = mma_f32q(o.f[jt], w.f[jt], acc);
+    } else {
+#pragma unroll
+        for (int jt = 0; jt < 4; jt += 2) {
+            acc = mma_k32(o.h[jt], o.h[jt + 1], w.h[jt], w.h[jt + 1], acc);
+            acc = mma_k32(o.h[jt], o.h[jt + 1], w.l[jt], w.l[jt + 1], acc);
+        }
     }
     return acc;
 }
@@ -417,8 +434,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
     using G = Geo<NS, F32>;
     using AT = typename Act<F32>::T;
     constexpr int QN = G::QN;
-    __shared__ __align__(16) uint2 sBt[16 * NS];
-    __shared__ __align__(16) uint2 sBtl[F32 ? 16 * NS : 1];
+    __shared__ __align__(16) uint2 sBt[(F32 ? 2 : 1) * 16 * NS];
     __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
     __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC], sWr[kC];
 
@@ -444,34 +460,32 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
-        st.stage(tid, nullptr, nullptr, nullptr, nullptr, sBt, sBtl, sXt);
+        st.stage(tid, nullptr, nullptr, sBt, sXt);
         if (wave == 0)
             decay_sums<BOTH>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, sWr);
         __syncthreads();
         if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
 
         const float tot = sCs[kC - 1];
-        s16x4 fh[4], fl[4], rh[4], rl[4];
+        WOps<F32> wf, wr;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             s16x4 xh, xl;
             f32x4 xv;
             x_operand<F32>(sXt[(4 * jt + grp) * kP + p], xh, xl, xv);
-            const f32x4 wf = *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]);
-            split4(wf * xv, fh[jt], fl[jt]);
-            if constexpr (BOTH) {
-                const f32x4 wr = *reinterpret_cast<const f32x4 *>(&sWr[16 * jt + 4 * grp]);
-                split4(wr * xv * ex2(off), rh[jt], rl[jt]);
-            }
+            w_set<F32>(wf, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv);
+            if constexpr (BOTH)
+                w_set<F32>(wr, jt,
+                           *reinterpret_cast<const f32x4 *>(&sWr[16 * jt + 4 * grp]) * xv * ex2(off));
         }
         const float keep = ex2(tot);
         BtOps<F32> cur, nxt;
-        bt_read<NS, F32>(cur, sBt, sBtl, 0, grp, col);
+        bt_read<NS, F32>(cur, sBt, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
-            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, sBtl, q + 1, grp, col);
-            F[q] = bt_mma<F32>(cur, fh, fl, F[q] * keep);
-            if constexpr (BOTH) R[q] = bt_mma<F32>(cur, rh, rl, R[q]);
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, grp, col);
+            F[q] = bt_mma<F32>(cur, wf, F[q] * keep);
+            if constexpr (BOTH) R[q] = bt_mma<F32>(cur, wr, R[q]);
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -495,10 +509,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
     using AT = typename Act<F32>::T;
     constexpr int QN = G::QN;
     constexpr int IMG = G::IMG;
-    __shared__ __align__(16) uint2 sB[IMG], sC[IMG];
-    __shared__ __align__(16) uint2 sBl[F32 ? IMG : 1], sCl[F32 ? IMG : 1];
-    __shared__ __align__(16) uint2 sBt[16 * NS];
-    __shared__ __align__(16) uint2 sBtl[F32 ? 16 * NS : 1];
+    __shared__ __align__(16) uint2 sB[(F32 ? 2 : 1) * IMG], sC[(F32 ? 2 : 1) * IMG];
+    __shared__ __align__(16) uint2 sBt[(F32 ? 2 : 1) * 16 * NS];
     __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
     __shared__ __align__(16) uint4 sM[kTiles * 64];
     __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC];
@@ -540,7 +552,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
-        st.stage(tid, sB, sBl, sC, sCl, sBt, sBtl, sXt);
+        st.stage(tid, sB, sC, sBt, sXt);
         if (wave == 0)
             decay_sums<false>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, nullptr);
         __syncthreads();
@@ -554,26 +566,29 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         for (int k = wave; k < ntiles; k += 4) {
             const int mt = k < 1 ? 0 : (k < 3 ? 1 : (k < 6 ? 2 : 3));
             const int jt = k - mt * (mt + 1) / 2;
-            s16x4 bq[QN], cq[QN], blq[F32 ? QN : 1], clq[F32 ? QN : 1];
+            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (F32) {
+                f32x4 bq[QN], cq[QN];
 #pragma unroll
-            for (int q = 0; q < QN; ++q) {
-                bq[q] = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
-                cq[q] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-                if constexpr (F32) {
-                    blq[q] = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
-                    clq[q] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
+                for (int q = 0; q < QN; ++q) {
+                    bq[q] = f32q(sB, img_idx<QN, true>(jt, q, grp, col));
+                    cq[q] = f32q(sC, img_idx<QN, true>(mt, q, grp, col));
                 }
+#pragma unroll
+                for (int q = 0; q < QN; ++q) gacc = mma_f32q(bq[q], cq[q], gacc);
+            } else {
+                s16x4 bq[QN], cq[QN];
+#pragma unroll
+                for (int q = 0; q < QN; ++q) {
+                    bq[q] = as_s16x4(sB[img_idx<QN, false>(jt, q, grp, col)]);
+                    cq[q] = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
+                }
+                gacc = mma_quads<QN>(bq, cq, gacc);
             }
             const int t = 16 * mt + col;
             const float cst = sCs[t];
             const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
             const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
-            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
-            gacc = mma_quads<QN>(bq, cq, gacc);
-            if constexpr (F32) {
-                gacc = mma_quads<QN>(bq, clq, gacc);
-                gacc = mma_quads<QN>(blq, cq, gacc);
-            }
             f32x4 m;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -581,10 +596,14 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 const float w = ex2(cst - csj[r]) * dtj[r];
                 m[r] = j <= t ? gacc[r] * w : 0.f;
             }
-            s16x4 mh, ml;
-            split4(m, mh, ml);
-            const uint2 h2 = as_u2(mh), l2 = as_u2(ml);
-            sM[k * 64 + lane] = uint4{h2.x, h2.y, l2.x, l2.y};
+            if constexpr (F32) {
+                sM[k * 64 + lane] = __builtin_bit_cast(uint4, m);
+            } else {
+                s16x4 mh, ml;
+                split4(m, mh, ml);
+                const uint2 h2 = as_u2(mh), l2 = as_u2(ml);
+                sM[k * 64 + lane] = uint4{h2.x, h2.y, l2.x, l2.y};
+            }
         }
 
         // prefix term 2^{cs_t} (C_t . S) for this wave's columns; the state is split
@@ -593,18 +612,25 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) Y[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (a.y) {
+        if constexpr (F32) {
+#pragma unroll
+            for (int q = 0; q < QN; ++q) {
+                f32x4 cq[4];
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) cq[mt] = f32q(sC, img_idx<QN, true>(mt, q, grp, col));
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) Y[mt] = mma_f32q(cq[mt], S[q], Y[mt]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
 #pragma unroll
         for (int q = 0; q < QN; q += 2) {
             if (q + 1 < QN) {
-                s16x4 c0[4], c1[4], d0[F32 ? 4 : 1], d1[F32 ? 4 : 1];
+                s16x4 c0[4], c1[4];
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
-                    c0[mt] = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-                    c1[mt] = as_s16x4(sC[img_idx<QN, F32>(mt, q + 1, grp, col)]);
-                    if constexpr (F32) {
-                        d0[mt] = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                        d1[mt] = as_s16x4(sCl[img_idx<QN, F32>(mt, q + 1, grp, col)]);
-                    }
+                    c0[mt] = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
+                    c1[mt] = as_s16x4(sC[img_idx<QN, false>(mt, q + 1, grp, col)]);
                 }
                 s16x4 h0, l0, h1, l1;
                 split4(S[q], h0, l0);
@@ -613,23 +639,19 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 for (int mt = 0; mt < 4; ++mt) {
                     Y[mt] = mma_k32(c0[mt], c1[mt], h0, h1, Y[mt]);
                     Y[mt] = mma_k32(c0[mt], c1[mt], l0, l1, Y[mt]);
-                    if constexpr (F32) Y[mt] = mma_k32(d0[mt], d1[mt], h0, h1, Y[mt]);
                 }
             } else {
                 s16x4 h0, l0;
                 split4(S[q], h0, l0);
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
-                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
                     Y[mt] = mma_k16(c0, h0, Y[mt]);
                     Y[mt] = mma_k16(c0, l0, Y[mt]);
-                    if constexpr (F32) {
-                        const s16x4 d0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                        Y[mt] = mma_k16(d0, h0, Y[mt]);
-                    }
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
+        }
         }
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
@@ -656,6 +678,12 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         // intra-chunk term: y += M x over j <= t
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
+            if constexpr (F32) {
+#pragma unroll
+                for (int jt = 0; jt <= mt; ++jt)
+                    Y[mt] = mma_f32q(__builtin_bit_cast(f32x4, sM[(mt * (mt + 1) / 2 + jt) * 64 + lane]),
+                                     xvf[jt], Y[mt]);
+            } else {
 #pragma unroll
             for (int jt = 0; jt <= mt; jt += 2) {
                 const uint4 v0 = sM[(mt * (mt + 1) / 2 + jt) * 64 + lane];
@@ -665,12 +693,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     const s16x4 h1 = as_s16x4(uint2{v1.x, v1.y}), l1 = as_s16x4(uint2{v1.z, v1.w});
                     Y[mt] = mma_k32(h0, h1, xh[jt], xh[jt + 1], Y[mt]);
                     Y[mt] = mma_k32(l0, l1, xh[jt], xh[jt + 1], Y[mt]);
-                    if constexpr (F32) Y[mt] = mma_k32(h0, h1, xl[jt], xl[jt + 1], Y[mt]);
                 } else {
                     Y[mt] = mma_k16(h0, xh[jt], Y[mt]);
                     Y[mt] = mma_k16(l0, xh[jt], Y[mt]);
-                    if constexpr (F32) Y[mt] = mma_k16(h0, xl[jt], Y[mt]);
                 }
+            }
             }
         }
 
@@ -701,19 +728,17 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         // carry the state across the chunk (not after the last one unless it is kept)
         if (c + 1 == nch && !a.pool_out) break;
         const float keep = ex2(sCs[kC - 1]);
-        s16x4 wh[4], wl[4];
+        WOps<F32> wx;
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
-            const f32x4 w = *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]);
-            split4(w * xv(jt), wh[jt], wl[jt]);
-        }
+        for (int jt = 0; jt < 4; ++jt)
+            w_set<F32>(wx, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv(jt));
         BtOps<F32> cur, nxt;
-        bt_read<NS, F32>(cur, sBt, sBtl, 0, grp, col);
+        bt_read<NS, F32>(cur, sBt, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
             // the next tile's operands are read while this tile's MFMAs run
-            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, sBtl, q + 1, grp, col);
-            S[q] = bt_mma<F32>(cur, wh, wl, S[q] * keep);
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, grp, col);
+            S[q] = bt_mma<F32>(cur, wx, S[q] * keep);
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }

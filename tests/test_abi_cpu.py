@@ -399,3 +399,31 @@ def test_block_step_sep_checks(L):
     assert check_sep(L, d, q=q) == bd.E_ALIGN
     assert check_sep(L, d, p=ptrs(h=None)) == bd.E_NULL
     assert check_sep(L, d, slots=np.array([5, 0], np.int32)) == bd.E_SLOT
+
+
+def test_conv_entry_point_checks(L):
+    d = desc(batch=2, H=4, N=32, L=32)
+    ch = 4 * 64 + 2 * 32
+    n = ctypes.c_int64(-1)
+    assert L.bdlm_conv_workspace(ctypes.byref(d), ctypes.byref(n)) == bd.OK
+    assert n.value == (2 * 32 * (2 * 256 + 4 * 32 + 4) * 4 + 255) // 256 * 256
+    p = ptrs()
+    cw, cb, cp = FAKE + 0x30000, FAKE + 0x31000, FAKE + 0x32000
+
+    def step(cw=cw, cb=cb, cp=cp, ws=WS, wsb=BIG):
+        return L.bdlm_check_conv_block_step(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"],
+                                            p["C"], p["D"], p["Drev"], cw, cb, cp, p["h"], 4,
+                                            None, p["y"], ws, wsb)
+    assert step() == bd.OK
+    assert step(cw=None) == bd.E_NULL and step(cb=None) == bd.E_NULL and step(cp=None) == bd.E_NULL
+    assert step(cw=cw + 8) == bd.E_ALIGN
+    assert step(wsb=n.value - 4) == bd.E_WORKSPACE
+    nc, nb = np.zeros(4, np.int64), np.array([1, 1, 2, 2], np.int64)
+    rc = L.bdlm_check_conv_commit(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                  p["Drev"], cw, cb, cp, p["h"], 4, None, i64p(nc), i64p(nb), 1,
+                                  None, WS, BIG)
+    assert rc == bd.OK
+    rc = L.bdlm_check_conv_commit(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
+                                  p["Drev"], cw, cb, cp, p["h"], 4, i32p(np.array([1, 1], np.int32)),
+                                  i64p(nc), i64p(nb), -1, None, WS, BIG)
+    assert rc == bd.E_SLOT
