@@ -432,7 +432,6 @@ __device__ __forceinline__ void setup(ST &st, const SeqArgs &a, const Unit &un, 
 template <int NS, bool F32, bool BOTH>
 __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(const SeqArgs a) {
     using G = Geo<NS, F32>;
-    using AT = typename Act<F32>::T;
     constexpr int QN = G::QN;
     __shared__ __align__(16) uint2 sBt[(F32 ? 2 : 1) * 16 * NS];
     __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
@@ -506,7 +505,6 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 template <int NS, bool F32, bool REV>
 __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(const SeqArgs a) {
     using G = Geo<NS, F32>;
-    using AT = typename Act<F32>::T;
     constexpr int QN = G::QN;
     constexpr int IMG = G::IMG;
     __shared__ __align__(16) uint2 sB[(F32 ? 2 : 1) * IMG], sC[(F32 ? 2 : 1) * IMG];
