@@ -5,11 +5,12 @@
 // (local to the block, Sec. 4) is zero-padded past the block's end -- and, for a
 // commit, the cache rows replaced by the last three rows of (cache ++ block).
 //
-// One thread per (batch row, channel); channels are contiguous across threads, so a
-// token's row is one coalesced read.  Each thread runs a three-row shift register up
-// the block (forward) and down it (reverse); after the forward pass the register holds
-// exactly the rows the cache must keep.  Outputs are fp32 in the scan's input layouts
-// (plus dt widened to fp32), consumed by the sequence kernels.
+// One thread per (batch row, channel, 8-token tile); channels are contiguous across
+// threads, so a token's row is one coalesced read.  A thread loads its tile with a
+// three-row halo on each side (cached rows before the block, zeros after it) and
+// computes both branches from registers; a commit's new cache rows are written by a
+// second small kernel once every tile has read the old ones.  Outputs are fp32 in the
+// scan's input layouts (plus dt widened to fp32), consumed by the sequence kernels.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -36,20 +37,24 @@ __device__ __forceinline__ float load_act(const void *p, int64_t i, int bf16) {
 }
 __device__ __forceinline__ float silu(float v) { return v / (1.f + expf(-v)); }
 
+constexpr int kTT = 8;   // tokens per thread
+
+// grid: (channel blocks of 256, batch rows, token tiles of kTT)
 __global__ void __launch_bounds__(256) bdlm_conv_kernel(const ConvArgs a) {
     const int HP = a.nheads * 64, GN = a.ngroups * a.dstate, CH = HP + 2 * GN;
     const int c = blockIdx.x * 256 + threadIdx.x;
     const int b = blockIdx.y;
+    const int t0 = blockIdx.z * kTT;
     if (c >= CH) return;
     const int64_t L = a.L;
     const int64_t BL = static_cast<int64_t>(a.batch) * L;
 
     // where this channel lives: input element offset of token 0, token stride, and
-    // the fp32 output plane / row width
+    // the fp32 output plane / offset of token 0 / token stride within the plane
     const void *src;
     int64_t in0, in_t;
     int plane;            // 0 x, 1 B, 2 C
-    int64_t o0, o_t;      // output offset of token 0 and token stride within the plane
+    int64_t o0, o_t;
     if (c < HP) {
         const int h = c / 64, p = c % 64;
         src = a.x;
@@ -83,33 +88,61 @@ __global__ void __launch_bounds__(256) bdlm_conv_kernel(const ConvArgs a) {
     const int64_t slot = a.use_slots ? a.slots[b] : b;
     float *crow = a.cache + slot * 3 * CH + c;
 
-    // forward: u[t-3], u[t-2], u[t-1] in p0, p1, p2 (the cached rows before token 0)
-    float p0 = crow[0], p1 = crow[CH], p2 = crow[2 * CH];
-    for (int64_t t = 0; t < L; ++t) {
-        const float u = load_act(src, in0 + t * in_t, a.bf16);
-        of[t * o_t] = silu(bc + wv.x * p0 + wv.y * p1 + wv.z * p2 + wv.w * u);
-        p0 = p1;
-        p1 = p2;
-        p2 = u;
+    // inputs u[t0 - 3 .. t0 + kTT + 2]: cached rows before token 0, zeros past L
+    float u[kTT + 6];
+#pragma unroll
+    for (int i = 0; i < kTT + 6; ++i) {
+        const int64_t t = t0 - 3 + i;
+        u[i] = t < 0 ? crow[(t + 3) * CH] : (t < L ? load_act(src, in0 + t * in_t, a.bf16) : 0.f);
     }
-    // reverse: u[t+1], u[t+2], u[t+3] in n1, n2, n3 (zeros past the block's end)
-    float n1 = 0.f, n2 = 0.f, n3 = 0.f;
-    for (int64_t t = L - 1; t >= 0; --t) {
-        const float u = load_act(src, in0 + t * in_t, a.bf16);
-        orv[t * o_t] = silu(bc + wv.x * n3 + wv.y * n2 + wv.z * n1 + wv.w * u);
-        n3 = n2;
-        n2 = n1;
-        n1 = u;
-    }
-    if (a.commit) {   // the last three rows of (cache ++ block)
-        crow[0] = p0;
-        crow[CH] = p1;
-        crow[2 * CH] = p2;
+#pragma unroll
+    for (int i = 0; i < kTT; ++i) {
+        const int64_t t = t0 + i;
+        if (t < L) {
+            // forward: u[t-3 .. t]; reverse: u[t .. t+3] (zeros past the block's end)
+            of[t * o_t] = silu(bc + wv.x * u[i] + wv.y * u[i + 1] + wv.z * u[i + 2] + wv.w * u[i + 3]);
+            orv[t * o_t] =
+                silu(bc + wv.x * u[i + 6] + wv.y * u[i + 5] + wv.z * u[i + 4] + wv.w * u[i + 3]);
+        }
     }
     // dt widened to fp32 (one thread per head)
     if (c < a.nheads)
-        for (int64_t t = 0; t < L; ++t)
-            dtf[(b * L + t) * a.nheads + c] = load_act(a.dt, b * a.dts_b + t * a.dts_t + c, a.bf16);
+        for (int i = 0; i < kTT; ++i)
+            if (t0 + i < L)
+                dtf[(b * L + t0 + i) * a.nheads + c] =
+                    load_act(a.dt, b * a.dts_b + (t0 + i) * a.dts_t + c, a.bf16);
+}
+
+// A commit's cache rows: the last three rows of (cache ++ block), one thread per
+// (batch row, channel).  A kernel of its own, launched after the convolution, so that
+// no tile of the convolution can read rows it already replaced.
+__global__ void __launch_bounds__(256) bdlm_conv_keep_kernel(const ConvArgs a) {
+    const int HP = a.nheads * 64, GN = a.ngroups * a.dstate, CH = HP + 2 * GN;
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int b = blockIdx.y;
+    if (c >= CH) return;
+    const void *src;
+    int64_t in0, in_t;
+    if (c < HP) {
+        src = a.x;
+        in0 = b * a.xs_b + (c / 64) * a.xs_h + c % 64;
+        in_t = a.xs_t;
+    } else {
+        const int j = (c - HP) % GN;
+        src = c < HP + GN ? a.Bm : a.Cm;
+        in0 = b * a.bcs_b + (j / a.dstate) * a.bcs_g + j % a.dstate;
+        in_t = a.bcs_t;
+    }
+    const int64_t slot = a.use_slots ? a.slots[b] : b;
+    float *crow = a.cache + slot * 3 * CH + c;
+    float r[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        const int64_t t = static_cast<int64_t>(a.L) - 3 + k;   // < 0: an older cached row
+        r[k] = t < 0 ? crow[(t + 3) * CH] : load_act(src, in0 + t * in_t, a.bf16);
+    }
+#pragma unroll
+    for (int k = 0; k < 3; ++k) crow[k * CH] = r[k];
 }
 
 }  // namespace
@@ -145,9 +178,14 @@ int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, fl
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
         k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
     const int ch = a.nheads * 64 + 2 * a.ngroups * a.dstate;
-    hipLaunchKernelGGL(bdlm_conv_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
-                       static_cast<hipStream_t>(stream), k);
+    hipLaunchKernelGGL(bdlm_conv_kernel, dim3((ch + 255) / 256, a.batch, (a.L + kTT - 1) / kTT),
+                       dim3(256), 0, static_cast<hipStream_t>(stream), k);
     if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
+    if (commit) {
+        hipLaunchKernelGGL(bdlm_conv_keep_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
+                           static_cast<hipStream_t>(stream), k);
+        if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
+    }
 
     // the scan over the convolved inputs: fp32, contiguous, in the workspace
     const int64_t BL = static_cast<int64_t>(a.batch) * a.L;
