@@ -273,9 +273,7 @@ int bdlm_boundary_states_workspace(const bdlm_desc_t *d, int64_t n_blocks, int64
     const int rc = check_desc(d, BDLM_MAX_BLOCK_LEN);
     if (rc != BDLM_OK) return rc;
     if (n_blocks < 0) return BDLM_E_SHAPE;
-    *bytes = (d->batch == 0 || d->block_len == 0) ? 0
-                                                  : bdlm::boundary_workspace(d->batch, d->nheads,
-                                                                             n_blocks);
+    *bytes = bdlm::boundary_workspace(d->batch, d->nheads, d->dstate, n_blocks, d->block_len);
     return BDLM_OK;
 }
 
@@ -302,7 +300,9 @@ int bdlm_check_block_boundary_states(const bdlm_desc_t *d, int64_t n_blocks, con
     if (!s_out && !empty) return BDLM_E_NULL;
     if (!aligned(s_out, 16) || !aligned(s_init, 16) || !aligned(y_fwd, 4)) return BDLM_E_ALIGN;
     return check_workspace(workspace, workspace_bytes,
-                           empty ? 0 : bdlm::boundary_workspace(d->batch, d->nheads, n_blocks));
+                           empty ? 0
+                                 : bdlm::boundary_workspace(d->batch, d->nheads, d->dstate,
+                                                            n_blocks, d->block_len));
 }
 
 int bdlm_block_boundary_states(const bdlm_desc_t *d, int64_t n_blocks, const void *x,

@@ -73,11 +73,31 @@ int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream);
 // s_out[(row * nblocks + k) * nheads + head] (pool layout) = the forward state after
 // blocks 0 .. k-1, starting from s_init[row * nheads + head] (nullptr: zero).  a.y
 // (optional) receives the forward outputs of the sequence.  ws: boundary_workspace
-// bytes (one log-decay per row, head and block).
+// bytes.  The blocks go in segments of blocks_per_seg (sized for ~4096 workgroups);
+// the workspace holds one state and one log-decay per (row, head, segment).
+struct BoundaryPlan {
+    int64_t blocks_per_seg, nseg, state_bytes, total_bytes;
+};
+inline BoundaryPlan boundary_plan(int64_t batch, int64_t nheads, int64_t dstate, int64_t nblocks,
+                                  int64_t L) {
+    BoundaryPlan p;
+    const int64_t units = batch * nheads;
+    const int64_t want = units >= 4096 ? 1 : (4096 + units - 1) / units;   // segments per row
+    p.blocks_per_seg = (nblocks + want - 1) / want;
+    if (p.blocks_per_seg * L < 256) p.blocks_per_seg = (256 + L - 1) / L;   // >= 256 tokens
+    if (p.blocks_per_seg > nblocks) p.blocks_per_seg = nblocks > 0 ? nblocks : 1;
+    p.nseg = nblocks > 0 ? (nblocks + p.blocks_per_seg - 1) / p.blocks_per_seg : 1;
+    p.state_bytes = units * p.nseg * int64_t(BDLM_HEADDIM) * dstate * 4;
+    p.total_bytes = p.state_bytes + (units * p.nseg * 4 + 255) / 256 * 256;
+    return p;
+}
 int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_init,
                            float *s_out, void *ws, void *stream);
-inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t nblocks) {
-    return (batch * nheads * nblocks * 4 + 255) / 256 * 256;
+inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t dstate, int64_t nblocks,
+                                  int64_t L) {
+    if (batch == 0 || nblocks == 0 || L == 0) return 0;
+    const BoundaryPlan p = boundary_plan(batch, nheads, dstate, nblocks, L);
+    return p.nseg > 1 ? p.total_bytes : 0;   // one segment: a single sweep, no workspace
 }
 
 // A block of any length (a.L) as one segment per row: the forward branch from the

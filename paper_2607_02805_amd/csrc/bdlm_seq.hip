@@ -69,6 +69,12 @@ struct SeqArgs {
     // seg_out with one segment per row (a block step or commit of any length):
     const float *pool_in;        // the entering state from the cache (slot per row)
     float *pool_out;             // the final state written back to the cache (in place)
+    // seg_out, forward: chunks of cstride (<= 64) tokens, and the state entering every
+    // chunk written to emit[(row * emit_blocks + block) * nheads + head] (block = the
+    // chunk's index in the sequence; segments hold whole chunks)
+    int32_t cstride;
+    float *emit;
+    int64_t emit_blocks;
     int32_t use_slots;
     int32_t slots[BDLM_MAX_SLOT_ROWS];
 };
@@ -159,19 +165,24 @@ struct Stager {
     const char *xg, *dtg, *Bg, *Cg;  // this (row, head / group) at token 0
     int64_t xrow, dtrow, bcrow;      // bytes between consecutive tokens
     int64_t s0, s1;
+    int cstride;                     // tokens per chunk (64; forward: any <= 64)
     uint32_t ob[G::BPT][4], ox[G::XPT][G::XROWS], odt;   // per-thread byte offsets
     u32x4 rb[G::BPT][4], rc[LOADC ? G::BPT : 1][4], rx[G::XPT][G::XROWS];
     uint32_t dtraw;
 
+    static constexpr bool kRev = REV;
     __device__ __forceinline__ static int row(int i) { return REV ? kC - 1 - i : i; }
 
     // first token of chunk c's memory window, and the number of valid local tokens
     __device__ __forceinline__ int64_t window(int c) const {
-        return REV ? s1 - static_cast<int64_t>(kC) * (c + 1) : s0 + static_cast<int64_t>(kC) * c;
+        return REV ? s1 - static_cast<int64_t>(kC) * (c + 1) : s0 + static_cast<int64_t>(cstride) * c;
     }
     __device__ __forceinline__ int valid(int c) const {
-        const int64_t v = (s1 - s0) - static_cast<int64_t>(kC) * c;
-        return v < kC ? static_cast<int>(v) : kC;
+        const int64_t v = (s1 - s0) - static_cast<int64_t>(cstride) * c;
+        return v < cstride ? static_cast<int>(v) : cstride;
+    }
+    __device__ __forceinline__ int nchunks() const {
+        return static_cast<int>((s1 - s0 + cstride - 1) / cstride);
     }
     // global token of local token i of chunk c; false outside the segment
     __device__ __forceinline__ bool token(int c, int i, int64_t &t) const {
@@ -423,6 +434,7 @@ __device__ __forceinline__ void setup(ST &st, const SeqArgs &a, const Unit &un, 
     st.bcrow = a.bcs_t * ES;
     st.s0 = static_cast<int64_t>(un.seg) * a.S;
     st.s1 = st.s0 + a.S < a.T ? st.s0 + a.S : a.T;
+    st.cstride = ST::kRev ? kC : a.cstride;
     st.init(tid, lane);
 }
 
@@ -446,7 +458,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 
     Stager<NS, F32, false, false> st;
     setup(st, a, un, g, tid, lane);
-    const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
+    const int nch = st.nchunks();
     const float A2 = a.A[un.h] * kLog2e;
 
     f32x4 F[QN], R[BOTH ? QN : 1];
@@ -522,7 +534,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 
     Stager<NS, F32, REV, true> st;
     setup(st, a, un, g, tid, lane);
-    const int nch = static_cast<int>((st.s1 - st.s0 + kC - 1) / kC);
+    const int nch = st.nchunks();
     const float A2 = a.A[un.h] * kLog2e;
     const float skip = a.skip[un.h];
 
@@ -542,6 +554,17 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
     }
+    // states entering the segment's chunks (blocks), forward only
+    float *emit_base = nullptr;
+    int64_t emit_first = 0;
+    if (!REV && a.emit) {
+        emit_first = (static_cast<int64_t>(un.seg) * a.S) / a.cstride;
+        emit_base = a.emit + (static_cast<int64_t>(un.b) * a.emit_blocks * a.nheads + un.h) * (kP * NS);
+        float *dst = emit_base + emit_first * a.nheads * (kP * NS);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) *reinterpret_cast<f32x4 *>(dst + quad_off(q, grp, p)) = S[q];
+    }
+
     // y of this (row, head) at token 0, bytes between tokens, and this lane's offset of
     // local token 4grp within a chunk's memory window (tokens 16mt + r further on)
     const float *ybase = a.y + (static_cast<int64_t>(un.b) * a.T * a.nheads + un.h) * kP;
@@ -740,6 +763,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }
+        if (emit_base && c + 1 < nch) {   // the next segment writes the state entering it
+            float *dst = emit_base + (emit_first + c + 1) * a.nheads * (kP * NS);
+#pragma unroll
+            for (int q = 0; q < QN; ++q) *reinterpret_cast<f32x4 *>(dst + quad_off(q, grp, p)) = S[q];
+        }
         __syncthreads();   // LDS is rewritten by the next chunk
     }
     if (a.pool_out) {
@@ -783,20 +811,43 @@ __global__ void __launch_bounds__(256) bdlm_seg_combine_kernel(const CombineArgs
         pst = c.pool + (slot * c.nheads + h) * c.state_floats + e;
         s = *reinterpret_cast<const f32x4 *>(pst);
     }
-    for (int k = 0; k < c.nseg; ++k) {
-        f32x4 *f = seg(k);
-        const f32x4 fk = *f;
-        *f = s;
-        s = s * ex2(tot[k]) + fk;
+    // the recurrence is sequential but its inputs are not: segments go in groups of
+    // kG whose loads are all issued before the group's (cheap) arithmetic
+    constexpr int kG = 8;
+    for (int k0 = 0; k0 < c.nseg; k0 += kG) {
+        f32x4 fk[kG];
+        float tk[kG];
+#pragma unroll
+        for (int i = 0; i < kG; ++i)
+            if (k0 + i < c.nseg) {
+                fk[i] = *seg(k0 + i);
+                tk[i] = tot[k0 + i];
+            }
+#pragma unroll
+        for (int i = 0; i < kG; ++i)
+            if (k0 + i < c.nseg) {
+                *seg(k0 + i) = s;
+                s = s * ex2(tk[i]) + fk[i];
+            }
     }
     if (c.write_final) *reinterpret_cast<f32x4 *>(pst) = s;
     if (c.dirs == 2) {
         f32x4 r = {0.f, 0.f, 0.f, 0.f};
-        for (int k = c.nseg - 1; k >= 0; --k) {
-            f32x4 *f = seg(k) + c.state_floats / 4;
-            const f32x4 rk = *f;
-            *f = r;
-            r = r * ex2(tot[k]) + rk;
+        for (int k0 = c.nseg - 1; k0 >= 0; k0 -= kG) {
+            f32x4 rk[kG];
+            float tk[kG];
+#pragma unroll
+            for (int i = 0; i < kG; ++i)
+                if (k0 - i >= 0) {
+                    rk[i] = *(seg(k0 - i) + c.state_floats / 4);
+                    tk[i] = tot[k0 - i];
+                }
+#pragma unroll
+            for (int i = 0; i < kG; ++i)
+                if (k0 - i >= 0) {
+                    *(seg(k0 - i) + c.state_floats / 4) = r;
+                    r = r * ex2(tk[i]) + rk[i];
+                }
         }
     }
 }
@@ -869,6 +920,9 @@ SeqArgs seq_args(const LaunchArgs &a, int64_t T, const SeqPlan &pl, void *ws) {
     k.blk_major = 0;
     k.pool_in = nullptr;
     k.pool_out = nullptr;
+    k.cstride = kC;
+    k.emit = nullptr;
+    k.emit_blocks = 0;
     k.use_slots = a.slots ? 1 : 0;
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
         k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
@@ -953,29 +1007,39 @@ int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_
                            float *s_out, void *ws, void *stream) {
     if (a.batch == 0 || nblocks == 0) return BDLM_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // one segment per block; the block states live in s_out, the segment decays in ws
+    // segments of G whole blocks: local segment states (seg_state), the states entering
+    // the segments (seg_combine), then one sweep per segment, a block per chunk, that
+    // writes every block's entering state (and the forward outputs if wanted)
+    const BoundaryPlan bp = boundary_plan(a.batch, a.nheads, a.dstate, nblocks, a.L);
     SeqPlan pl;
-    pl.seg_len = a.L;
-    pl.nseg = nblocks;
+    pl.seg_len = bp.blocks_per_seg * a.L;
+    pl.nseg = bp.nseg;
     pl.dirs = 1;
-    pl.state_bytes = 0;
-    pl.total_bytes = 0;
-    SeqArgs k = seq_args(a, nblocks * a.L, pl, s_out);
-    k.tot = static_cast<float *>(ws);
-    k.blk_major = 1;
-    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * nblocks);
+    pl.state_bytes = bp.state_bytes;
+    pl.total_bytes = bp.total_bytes;
+    SeqArgs k = seq_args(a, nblocks * a.L, pl, bp.nseg > 1 ? ws : nullptr);
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * bp.nseg);
     const bool f32 = !a.bf16;
-    if ((f32 ? run_state<true>(a.dstate, k, false, grid, s)
-             : run_state<false>(a.dstate, k, false, grid, s)) != hipSuccess)
-        return BDLM_E_LAUNCH;
-    if (combine(a, pl, k, const_cast<float *>(s_init), false, s) != hipSuccess) return BDLM_E_LAUNCH;
-    if (a.y) {
-        k.zero_init = 0;
-        k.skip = a.D;
-        if ((f32 ? run_out<true>(a.dstate, k, false, grid, s)
-                 : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+    if (bp.nseg > 1 || s_init) {
+        if (bp.nseg > 1 && (f32 ? run_state<true>(a.dstate, k, false, grid, s)
+                                : run_state<false>(a.dstate, k, false, grid, s)) != hipSuccess)
             return BDLM_E_LAUNCH;
+        if (bp.nseg == 1) {   // one segment: its entering state is s_init itself
+            k.pool_in = s_init;
+            k.use_slots = 0;
+        } else {
+            if (combine(a, pl, k, const_cast<float *>(s_init), false, s) != hipSuccess)
+                return BDLM_E_LAUNCH;
+            k.zero_init = 0;
+        }
     }
+    k.cstride = a.L;
+    k.emit = s_out;
+    k.emit_blocks = nblocks;
+    k.skip = a.D;
+    if ((f32 ? run_out<true>(a.dstate, k, false, grid, s)
+             : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
+        return BDLM_E_LAUNCH;
     return BDLM_OK;
 }
 

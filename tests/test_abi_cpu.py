@@ -361,11 +361,16 @@ def test_boundary_states_checks(L):
     assert check_bstates(L, desc(L=65)) == bd.E_SHAPE                 # blocks of at most 64
     assert check_bstates(L, d, K=(2 ** 31) // 32 + 1) == bd.E_SHAPE   # sequence too long
     assert check_bstates(L, desc(batch=1 << 10, H=1 << 10), K=2 ** 11) == bd.E_SHAPE   # grid
-    need = ws_bytes_b(L, d, 4)
-    assert need == (2 * 4 * 4 * 4 + 255) // 256 * 256
-    assert check_bstates(L, d, ws=WS, wsb=need) == bd.OK
-    assert check_bstates(L, d, ws=WS, wsb=need - 4) == bd.E_WORKSPACE
-    assert check_bstates(L, d, ws=None, wsb=need) == bd.E_WORKSPACE
+    assert ws_bytes_b(L, d, 4) == 0                                   # one segment
+    assert check_bstates(L, d, ws=None, wsb=0) == bd.OK
+    # 4096 blocks of 32 tokens over 8 (row, head) units: 512 segments of 8 blocks, each
+    # with a 64 x 32 fp32 state and a log-decay
+    need = ws_bytes_b(L, d, 4096)
+    assert need == 8 * 512 * 64 * 32 * 4 + (8 * 512 * 4 + 255) // 256 * 256
+    d = desc(batch=2, H=4, N=32, L=32)
+    assert check_bstates(L, d, K=4096, ws=WS, wsb=need) == bd.OK
+    assert check_bstates(L, d, K=4096, ws=WS, wsb=need - 4) == bd.E_WORKSPACE
+    assert check_bstates(L, d, K=4096, ws=None, wsb=need) == bd.E_WORKSPACE
     assert check_bstates(L, d, K=0, ws=None, wsb=0) == bd.OK          # empty: nothing to do
     assert L.bdlm_block_boundary_states(None, 4, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
                                         FAKE, None, WS, BIG, None) == bd.E_NULL

@@ -44,8 +44,11 @@ def oracle_states(clean, K, L, s0):
     return np.stack(states), y
 
 
+# K * L above 256 tokens splits the window into segments of whole blocks (with a short
+# last segment where K is not a multiple of the segment's blocks)
 @pytest.mark.parametrize("N,L,K", [(16, 16, 5), (64, 32, 4), (128, 32, 6), (128, 64, 3),
-                                   (32, 24, 3), (128, 32, 1)])
+                                   (32, 24, 3), (128, 32, 1), (64, 32, 21), (32, 24, 25),
+                                   (16, 16, 40), (128, 64, 9)])
 def test_boundary_states_and_clean_outputs(N, L, K):
     import paper_2607_02805_amd as bd
     w, clean, _ = window(2, 3, N, L, K, seed=9800 + N + L + K)
@@ -65,7 +68,7 @@ def test_boundary_states_and_clean_outputs(N, L, K):
 
 
 @pytest.mark.parametrize("N,L,K,bf16", [(64, 32, 4, True), (128, 32, 5, True), (16, 16, 3, False),
-                                        (128, 64, 2, True)])
+                                        (128, 64, 2, True), (64, 32, 20, True), (32, 16, 35, False)])
 def test_all_block_forward(N, L, K, bf16):
     import paper_2607_02805_amd as bd
     w, clean, noised = window(2, 4, N, L, K, bf16=bf16, seed=9900 + N + L + K)
