@@ -19,6 +19,8 @@ C function follows are cited in that file:
 * ``conv``         -- the convolution part of the Mamba boundary state (Sec. 2, Sec. 4;
   App. C: width 4): forward continued from the cached last three input rows, reverse
   zero-padded inside the block, SiLU; a commit keeps the last three rows.
+* ``gated_rmsnorm`` -- the gated RMS normalisation after the scan in the Mamba-2 mixers
+  the paper uses (App. C): y * silu(z), normalised over channel groups, scaled by w.
 
 Inputs are the exact stored bytes the GPU reads: activations as fp32 or bf16
 (numpy ``uint16`` holding the bf16 bit pattern), ``A``/``D``/``D_rev`` fp32.
@@ -266,3 +268,30 @@ def conv(inp: dict, w: np.ndarray, bias: np.ndarray, cache: np.ndarray, slot_idx
         raise ValueError(f"oracle conv failed: {rc}")
     return dict(x=out[0], B=out[1], C=out[2]), dict(x=out[3], B=out[4], C=out[5])
 
+
+
+def gated_rmsnorm(y: np.ndarray, z: np.ndarray, w: np.ndarray, eps: float,
+                  ngroups: int = 1) -> np.ndarray:
+    """Gated RMS normalisation over the channels of each token.
+
+    ``y`` float [..., nch] (any float dtype; taken as float64), ``z`` stored bytes
+    [..., nch] (fp32, or bf16 bits as uint16), ``w`` fp32 [nch]; the channels split into
+    ``ngroups`` groups of consecutive channels.  Returns float64 of ``y``'s shape.
+    """
+    y = np.ascontiguousarray(y, dtype=np.float64)
+    z, zdt = _act(z)
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    nch = y.shape[-1]
+    if z.shape != y.shape or w.shape != (nch,):
+        raise ValueError("y and z share a shape; w is [channels]")
+    ntok = y.size // nch if nch else 0
+    out = np.zeros(y.shape, np.float64)
+    L_ = lib()
+    L_.bdlm_oracle_gated_rmsnorm.restype = ctypes.c_int
+    rc = L_.bdlm_oracle_gated_rmsnorm(ctypes.c_int64(ntok), ctypes.c_int64(nch),
+                                      ctypes.c_int64(ngroups), _p(y, ctypes.c_double), _v(z),
+                                      ctypes.c_int(zdt), _p(w, ctypes.c_float),
+                                      ctypes.c_double(eps), _p(out, ctypes.c_double))
+    if rc != OK:
+        raise ValueError(f"oracle gated_rmsnorm failed: {rc}")
+    return out

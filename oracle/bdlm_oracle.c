@@ -26,6 +26,10 @@
  *     the forward branch and zero-padded inside the block in the reverse branch
  *     (Sec. 2 and Sec. 4: the cached boundary state includes the convolution
  *     state; the reverse scan is local to the active block)
+ *   - the gated RMS normalisation that follows the scan in a Mamba-2 mixer
+ *     (App. C: the paper's Mamba layers are Mamba-2 mixers; the paper gives no
+ *     formula, so the Mamba-2 mixer's output path is taken as written there:
+ *     gate by SiLU(z), then normalise over channel groups, then scale)
  *
  * Every function takes the same stored bytes the GPU reads (fp32 or bf16
  * activations, fp32 per-head A / D / D_rev) and decodes them exactly to
@@ -369,6 +373,38 @@ int bdlm_oracle_conv(const or_shape *s, const void *x, const void *Bm, const voi
         }
     }
     free(u);
+    return OR_OK;
+}
+
+/*
+ * Gated RMS normalisation of the mixer output (Mamba-2 mixer, App. C):
+ *
+ *   g[c]   = y[c] * silu(z[c])
+ *   out[c] = w[c] * g[c] / sqrt(ms(group of c) + eps),
+ *   ms(G)  = (1 / |G|) * sum over c' in G of g[c']^2
+ *
+ * per token, over nch = nheads * headdim channels (head-major) split into ngroups
+ * groups of nch / ngroups consecutive channels.  y double [ntok][nch]; z stored
+ * (zdtype) [ntok][nch]; w fp32 [nch]; out double [ntok][nch].
+ */
+int bdlm_oracle_gated_rmsnorm(int64_t ntok, int64_t nch, int64_t ngroups, const double *y,
+                              const void *z, int zdtype, const float *w, double eps, double *out)
+{
+    if (ntok < 0 || nch <= 0 || ngroups <= 0 || nch % ngroups != 0 || !y || !z || !w || !out)
+        return OR_ERR_ARG;
+    const int64_t gs = nch / ngroups;
+    double *g = malloc((size_t)nch * sizeof(double));
+    if (!g) return OR_ERR_ARG;
+    for (int64_t t = 0; t < ntok; ++t) {
+        for (int64_t c = 0; c < nch; ++c) g[c] = y[t * nch + c] * silu(rd(z, t * nch + c, zdtype));
+        for (int64_t k = 0; k < ngroups; ++k) {
+            double ss = 0.0;
+            for (int64_t c = k * gs; c < (k + 1) * gs; ++c) ss += g[c] * g[c];
+            const double r = 1.0 / sqrt(ss / (double)gs + eps);
+            for (int64_t c = k * gs; c < (k + 1) * gs; ++c) out[t * nch + c] = (double)w[c] * g[c] * r;
+        }
+    }
+    free(g);
     return OR_OK;
 }
 

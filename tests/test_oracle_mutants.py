@@ -130,3 +130,42 @@ def test_conv_mutant_is_caught(tmp_path, name, old, new, monkeypatch):
         except (AssertionError, ValueError):
             caught.append(i)
     assert caught, f"no pin catches mutant {name}"
+
+
+# Mutants of the gated RMS normalisation (oracle.gated_rmsnorm), caught by its pins.
+import tests.test_oracle_norm as npins  # noqa: E402
+
+NORM_MUTANTS = [
+    ("norm-no-gate", "g[c] = y[t * nch + c] * silu(rd(z, t * nch + c, zdtype));",
+     "g[c] = y[t * nch + c];"),
+    ("norm-gate-is-sigmoid", "g[c] = y[t * nch + c] * silu(rd(z, t * nch + c, zdtype));",
+     "g[c] = y[t * nch + c] / (1.0 + exp(-rd(z, t * nch + c, zdtype)));"),
+    ("norm-mean-over-all-channels", "sqrt(ss / (double)gs + eps)", "sqrt(ss / (double)nch + eps)"),
+    ("norm-eps-outside-sqrt", "1.0 / sqrt(ss / (double)gs + eps)", "1.0 / (sqrt(ss / (double)gs) + eps)"),
+    ("norm-eps-on-sum", "sqrt(ss / (double)gs + eps)", "sqrt((ss + eps) / (double)gs)"),
+    ("norm-weight-dropped", "out[t * nch + c] = (double)w[c] * g[c] * r;", "out[t * nch + c] = g[c] * r;"),
+    ("norm-sums-first-group", "for (int64_t c = k * gs; c < (k + 1) * gs; ++c) ss += g[c] * g[c];",
+     "for (int64_t c = 0; c < gs; ++c) ss += g[c] * g[c];"),
+]
+
+NORM_PINS = [
+    lambda: npins.test_hand_example_and_gate_sign(),
+    lambda: npins.test_gate_is_silu_against_scipy_expit(),
+    lambda: npins.test_unit_mean_square_per_group(2),
+    lambda: npins.test_weight_scales_each_channel(),
+    lambda: npins.test_eps_closed_form(),
+    lambda: npins.test_groups_are_independent_and_consecutive(),
+]
+
+
+@pytest.mark.parametrize("name,old,new", NORM_MUTANTS, ids=[m[0] for m in NORM_MUTANTS])
+def test_norm_mutant_is_caught(tmp_path, name, old, new, monkeypatch):
+    mut = _load_mutant(tmp_path, name, old, new)
+    monkeypatch.setattr(oracle, "_lib", mut)
+    caught = []
+    for i, pin in enumerate(NORM_PINS):
+        try:
+            pin()
+        except (AssertionError, ValueError):
+            caught.append(i)
+    assert caught, f"no pin catches mutant {name}"
