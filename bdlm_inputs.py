@@ -12,6 +12,8 @@ use random-initialised models and synthetic batches, Sec. 5.3):
 * ``A_h = -exp(U(0, ln 16))``                   [nheads]   (fp32, always)
 * ``B, C ~ N(0, 1) / sqrt(dstate)``             [batch, len, ngroups, dstate]
 * ``D ~ N(0, 1)``, ``D_rev = D``                [nheads]   (fp32, always)
+* gate ``z ~ N(0, 1)``                          [batch, len, nheads * headdim]
+* normalisation weight ``1 + 0.1 * N(0, 1)``    [nheads * headdim]  (fp32, always)
 
 Everything is drawn in fp32 from numpy's PCG64 and, for bf16 workloads, rounded
 to bf16 with round-to-nearest-even.  Seeds: workload ``c`` uses ``base = 1000*c``;
@@ -159,3 +161,14 @@ def random_state(w: Workload, nslots: int, seed: int, scale: float = 1.0) -> np.
     r = _rng(seed)
     return (r.standard_normal((nslots, w.nheads, w.headdim, w.dstate), dtype=np.float32)
             * np.float32(scale))
+
+
+def gate_inputs(w: Workload, ntok: int, seed: int, batch: int | None = None) -> dict:
+    """The gate ``z`` (workload storage dtype, [batch, ntok, nheads * headdim]) and the
+    normalisation weight ``norm_w`` (fp32 [nheads * headdim]) of the mixer's output path."""
+    bsz = w.batch if batch is None else batch
+    r = _rng(seed)
+    z = r.standard_normal((bsz, ntok, w.nheads * w.headdim), dtype=np.float32)
+    norm_w = (1.0 + 0.1 * r.standard_normal(w.nheads * w.headdim, dtype=np.float32)).astype(
+        np.float32)
+    return {"z": to_bf16_bits(z) if w.bf16 else z, "norm_w": norm_w}

@@ -500,6 +500,29 @@ def run_variants(args) -> dict:
         "step_us": round(t_cs * 1e6, 2), "commit_us": round(t_cc * 1e6, 2), "step_bytes": sb,
         "step_gbs": round(sb / t_cs / 1e9, 1)}
     del pools, convs, y, ws
+    # the gated RMS normalisation of the step's output (the mixer's output path), alone
+    # (y, gate and output over a ring of 48 layers: cold) and after the step, in place
+    nl2 = 48
+    gi = bi.gate_inputs(w, 32, 7500)
+    zt = to_dev({"z": gi["z"]}, dev)["z"]
+    ys = [torch.randn((16, 32, 32, 64), device=dev) for _ in range(nl2)]
+    zs = [zt.clone() for _ in range(nl2)]
+    outs = [torch.empty_like(ys[0]) for _ in range(nl2)]
+    nw = torch.from_numpy(gi["norm_w"]).to(dev)
+    t_norm = _graph_time(lambda li: bd.gated_rmsnorm(ys[li], zs[li], nw, 1e-5, out=outs[li]), nl2)
+    pools = [torch.zeros(bd.pool_shape(16, 32, 128), device=dev) for _ in range(nl)]
+
+    def step_norm(li):
+        bd.scan_block_step(f["x"], f["dt"], f["A"], f["B"], f["C"], f["D"], f["D_rev"], pools[li],
+                           y=ys[li])
+        bd.gated_rmsnorm(ys[li], zs[li], nw, 1e-5, out=ys[li])
+    t_sn = _graph_time(step_norm, nl)
+    nbytes = 16 * 32 * 2048 * (4 + 2 + 4) + 2048 * 4
+    out["gated_norm_L32"] = {
+        "workload": "350m-mamba-layer-b16-L32-gated-rmsnorm", "norm_us": round(t_norm * 1e6, 2),
+        "norm_bytes": nbytes, "norm_gbs": round(nbytes / t_norm / 1e9, 1),
+        "step_plus_norm_us": round(t_sn * 1e6, 2)}
+    del ys, zs, outs, pools
     torch.cuda.empty_cache()
     return out
 

@@ -57,6 +57,8 @@ extern "C" {
 /* Largest batch for which an explicit slot_idx may be given (it is passed to
    the kernels by value). */
 #define BDLM_MAX_SLOT_ROWS 256
+/* Most heads (nheads * 64 channels) bdlm_gated_rmsnorm takes per token. */
+#define BDLM_NORM_MAX_HEADS 256
 
 enum bdlm_status {
     BDLM_OK = 0,
@@ -334,6 +336,36 @@ int bdlm_cache_reset(float *h_pool, int64_t nslots, int64_t state_elems, const i
                      int64_t nreset, int64_t *n_committed, int64_t *n_blocks, void *stream);
 
 /*
+ * Gated RMS normalisation of the scan output, the step after the scan in the
+ * Mamba-2 mixers the paper's Mamba layers use (App. C; the paper states no formula,
+ * the Mamba-2 mixer's output path is taken):
+ *
+ *   g[c]   = y[c] * silu(z[c]),              silu(v) = v / (1 + exp(-v))
+ *   out[c] = norm_w[c] * g[c] / sqrt(mean over c's group of g^2 + eps)
+ *
+ * per token (batch row, position), over the nheads * 64 channels (head-major, the
+ * layout of y from every scan entry point), in ngroups groups of nheads / ngroups
+ * whole heads.
+ *
+ * y        device fp32 [batch][len][nheads * 64], contiguous, 16-byte aligned.
+ * z        device [batch][len][nheads * 64], z_dtype storage (BDLM_DTYPE_F32 or
+ *          BDLM_DTYPE_BF16); element strides z_stride_b, z_stride_t (multiples of
+ *          4, e.g. a slice of an in_proj output), unit channel stride; base aligned
+ *          to 4 elements.
+ * norm_w   device fp32 [nheads * 64], 16-byte aligned.
+ * eps      finite, >= 0.
+ * out      device fp32, y's layout, 16-byte aligned; may be y itself (in place);
+ *          must not overlap z or norm_w, nor partly overlap y.
+ * 1 <= nheads <= BDLM_NORM_MAX_HEADS; nheads % ngroups == 0.  batch == 0 or
+ * len == 0 enqueues nothing (y, z and out may then be NULL).
+ * Errors: BDLM_E_NULL, BDLM_E_SHAPE, BDLM_E_DTYPE, BDLM_E_ALIGN, BDLM_E_LAUNCH.
+ */
+int bdlm_gated_rmsnorm(int64_t batch, int64_t len, int64_t nheads, int64_t ngroups,
+                       int32_t z_dtype, const float *y, const void *z, int64_t z_stride_b,
+                       int64_t z_stride_t, const float *norm_w, float eps, float *out,
+                       void *stream);
+
+/*
  * Host-only argument checks used by the entry points above, exported so they
  * can be exercised without a GPU.  Same arguments (the stream is not needed),
  * same return codes; nothing is enqueued and nothing is modified.
@@ -375,6 +407,10 @@ int bdlm_check_block_boundary_states(const bdlm_desc_t *desc, int64_t n_blocks, 
                                      const void *C, const float *D, const float *s_init,
                                      const float *s_out, const float *y_fwd,
                                      const void *workspace, int64_t workspace_bytes);
+int bdlm_check_gated_rmsnorm(int64_t batch, int64_t len, int64_t nheads, int64_t ngroups,
+                             int32_t z_dtype, const float *y, const void *z, int64_t z_stride_b,
+                             int64_t z_stride_t, const float *norm_w, float eps,
+                             const float *out);
 int bdlm_check_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
                        const void *B, const void *C, const float *D, const float *h_pool,
                        int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,

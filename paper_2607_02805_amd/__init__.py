@@ -118,7 +118,13 @@ def lib() -> ctypes.CDLL:
                                          i64, i64, fp, vp, i64]
         L.bdlm_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p, i64,
                                    i64, fp, vp, i64, vp]
+        f32 = ctypes.c_float
+        L.bdlm_check_gated_rmsnorm.argtypes = [i64, i64, i64, i64, ctypes.c_int32, fp, vp, i64,
+                                               i64, fp, f32, fp]
+        L.bdlm_gated_rmsnorm.argtypes = [i64, i64, i64, i64, ctypes.c_int32, fp, vp, i64, i64, fp,
+                                         f32, fp, vp]
         for name in ("bdlm_desc_init", "bdlm_check_block_step", "bdlm_check_commit",
+                     "bdlm_check_gated_rmsnorm", "bdlm_gated_rmsnorm",
                      "bdlm_scan_block_step", "bdlm_commit_boundary", "bdlm_cache_reset",
                      "bdlm_state_pack", "bdlm_state_unpack", "bdlm_check_full_window",
                      "bdlm_scan_full_window", "bdlm_check_prefill", "bdlm_prefill",
@@ -550,6 +556,50 @@ def all_block_forward(clean, noised, A, D, D_rev, block_len, s_init=None, want_c
                         stream=stream)
     y = y.reshape(bsz, T, *y.shape[2:])
     return (y, s_out, out[1]) if want_clean_y else (y, s_out)
+
+
+def gated_rmsnorm(y, z, norm_w, eps=1e-5, ngroups=1, out=None, stream=None):
+    """Gated RMS normalisation of a scan output (the Mamba-2 mixer's output path):
+    ``out = norm_w * g / sqrt(mean_group(g^2) + eps)``, ``g = y * silu(z)``, per token over
+    the ``nheads * 64`` channels in ``ngroups`` groups of whole heads.
+
+    ``y`` float32 [B, L, H, 64] (or [B, L, H * 64]), contiguous; ``z`` bfloat16 or float32
+    [B, L, H * 64] with unit channel stride (a slice of a projection output is fine);
+    ``norm_w`` float32 [H * 64].  ``out`` may be ``y`` (in place).  Returns ``out``.
+    """
+    torch = _torch()
+    if y.dtype != torch.float32 or not y.is_contiguous() or y.dim() not in (3, 4):
+        raise ValueError("y must be a contiguous float32 [B, L, H, 64] or [B, L, H*64] tensor")
+    bsz, L = y.shape[0], y.shape[1]
+    nch = y.shape[2] * y.shape[3] if y.dim() == 4 else y.shape[2]
+    if nch % HEADDIM:
+        raise ValueError("channels must be whole heads of 64")
+    H = nch // HEADDIM
+    if z.dim() != 3 or tuple(z.shape) != (bsz, L, nch):
+        raise ValueError(f"z must be [B, L, {nch}]")
+    if z.dtype == torch.bfloat16:
+        zdt = DTYPE_BF16
+    elif z.dtype == torch.float32:
+        zdt = DTYPE_F32
+    else:
+        raise ValueError(f"z must be bfloat16 or float32, got {z.dtype}")
+    if bsz * L and z.stride(2) != 1:
+        raise ValueError("z must have unit channel stride")
+    if norm_w.dtype != torch.float32 or tuple(norm_w.shape) != (nch,) or not norm_w.is_contiguous():
+        raise ValueError(f"norm_w must be a contiguous float32 [{nch}] tensor")
+    if out is None:
+        out = torch.empty_like(y)
+    elif out.dtype != torch.float32 or tuple(out.shape) != tuple(y.shape) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor shaped like y")
+    empty = bsz * L == 0
+    rc = lib().bdlm_gated_rmsnorm(
+        bsz, L, H, int(ngroups), zdt, None if empty else _dev_ptr(y, "y"),
+        None if empty else _dev_ptr(z, "z"), z.stride(0) if not empty else 0,
+        z.stride(1) if not empty else 0, _dev_ptr(norm_w, "norm_w"), float(eps),
+        None if empty else _dev_ptr(out, "out"), _stream_handle(stream))
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_gated_rmsnorm")
+    return out
 
 
 def cache_reset(h_pool, slots=None, n_committed=None, n_blocks=None, stream=None):

@@ -39,7 +39,7 @@ def _run(cmd: list[str]) -> None:
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = []
-    for src in ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip"):
+    for src in ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip", "bdlm_norm.hip"):
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),
               "-o", obj])

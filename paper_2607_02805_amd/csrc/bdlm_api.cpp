@@ -542,4 +542,66 @@ int bdlm_cache_reset(float *h_pool, int64_t nslots, int64_t state_elems, const i
     return BDLM_OK;
 }
 
+namespace {
+bool disjoint(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
+    const char *p = static_cast<const char *>(a), *q = static_cast<const char *>(b);
+    return abytes <= 0 || bbytes <= 0 || p + abytes <= q || q + bbytes <= p;
+}
+}  // namespace
+
+int bdlm_check_gated_rmsnorm(int64_t batch, int64_t len, int64_t nheads, int64_t ngroups,
+                             int32_t z_dtype, const float *y, const void *z, int64_t z_stride_b,
+                             int64_t z_stride_t, const float *norm_w, float eps,
+                             const float *out) {
+    if (z_dtype != BDLM_DTYPE_F32 && z_dtype != BDLM_DTYPE_BF16) return BDLM_E_DTYPE;
+    if (batch < 0 || len < 0 || nheads <= 0 || nheads > BDLM_NORM_MAX_HEADS || ngroups <= 0 ||
+        nheads % ngroups != 0)
+        return BDLM_E_SHAPE;
+    if (z_stride_b < 0 || z_stride_t < 0) return BDLM_E_SHAPE;
+    if (!(eps >= 0.f && eps <= 3.0e38f)) return BDLM_E_SHAPE;   // finite, not negative, not NaN
+    constexpr int64_t kMax = int64_t(1) << 31;
+    if (batch > kMax || len > kMax || (len > 0 && batch > (int64_t(1) << 40) / len))
+        return BDLM_E_SHAPE;
+    if (!norm_w) return BDLM_E_NULL;
+    const bool empty = batch == 0 || len == 0;
+    if (!empty && (!y || !z || !out)) return BDLM_E_NULL;
+    const int64_t es = elem_size(z_dtype);
+    if (!aligned(y, 16) || !aligned(out, 16) || !aligned(norm_w, 16) || !aligned(z, 4 * es))
+        return BDLM_E_ALIGN;
+    if (z_stride_b % 4 != 0 || z_stride_t % 4 != 0) return BDLM_E_ALIGN;
+    if (empty) return BDLM_OK;
+    const int64_t ch = nheads * BDLM_HEADDIM;
+    if (z_stride_b > (int64_t(1) << 40) || z_stride_t > (int64_t(1) << 40)) return BDLM_E_SHAPE;
+    const int64_t ybytes = batch * len * ch * 4;
+    const int64_t zbytes = ((batch - 1) * z_stride_b + (len - 1) * z_stride_t + ch) * es;
+    // out may be y itself (in place); no other overlap with an input
+    if (out != y && !disjoint(out, ybytes, y, ybytes)) return BDLM_E_SHAPE;
+    if (!disjoint(out, ybytes, z, zbytes) || !disjoint(out, ybytes, norm_w, ch * 4))
+        return BDLM_E_SHAPE;
+    return BDLM_OK;
+}
+
+int bdlm_gated_rmsnorm(int64_t batch, int64_t len, int64_t nheads, int64_t ngroups,
+                       int32_t z_dtype, const float *y, const void *z, int64_t z_stride_b,
+                       int64_t z_stride_t, const float *norm_w, float eps, float *out,
+                       void *stream) {
+    const int rc = bdlm_check_gated_rmsnorm(batch, len, nheads, ngroups, z_dtype, y, z,
+                                            z_stride_b, z_stride_t, norm_w, eps, out);
+    if (rc != BDLM_OK) return rc;
+    bdlm::NormLaunch n;
+    n.y = y;
+    n.z = z;
+    n.w = norm_w;
+    n.out = out;
+    n.zs_b = z_stride_b;
+    n.zs_t = z_stride_t;
+    n.batch = batch;
+    n.len = len;
+    n.nheads = nheads;
+    n.ngroups = ngroups;
+    n.bf16 = z_dtype == BDLM_DTYPE_BF16 ? 1 : 0;
+    n.eps = eps;
+    return bdlm::launch_gated_rmsnorm(n, stream);
+}
+
 }  // extern "C"

@@ -120,6 +120,21 @@ inline int64_t conv_workspace(int64_t batch, int64_t L, int64_t nheads, int64_t 
 }
 
 // Permute nstates states between row-major [64][dstate] and the pool layout.
+// Gated RMS normalisation of a mixer output: out = w * g / sqrt(mean_group(g^2) + eps),
+// g = y * silu(z), per token over nheads * 64 channels in ngroups groups of whole heads.
+// y, out fp32 [batch][len][nheads * 64] contiguous (out may be y); z [batch][len][channels]
+// with strides zs_b, zs_t (elements), unit channel stride; nheads <= 256.
+struct NormLaunch {
+    const float *y;
+    const void *z;
+    const float *w;
+    float *out;
+    int64_t zs_b, zs_t, batch, len, nheads, ngroups;
+    int32_t bf16;
+    float eps;
+};
+int launch_gated_rmsnorm(const NormLaunch &n, void *stream);
+
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream);
 

@@ -432,3 +432,43 @@ def test_conv_entry_point_checks(L):
                                   p["Drev"], cw, cb, cp, p["h"], 4, i32p(np.array([1, 1], np.int32)),
                                   i64p(nc), i64p(nb), -1, None, WS, BIG)
     assert rc == bd.E_SLOT
+
+
+def check_norm(L, batch=2, ln=8, H=4, G=1, zdt=bd.DTYPE_BF16, y=FAKE, z=FAKE + 0x100000,
+               zsb=None, zst=None, w=FAKE + 0x200000, eps=1e-5, out=FAKE + 0x300000):
+    zst = H * 64 if zst is None else zst
+    zsb = ln * zst if zsb is None else zsb
+    return L.bdlm_check_gated_rmsnorm(batch, ln, H, G, zdt, y, z, zsb, zst, w, eps, out)
+
+
+def test_gated_rmsnorm_checks(L):
+    assert check_norm(L) == bd.OK
+    assert check_norm(L, zdt=bd.DTYPE_F32) == bd.OK
+    assert check_norm(L, out=FAKE) == bd.OK                          # in place
+    assert check_norm(L, H=6, G=3) == bd.OK
+    assert check_norm(L, H=256) == bd.OK
+    assert check_norm(L, H=257) == bd.E_SHAPE                        # too many channels
+    assert check_norm(L, H=0) == bd.E_SHAPE
+    assert check_norm(L, H=6, G=4) == bd.E_SHAPE                     # groups of whole heads
+    assert check_norm(L, zdt=7) == bd.E_DTYPE
+    assert check_norm(L, eps=-1.0) == bd.E_SHAPE
+    assert check_norm(L, eps=float("nan")) == bd.E_SHAPE
+    assert check_norm(L, eps=float("inf")) == bd.E_SHAPE
+    assert check_norm(L, batch=-1) == bd.E_SHAPE
+    assert check_norm(L, zst=-256) == bd.E_SHAPE
+    assert check_norm(L, y=None) == bd.E_NULL
+    assert check_norm(L, z=None) == bd.E_NULL
+    assert check_norm(L, w=None) == bd.E_NULL
+    assert check_norm(L, out=None) == bd.E_NULL
+    assert check_norm(L, batch=0, y=None, z=None, out=None) == bd.OK  # empty: nothing read
+    assert check_norm(L, y=FAKE + 8) == bd.E_ALIGN
+    assert check_norm(L, out=FAKE + 0x300008) == bd.E_ALIGN
+    assert check_norm(L, w=FAKE + 0x200004) == bd.E_ALIGN
+    assert check_norm(L, z=FAKE + 0x100008) == bd.OK                 # bf16: 8-byte quads
+    assert check_norm(L, zdt=bd.DTYPE_F32, z=FAKE + 0x100008) == bd.E_ALIGN
+    assert check_norm(L, zst=258) == bd.E_ALIGN                      # strides in quads
+    # y spans 2 * 8 * 256 * 4 = 16 KiB: out partly over y, or over z / w
+    assert check_norm(L, out=FAKE + 0x1000) == bd.E_SHAPE
+    assert check_norm(L, out=FAKE + 0x100000 - 0x1000) == bd.E_SHAPE
+    assert check_norm(L, out=FAKE + 0x200000) == bd.E_SHAPE
+    assert check_norm(L, out=FAKE + 0x100000 - 0x4000) == bd.OK      # ends where z starts
