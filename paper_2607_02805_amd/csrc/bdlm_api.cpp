@@ -361,7 +361,8 @@ int bdlm_scan_block_step_sep(const bdlm_desc_t *d, const void *x, const void *dt
         make_args(d, x, dt, A, B, C, D, D, const_cast<float *>(h_pool), slot_idx, y);
     const bdlm::LaunchArgs r =
         make_args(d, x_rev, dt_rev, A_rev, B_rev, C_rev, D_rev, D_rev, nullptr, slot_idx, y);
-    return bdlm::launch_block_long(f, r, false, true, stream);
+    return d->block_len <= BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_pair(f, r, false, true, stream)
+                                              : bdlm::launch_block_long(f, r, false, true, stream);
 }
 
 int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,

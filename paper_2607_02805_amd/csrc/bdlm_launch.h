@@ -25,6 +25,13 @@ struct LaunchArgs {
 // Arguments are already validated.  Returns BDLM_OK or BDLM_E_LAUNCH.
 int launch_block(const LaunchArgs &a, bool commit, void *stream);
 
+// A step (or commit) of a block of at most 64 tokens whose reverse branch has inputs of
+// its own: the forward branch of `fwd` from the cached state (skip fwd.D) stores y,
+// then the reverse branch of `rev` (skip rev.D_rev) adds onto it; a commit updates the
+// state from `fwd`.  want_y false (commit only): no outputs, no reverse launch.
+int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
+                      void *stream);
+
 // How the sequence kernels cut T tokens into segments (one workgroup per batch row,
 // head and segment) and the device workspace they need: per (row, head, segment)
 // `dirs` states of 64 x dstate fp32, then one fp32 log-decay, rounded up to 256

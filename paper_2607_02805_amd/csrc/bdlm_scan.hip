@@ -74,6 +74,11 @@ struct KArgs {
 // LT: block tile (16, 32 or 64 tokens; the block length L <= LT, padded tokens
 //     have dt = 0, x = B = C = 0, which changes no output and no state).
 // NS: dstate.  F32: fp32 activation storage.  COMMIT: also update the state.
+// DIR: kBoth computes both branches (one input set for both, Eq. partial-reverse);
+//     kFwd only the forward branch from the cached state (skip D) and stores y;
+//     kRev only the block-local reverse branch (skip D_rev) and adds it onto y.  A
+//     step whose branches have inputs of their own is a kFwd launch followed by a
+//     kRev launch on the same stream.
 // NPART: the state of a head is split over NPART groups of four waves along
 //     dstate (4 * NPART waves per workgroup).  Streaming the state from HBM needs
 //     many waves per CU, each with few loads in flight; the partial prefix
@@ -96,9 +101,13 @@ struct KArgs {
 //      dstate quads of the state (the only step that waits for the state loads);
 //      the partial products are summed and y is stored; a commit then adds the
 //      block to each wave's quads of the state in place.
-template <int LT, int NS, bool F32, bool COMMIT, int NPART>
+constexpr int kBoth = 0, kFwd = 1, kRev = 2;
+
+template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR>
 __global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
+    static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev, "direction");
+    static_assert(!(COMMIT && DIR == kRev), "a commit updates the forward state");
     constexpr int NT = 256 * NPART;       // threads
     constexpr int NW = 4 * NPART;         // waves
     constexpr int MT = LT / 16;           // token tiles = quads along the block
@@ -191,9 +200,10 @@ bdlm_block_kernel(const KArgs args) {
     __builtin_amdgcn_sched_barrier(0);
     f32x4 hq[QW];  // state s[p, 16(q0 + k) + 4grp + r]
 #pragma unroll
-    for (int k = 0; k < QW; ++k)  // read once per step: stream past the caches
-        hq[k] = __builtin_nontemporal_load(
-            reinterpret_cast<const f32x4 *>(hs + (q0 + k) * 16 * kP));
+    for (int k = 0; k < QW; ++k) {  // read once per step: stream past the caches
+        if constexpr (DIR == kRev) hq[k] = f32x4{0.f, 0.f, 0.f, 0.f};   // the state is not used
+        else hq[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(hs + (q0 + k) * 16 * kP));
+    }
 
     // ---- phase 1: LDS images
 #pragma unroll
@@ -283,9 +293,9 @@ bdlm_block_kernel(const KArgs args) {
             const int j = 16 * jt + 4 * grp + r;
             const float csj = shfl(cs, j), exj = shfl(ex, j), dtj = shfl(dtv, j);
             float w;
-            if (j < t) w = exp2f(cst - csj);
-            else if (j == t) w = 2.f;
-            else w = exp2f(exj - ext);
+            if (j < t) w = DIR == kRev ? 0.f : exp2f(cst - csj);
+            else if (j == t) w = DIR == kBoth ? 2.f : 1.f;
+            else w = DIR == kFwd ? 0.f : exp2f(exj - ext);
             m[r] = gacc[r] * w * dtj;
         }
         s16x4 mh, ml;
@@ -313,7 +323,8 @@ bdlm_block_kernel(const KArgs args) {
         // waiting for the state
         float pre[MT][4], es[MT][4];
         if (part == 0) {
-            const float skip = sPar[1] + sPar[2];
+            const float skip =
+                DIR == kBoth ? sPar[1] + sPar[2] : (DIR == kFwd ? sPar[1] : sPar[2]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 s16x4 mh[MT], ml[MT];
@@ -353,7 +364,7 @@ bdlm_block_kernel(const KArgs args) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int k = 0; k < QW; k += 2) {
+        for (int k = 0; k < (DIR == kRev ? 0 : QW); k += 2) {
             if (k + 1 < QW) {
                 s16x4 h0, l0, h1, l1;
                 split4(hq[k], h0, l0);
@@ -375,7 +386,7 @@ bdlm_block_kernel(const KArgs args) {
                 }
             }
         }
-        if constexpr (NPART > 1) {
+        if constexpr (NPART > 1 && DIR != kRev) {
             if (part > 0)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
@@ -392,7 +403,17 @@ bdlm_block_kernel(const KArgs args) {
             // y straight from the accumulators: lanes of a group write 64 contiguous bytes
             float *yrow = yb + ((static_cast<int64_t>(b) * L + 4 * grp) * args.nheads + h) * kP + p;
             const int ytok = args.nheads * kP;           // elements between consecutive tokens
-            if (L == LT) {
+            if constexpr (DIR == kRev) {
+                // add onto the forward launch's outputs (one writer per element)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (16 * mt + 4 * grp + r < L) {
+                            float *at = yrow + (16 * mt + r) * ytok;
+                            __builtin_nontemporal_store(*at + pre[mt][r], at);
+                        }
+            } else if (L == LT) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -500,36 +521,33 @@ constexpr int nparts() {
     return (NS / 16) % 2 == 0 ? 2 : 1;
 }
 
-template <int LT, int NS, bool F32, bool COMMIT>
+template <int LT, int NS, bool F32, bool COMMIT, int DIR>
 hipError_t launch_t(const KArgs &k, unsigned grid, hipStream_t s) {
     constexpr int NP = nparts<LT, NS>();
-    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT, NP>), dim3(grid), dim3(256 * NP), 0,
-                       s, k);
+    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT, NP, DIR>), dim3(grid),
+                       dim3(256 * NP), 0, s, k);
     return hipGetLastError();
 }
 
-template <int LT, bool F32, bool COMMIT>
+template <int LT, bool F32, bool COMMIT, int DIR>
 hipError_t by_ns(int ns, const KArgs &k, unsigned grid, hipStream_t s) {
     switch (ns) {
-        case 16: return launch_t<LT, 16, F32, COMMIT>(k, grid, s);
-        case 32: return launch_t<LT, 32, F32, COMMIT>(k, grid, s);
-        case 64: return launch_t<LT, 64, F32, COMMIT>(k, grid, s);
-        case 128: return launch_t<LT, 128, F32, COMMIT>(k, grid, s);
+        case 16: return launch_t<LT, 16, F32, COMMIT, DIR>(k, grid, s);
+        case 32: return launch_t<LT, 32, F32, COMMIT, DIR>(k, grid, s);
+        case 64: return launch_t<LT, 64, F32, COMMIT, DIR>(k, grid, s);
+        case 128: return launch_t<LT, 128, F32, COMMIT, DIR>(k, grid, s);
         default: return hipErrorInvalidValue;
     }
 }
 
-template <bool F32, bool COMMIT>
+template <bool F32, bool COMMIT, int DIR>
 hipError_t by_lt(int L, int ns, const KArgs &k, unsigned grid, hipStream_t s) {
-    if (L <= 16) return by_ns<16, F32, COMMIT>(ns, k, grid, s);
-    if (L <= 32) return by_ns<32, F32, COMMIT>(ns, k, grid, s);
-    return by_ns<64, F32, COMMIT>(ns, k, grid, s);
+    if (L <= 16) return by_ns<16, F32, COMMIT, DIR>(ns, k, grid, s);
+    if (L <= 32) return by_ns<32, F32, COMMIT, DIR>(ns, k, grid, s);
+    return by_ns<64, F32, COMMIT, DIR>(ns, k, grid, s);
 }
 
-}  // namespace
-
-int launch_block(const LaunchArgs &a, bool commit, void *stream) {
-    if (a.batch == 0 || a.L == 0) return BDLM_OK;
+KArgs kargs(const LaunchArgs &a) {
     KArgs k;
     k.x = a.x;
     k.dt = a.dt;
@@ -555,16 +573,50 @@ int launch_block(const LaunchArgs &a, bool commit, void *stream) {
     k.xcd_remap = (units % 8 == 0) ? 1 : 0;
     k.use_slots = a.slots ? 1 : 0;
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i) k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
-    const unsigned grid = static_cast<unsigned>(units);
+    return k;
+}
+
+int launch_dir(const LaunchArgs &a, int dir, bool commit, void *stream) {
+    const KArgs kn = kargs(a);
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads);
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
-    if (a.bf16)
-        e = commit ? by_lt<false, true>(a.L, a.dstate, k, grid, s)
-                   : by_lt<false, false>(a.L, a.dstate, k, grid, s);
-    else
-        e = commit ? by_lt<true, true>(a.L, a.dstate, k, grid, s)
-                   : by_lt<true, false>(a.L, a.dstate, k, grid, s);
+    switch (dir) {
+        case kBoth:
+            e = a.bf16 ? (commit ? by_lt<false, true, kBoth>(a.L, a.dstate, kn, grid, s)
+                                 : by_lt<false, false, kBoth>(a.L, a.dstate, kn, grid, s))
+                       : (commit ? by_lt<true, true, kBoth>(a.L, a.dstate, kn, grid, s)
+                                 : by_lt<true, false, kBoth>(a.L, a.dstate, kn, grid, s));
+            break;
+        case kFwd:
+            e = a.bf16 ? (commit ? by_lt<false, true, kFwd>(a.L, a.dstate, kn, grid, s)
+                                 : by_lt<false, false, kFwd>(a.L, a.dstate, kn, grid, s))
+                       : (commit ? by_lt<true, true, kFwd>(a.L, a.dstate, kn, grid, s)
+                                 : by_lt<true, false, kFwd>(a.L, a.dstate, kn, grid, s));
+            break;
+        default:
+            e = commit ? hipErrorInvalidValue
+                       : (a.bf16 ? by_lt<false, false, kRev>(a.L, a.dstate, kn, grid, s)
+                                 : by_lt<true, false, kRev>(a.L, a.dstate, kn, grid, s));
+    }
     return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+}
+
+}  // namespace
+
+int launch_block(const LaunchArgs &a, bool commit, void *stream) {
+    if (a.batch == 0 || a.L == 0) return BDLM_OK;
+    return launch_dir(a, kBoth, commit, stream);
+}
+
+int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
+                      void *stream) {
+    if (fwd.batch == 0 || fwd.L == 0) return BDLM_OK;
+    LaunchArgs f = fwd;
+    if (!want_y) f.y = nullptr;
+    int rc = launch_dir(f, kFwd, commit, stream);
+    if (rc != BDLM_OK || !want_y) return rc;
+    return launch_dir(rev, kRev, false, stream);
 }
 
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
