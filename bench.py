@@ -632,6 +632,26 @@ def summarize_trace(stats_csv: str) -> str:
     return "\n".join(out)
 
 
+def summarize_dispatches(trace_csv: str) -> str:
+    """Markdown table of a rocprofv3 --kernel-trace kernel_trace.csv grouped by kernel and
+    launch shape (grid threads, workgroup size): separates the workloads that launch one
+    kernel template at different shapes."""
+    import statistics as st
+    groups = {}
+    for r in _csv_rows(trace_csv):
+        name = r["Kernel_Name"].replace("bdlm::(anonymous namespace)::", "").split("(")[0]
+        if "bdlm" not in name:
+            continue
+        key = (name, int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))
+        groups.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    out = ["| kernel | workgroups x threads | calls | median us | mean us | min us |",
+           "|---|---|---|---|---|---|"]
+    for (name, grid, wg), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{name[:70]}` | {grid // wg} x {wg} | {len(d)} | {st.median(d):.2f} | "
+                   f"{st.fmean(d):.2f} | {min(d):.2f} |")
+    return "\n".join(out)
+
+
 def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
                       copy_bytes=256 << 20, kernels=None) -> dict:
     """Per-launch HBM bytes of kernels (default: the block step and the commit; else a
@@ -701,6 +721,8 @@ def main():
                     help="only run a 256 MiB device copy (counter calibration) and exit")
     ap.add_argument("--summarize-trace", metavar="KERNEL_STATS_CSV",
                     help="print a markdown summary of a rocprofv3 kernel_stats.csv and exit")
+    ap.add_argument("--summarize-dispatches", metavar="KERNEL_TRACE_CSV",
+                    help="print per-shape kernel durations from a rocprofv3 kernel_trace.csv")
     ap.add_argument("--summarize-traffic", nargs=4,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
@@ -712,6 +734,9 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_dispatches:
+        print(summarize_dispatches(args.summarize_dispatches))
         return
     if args.summarize_traffic:
         kern = None
