@@ -210,9 +210,9 @@ int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, fl
     r.x = base + BL * (HP + 2 * GN);
     r.Bm = base + BL * (2 * HP + 2 * GN);
     r.Cm = base + BL * (2 * HP + 3 * GN);
-    // the sequence kernels' fp32 path contracts on fp32 MFMA: the convolved operands are
-    // all fp32 and not zero-mean, and two-term bf16 splits lose too much to cancellation
-    return launch_block_long(f, r, commit, a.y != nullptr, stream);
+    // fp32 operands: both kernels contract them on fp32 MFMA
+    return a.L <= BDLM_MAX_BLOCK_LEN ? launch_block_pair(f, r, commit, a.y != nullptr, stream)
+                                     : launch_block_long(f, r, commit, a.y != nullptr, stream);
 }
 
 }  // namespace bdlm

@@ -24,12 +24,13 @@
 //   s_new  = exp(cs_{L-1}) s + sum_j exp(cs_{L-1} - cs_j) dt_j x[j,:] (outer) B_j
 //
 // Work decomposition: one workgroup of four 64-wide waves per (b, h); wave w
-// owns head-dim columns [16w, 16w+16).  All contractions run on bf16 MFMA
-// (v_mfma_f32_16x16x32_bf16 / 16x16x16) with fp32 accumulation.  Operands that
-// are not exact in bf16 (the fp32 state, the fp32 decay-weighted matrices, and
-// fp32 activations) are split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi),
-// which leaves a relative residual below 2^-16; products of bf16 values are
-// exact in fp32.
+// owns head-dim columns [16w, 16w+16).  With bf16 activations all contractions run
+// on bf16 MFMA (v_mfma_f32_16x16x32_bf16 / 16x16x16) with fp32 accumulation; the
+// operands that are not exact in bf16 (the fp32 state and the fp32 decay-weighted
+// matrices) are split as v = hi + lo with hi = bf16(v), lo = bf16(v - hi), which
+// leaves a relative residual below 2^-16, and products of bf16 values are exact in
+// fp32.  With fp32 activations every operand is fp32 and the contractions run on
+// fp32 MFMA (v_mfma_f32_16x16x4_f32).
 //
 // Register layouts.  Every 16x16 MFMA tile uses lane = 16 * grp + col.  An
 // operand "quad" is the four values a lane contributes to 16 consecutive
@@ -103,6 +104,14 @@ struct KArgs {
 //      block to each wave's quads of the state in place.
 constexpr int kBoth = 0, kFwd = 1, kRev = 2;
 
+// c += a b over one quad of 16 contraction indices on fp32 MFMA: instruction r takes
+// value r of every lane, i.e. index 4 grp + r of the quad layout.
+__device__ __forceinline__ f32x4 mma_q32(f32x4 a, f32x4 b, f32x4 c) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r], b[r], c, 0, 0, 0);
+    return c;
+}
+
 template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR>
 __global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
@@ -119,8 +128,11 @@ bdlm_block_kernel(const KArgs args) {
     constexpr int XS = kP + 4;            // x row stride in LDS (elements)
     using AT = typename Act<F32>::T;
 
-    __shared__ __align__(16) uint2 sC[IMG], sB[IMG];                  // bf16 quads (hi)
-    __shared__ __align__(16) uint2 sCl[F32 ? IMG : 1], sBl[F32 ? IMG : 1];  // lo, fp32 input
+    // operand images of C and B: bf16 quads, or fp32 quads for fp32 storage (fp32
+    // activations are contracted on fp32 MFMA: all-fp32 operands lose too much to
+    // cancellation under two-term bf16 splits)
+    __shared__ __align__(16) uint2 sC[F32 ? 1 : IMG], sB[F32 ? 1 : IMG];
+    __shared__ __align__(16) f32x4 sCf[F32 ? IMG : 1], sBf[F32 ? IMG : 1];
     __shared__ __align__(16) AT sX[LT * XS];
     __shared__ __align__(16) float sDt[64];
     __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
@@ -215,13 +227,8 @@ bdlm_block_kernel(const KArgs args) {
         if constexpr (F32) {
             // 4 floats = one quad: q = c / 4, grp = c % 4
             const int at = img_idx<QN, F32>(t >> 4, c >> 2, c & 3, t & 15);
-            s16x4 hi, lo;
-            split4(__builtin_bit_cast(f32x4, cz), hi, lo);
-            sC[at] = as_u2(hi);
-            sCl[at] = as_u2(lo);
-            split4(__builtin_bit_cast(f32x4, bz), hi, lo);
-            sB[at] = as_u2(hi);
-            sBl[at] = as_u2(lo);
+            sCf[at] = __builtin_bit_cast(f32x4, cz);
+            sBf[at] = __builtin_bit_cast(f32x4, bz);
         } else {
             // 8 bf16 = two quads: q = c / 2, grp = 2 (c % 2) and 2 (c % 2) + 1
             const int at = img_idx<QN, F32>(t >> 4, c >> 1, 2 * (c & 1), t & 15);
@@ -262,27 +269,21 @@ bdlm_block_kernel(const KArgs args) {
         const int mt = tile / MT, jt = tile % MT;
         // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
         f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (F32) {
 #pragma unroll
-        for (int q = 0; q < QN; q += 2) {   // two dstate quads per product
-            const int q1 = q + 1 < QN ? q + 1 : q;
-            const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
-            const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
-            const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-            const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
-            if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
-            else gacc = mma_k16(b0, c0, gacc);
-            if constexpr (F32) {
-                const s16x4 bl0 = as_s16x4(sBl[img_idx<QN, F32>(jt, q, grp, col)]);
-                const s16x4 bl1 = as_s16x4(sBl[img_idx<QN, F32>(jt, q1, grp, col)]);
-                const s16x4 cl0 = as_s16x4(sCl[img_idx<QN, F32>(mt, q, grp, col)]);
-                const s16x4 cl1 = as_s16x4(sCl[img_idx<QN, F32>(mt, q1, grp, col)]);
-                if (q + 1 < QN) {
-                    gacc = mma_k32(b0, b1, cl0, cl1, gacc);
-                    gacc = mma_k32(bl0, bl1, c0, c1, gacc);
-                } else {
-                    gacc = mma_k16(b0, cl0, gacc);
-                    gacc = mma_k16(bl0, c0, gacc);
-                }
+            for (int q = 0; q < QN; ++q)
+                gacc = mma_q32(sBf[img_idx<QN, F32>(jt, q, grp, col)],
+                               sCf[img_idx<QN, F32>(mt, q, grp, col)], gacc);
+        } else {
+#pragma unroll
+            for (int q = 0; q < QN; q += 2) {   // two dstate quads per product
+                const int q1 = q + 1 < QN ? q + 1 : q;
+                const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
+                const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
+                const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
+                const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
+                if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
+                else gacc = mma_k16(b0, c0, gacc);
             }
         }
         const int t = 16 * mt + col;
@@ -298,23 +299,31 @@ bdlm_block_kernel(const KArgs args) {
             else w = DIR == kFwd ? 0.f : exp2f(exj - ext);
             m[r] = gacc[r] * w * dtj;
         }
-        s16x4 mh, ml;
-        split4(m, mh, ml);
-        const uint2 a = as_u2(mh), c2 = as_u2(ml);
-        sM[tile * 64 + lane] = uint4{a.x, a.y, c2.x, c2.y};
+        if constexpr (F32) {
+            sM[tile * 64 + lane] = __builtin_bit_cast(uint4, m);
+        } else {
+            s16x4 mh, ml;
+            split4(m, mh, ml);
+            const uint2 a = as_u2(mh), c2 = as_u2(ml);
+            sM[tile * 64 + lane] = uint4{a.x, a.y, c2.x, c2.y};
+        }
     }
     __syncthreads();
 
     // ---- phase 3: x quads (B operand, j = 16jt + 4grp + r), products, output
     float xv[MT][4];
-    s16x4 xq[MT], xl[MT];
+    s16x4 xq[MT];   // bf16 storage: the x quads are exact in bf16
 #pragma unroll
     for (int jt = 0; jt < MT; ++jt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
             xv[jt][r] = Act<F32>::val(sX[(16 * jt + 4 * grp + r) * XS + p]);
-        split4(f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}, xq[jt], xl[jt]);
+        if constexpr (!F32) {
+            s16x4 lo;
+            split4(f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}, xq[jt], lo);
+        }
     }
+    auto xquad = [&](int jt) { return f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}; };
 
     float *yb = args.y;
     const bool want_y = !COMMIT || yb != nullptr;
@@ -327,17 +336,23 @@ bdlm_block_kernel(const KArgs args) {
                 DIR == kBoth ? sPar[1] + sPar[2] : (DIR == kFwd ? sPar[1] : sPar[2]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                s16x4 mh[MT], ml[MT];
-#pragma unroll
-                for (int jt = 0; jt < MT; ++jt) {
-                    const uint4 v = sM[(mt * MT + jt) * 64 + lane];
-                    mh[jt] = as_s16x4(uint2{v.x, v.y});
-                    ml[jt] = as_s16x4(uint2{v.z, v.w});
-                }
                 f32x4 ai = {0.f, 0.f, 0.f, 0.f};
-                ai = mma_quads<MT>(mh, xq, ai);
-                ai = mma_quads<MT>(ml, xq, ai);
-                if constexpr (F32) ai = mma_quads<MT>(mh, xl, ai);
+                if constexpr (F32) {
+#pragma unroll
+                    for (int jt = 0; jt < MT; ++jt)
+                        ai = mma_q32(__builtin_bit_cast(f32x4, sM[(mt * MT + jt) * 64 + lane]),
+                                     xquad(jt), ai);
+                } else {
+                    s16x4 mh[MT], ml[MT];
+#pragma unroll
+                    for (int jt = 0; jt < MT; ++jt) {
+                        const uint4 v = sM[(mt * MT + jt) * 64 + lane];
+                        mh[jt] = as_s16x4(uint2{v.x, v.y});
+                        ml[jt] = as_s16x4(uint2{v.z, v.w});
+                    }
+                    ai = mma_quads<MT>(mh, xq, ai);
+                    ai = mma_quads<MT>(ml, xq, ai);
+                }
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     pre[mt][r] = ai[r] + skip * xv[mt][r];
@@ -348,13 +363,14 @@ bdlm_block_kernel(const KArgs args) {
             }
         }
         // C quads of this wave's dstate share, before the state wait
-        s16x4 cq[MT][QW], cl[MT][F32 ? QW : 1];
+        s16x4 cq[MT][F32 ? 1 : QW];
+        f32x4 cf[MT][F32 ? QW : 1];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int k = 0; k < QW; ++k) {
-                cq[mt][k] = as_s16x4(sC[img_idx<QN, F32>(mt, q0 + k, grp, col)]);
-                if constexpr (F32) cl[mt][k] = as_s16x4(sCl[img_idx<QN, F32>(mt, q0 + k, grp, col)]);
+                if constexpr (F32) cf[mt][k] = sCf[img_idx<QN, F32>(mt, q0 + k, grp, col)];
+                else cq[mt][k] = as_s16x4(sC[img_idx<QN, F32>(mt, q0 + k, grp, col)]);
             }
         __builtin_amdgcn_sched_barrier(0);   // keep the above ahead of the state wait
 
@@ -363,26 +379,31 @@ bdlm_block_kernel(const KArgs args) {
         f32x4 ap[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (F32) {
 #pragma unroll
-        for (int k = 0; k < (DIR == kRev ? 0 : QW); k += 2) {
-            if (k + 1 < QW) {
-                s16x4 h0, l0, h1, l1;
-                split4(hq[k], h0, l0);
-                split4(hq[k + 1], h1, l1);
+            for (int k = 0; k < (DIR == kRev ? 0 : QW); ++k)
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], h0, h1, ap[mt]);
-                    ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], l0, l1, ap[mt]);
-                    if constexpr (F32) ap[mt] = mma_k32(cl[mt][k], cl[mt][k + 1], h0, h1, ap[mt]);
-                }
-            } else {
-                s16x4 h0, l0;
-                split4(hq[k], h0, l0);
+                for (int mt = 0; mt < MT; ++mt) ap[mt] = mma_q32(cf[mt][k], hq[k], ap[mt]);
+        } else {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    ap[mt] = mma_k16(cq[mt][k], h0, ap[mt]);
-                    ap[mt] = mma_k16(cq[mt][k], l0, ap[mt]);
-                    if constexpr (F32) ap[mt] = mma_k16(cl[mt][k], h0, ap[mt]);
+            for (int k = 0; k < (DIR == kRev ? 0 : QW); k += 2) {
+                if (k + 1 < QW) {
+                    s16x4 h0, l0, h1, l1;
+                    split4(hq[k], h0, l0);
+                    split4(hq[k + 1], h1, l1);
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], h0, h1, ap[mt]);
+                        ap[mt] = mma_k32(cq[mt][k], cq[mt][k + 1], l0, l1, ap[mt]);
+                    }
+                } else {
+                    s16x4 h0, l0;
+                    split4(hq[k], h0, l0);
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        ap[mt] = mma_k16(cq[mt][k], h0, ap[mt]);
+                        ap[mt] = mma_k16(cq[mt][k], l0, ap[mt]);
+                    }
                 }
             }
         }
@@ -448,27 +469,32 @@ bdlm_block_kernel(const KArgs args) {
                 wj[jt][r] = exp2f(cl2 - shfl(cs, j)) * shfl(dtv, j);
             }
         const uint16_t *sBh = reinterpret_cast<const uint16_t *>(sB);
-        const uint16_t *sBlo = reinterpret_cast<const uint16_t *>(sBl);
+        const float *sBff = reinterpret_cast<const float *>(sBf);
 #pragma unroll
         for (int k = 0; k < QW; ++k) {
             const int q = q0 + k;
             s16x4 th[MT], tl[MT];
+            f32x4 tf[MT];
 #pragma unroll
             for (int jt = 0; jt < MT; ++jt) {
                 f32x4 v;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int e = img_idx<QN, F32>(jt, q, col >> 2, 4 * grp + r) * 4 + (col & 3);
-                    float bv = bf16_to_f32(static_cast<short>(sBh[e]));
-                    if constexpr (F32) bv += bf16_to_f32(static_cast<short>(sBlo[e]));
+                    const float bv = F32 ? sBff[e] : bf16_to_f32(static_cast<short>(sBh[e]));
                     v[r] = bv * wj[jt][r];
                 }
-                split4(v, th[jt], tl[jt]);
+                if constexpr (F32) tf[jt] = v;
+                else split4(v, th[jt], tl[jt]);
             }
             f32x4 acc = hq[k] * keep;
-            acc = mma_quads<MT>(th, xq, acc);
-            acc = mma_quads<MT>(tl, xq, acc);
-            if constexpr (F32) acc = mma_quads<MT>(th, xl, acc);
+            if constexpr (F32) {
+#pragma unroll
+                for (int jt = 0; jt < MT; ++jt) acc = mma_q32(tf[jt], xquad(jt), acc);
+            } else {
+                acc = mma_quads<MT>(th, xq, acc);
+                acc = mma_quads<MT>(tl, xq, acc);
+            }
             __builtin_nontemporal_store(acc, reinterpret_cast<f32x4 *>(hs + q * 16 * kP));
         }
     }
