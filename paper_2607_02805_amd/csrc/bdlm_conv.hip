@@ -5,10 +5,10 @@
 // (local to the block, Sec. 4) is zero-padded past the block's end -- and, for a
 // commit, the cache rows replaced by the last three rows of (cache ++ block).
 //
-// One thread per (batch row, channel, 8-token tile); channels are contiguous across
-// threads, so a token's row is one coalesced read.  A thread loads its tile with a
-// three-row halo on each side (cached rows before the block, zeros after it) and
-// computes both branches from registers; a commit's new cache rows are written by a
+// One thread per (batch row, four channels, 2-token tile); channels are contiguous
+// across threads, so a token's row is one coalesced read of 8 (bf16) or 16 (fp32) bytes
+// per thread.  A thread loads its tile with a three-row halo on each side (cached rows
+// before the block, zeros after it) and computes both branches from registers; a commit's new cache rows are written by a
 // second small kernel once every tile has read the old ones.  Outputs are fp32 in the
 // scan's input layouts (plus dt widened to fp32), consumed by the sequence kernels.
 #include <hip/hip_runtime.h>
@@ -37,37 +37,66 @@ __device__ __forceinline__ float load_act(const void *p, int64_t i, int bf16) {
 }
 __device__ __forceinline__ float silu(float v) { return v / (1.f + expf(-v)); }
 
-constexpr int kTT = 8;   // tokens per thread
+constexpr int kTT = 2;    // tokens per thread
+constexpr int kCV = 4;    // channels per thread (never straddles x / B / C: their
+                          // boundaries are multiples of 16 channels)
+constexpr int kCT = 256;  // threads per workgroup
 
-// grid: (channel blocks of 256, batch rows, token tiles of kTT)
-__global__ void __launch_bounds__(256) bdlm_conv_kernel(const ConvArgs a) {
+// Four consecutive activations of one token row as floats.
+__device__ __forceinline__ void load_act4(const void *p, int64_t i, int bf16, float (&v)[kCV]) {
+    if (bf16) {
+        const uint2 u = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(p) + i);
+        v[0] = __uint_as_float(u.x << 16);
+        v[1] = __uint_as_float(u.x & 0xffff0000u);
+        v[2] = __uint_as_float(u.y << 16);
+        v[3] = __uint_as_float(u.y & 0xffff0000u);
+    } else {
+        const float4 f = *reinterpret_cast<const float4 *>(static_cast<const float *>(p) + i);
+        v[0] = f.x;
+        v[1] = f.y;
+        v[2] = f.z;
+        v[3] = f.w;
+    }
+}
+
+// grid: (channel blocks of kCT * kCV, batch rows, token tiles of kTT)
+__global__ void __launch_bounds__(kCT) bdlm_conv_kernel(const ConvArgs a) {
     const int HP = a.nheads * 64, GN = a.ngroups * a.dstate, CH = HP + 2 * GN;
-    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int c = (blockIdx.x * kCT + threadIdx.x) * kCV;   // first of this thread's channels
     const int b = blockIdx.y;
     const int t0 = blockIdx.z * kTT;
-    if (c >= CH) return;
     const int64_t L = a.L;
     const int64_t BL = static_cast<int64_t>(a.batch) * L;
 
-    // where this channel lives: input element offset of token 0, token stride, and
+    // dt widened to fp32 (heads c .. c + 3; nheads < CH)
+    for (int e = 0; e < kCV; ++e) {
+        const int hh = c + e;
+        if (hh < a.nheads)
+            for (int i = 0; i < kTT; ++i)
+                if (t0 + i < L)
+                    a.out[2 * BL * CH + (b * L + t0 + i) * a.nheads + hh] =
+                        load_act(a.dt, b * a.dts_b + (t0 + i) * a.dts_t + hh, a.bf16);
+    }
+    if (c >= CH) return;
+
+    // where these channels live: input element offset of token 0, token stride, and
     // the fp32 output plane / offset of token 0 / token stride within the plane
     const void *src;
     int64_t in0, in_t;
     int plane;            // 0 x, 1 B, 2 C
     int64_t o0, o_t;
     if (c < HP) {
-        const int h = c / 64, p = c % 64;
         src = a.x;
-        in0 = b * a.xs_b + h * a.xs_h + p;
+        in0 = b * a.xs_b + (c / 64) * a.xs_h + c % 64;
         in_t = a.xs_t;
         plane = 0;
         o0 = b * L * HP + c;
         o_t = HP;
     } else {
-        const int j = (c - HP) % GN, g = j / a.dstate, n = j % a.dstate;
+        const int j = (c - HP) % GN;
         plane = c < HP + GN ? 1 : 2;
         src = plane == 1 ? a.Bm : a.Cm;
-        in0 = b * a.bcs_b + g * a.bcs_g + n;
+        in0 = b * a.bcs_b + (j / a.dstate) * a.bcs_g + j % a.dstate;
         in_t = a.bcs_t;
         o0 = b * L * GN + j;
         o_t = GN;
@@ -80,37 +109,53 @@ __global__ void __launch_bounds__(256) bdlm_conv_kernel(const ConvArgs a) {
     planes[3] = planes[2] + BL * GN;
     planes[4] = planes[3] + BL * HP;
     planes[5] = planes[4] + BL * GN;
-    float *dtf = planes[5] + BL * GN;
     float *of = planes[plane] + o0, *orv = planes[3 + plane] + o0;
 
-    const float4 wv = *reinterpret_cast<const float4 *>(a.w + static_cast<int64_t>(c) * 4);
-    const float bc = a.bias[c];
+    float w[kCV][4], bc[kCV];
+#pragma unroll
+    for (int e = 0; e < kCV; ++e) {
+        const float4 wv = *reinterpret_cast<const float4 *>(a.w + static_cast<int64_t>(c + e) * 4);
+        w[e][0] = wv.x;
+        w[e][1] = wv.y;
+        w[e][2] = wv.z;
+        w[e][3] = wv.w;
+        bc[e] = a.bias[c + e];
+    }
     const int64_t slot = a.use_slots ? a.slots[b] : b;
-    float *crow = a.cache + slot * 3 * CH + c;
+    const float *crow = a.cache + slot * 3 * CH + c;
 
     // inputs u[t0 - 3 .. t0 + kTT + 2]: cached rows before token 0, zeros past L
-    float u[kTT + 6];
+    float u[kTT + 6][kCV];
 #pragma unroll
     for (int i = 0; i < kTT + 6; ++i) {
         const int64_t t = t0 - 3 + i;
-        u[i] = t < 0 ? crow[(t + 3) * CH] : (t < L ? load_act(src, in0 + t * in_t, a.bf16) : 0.f);
+        if (t < 0) {
+#pragma unroll
+            for (int e = 0; e < kCV; ++e) u[i][e] = crow[(t + 3) * CH + e];
+        } else if (t < L) {
+            load_act4(src, in0 + t * in_t, a.bf16, u[i]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < kCV; ++e) u[i][e] = 0.f;
+        }
     }
 #pragma unroll
     for (int i = 0; i < kTT; ++i) {
         const int64_t t = t0 + i;
         if (t < L) {
             // forward: u[t-3 .. t]; reverse: u[t .. t+3] (zeros past the block's end)
-            of[t * o_t] = silu(bc + wv.x * u[i] + wv.y * u[i + 1] + wv.z * u[i + 2] + wv.w * u[i + 3]);
-            orv[t * o_t] =
-                silu(bc + wv.x * u[i + 6] + wv.y * u[i + 5] + wv.z * u[i + 4] + wv.w * u[i + 3]);
+            float vf[kCV], vr[kCV];
+#pragma unroll
+            for (int e = 0; e < kCV; ++e) {
+                vf[e] = silu(bc[e] + w[e][0] * u[i][e] + w[e][1] * u[i + 1][e] +
+                             w[e][2] * u[i + 2][e] + w[e][3] * u[i + 3][e]);
+                vr[e] = silu(bc[e] + w[e][0] * u[i + 6][e] + w[e][1] * u[i + 5][e] +
+                             w[e][2] * u[i + 4][e] + w[e][3] * u[i + 3][e]);
+            }
+            *reinterpret_cast<float4 *>(of + t * o_t) = float4{vf[0], vf[1], vf[2], vf[3]};
+            *reinterpret_cast<float4 *>(orv + t * o_t) = float4{vr[0], vr[1], vr[2], vr[3]};
         }
     }
-    // dt widened to fp32 (one thread per head)
-    if (c < a.nheads)
-        for (int i = 0; i < kTT; ++i)
-            if (t0 + i < L)
-                dtf[(b * L + t0 + i) * a.nheads + c] =
-                    load_act(a.dt, b * a.dts_b + (t0 + i) * a.dts_t + c, a.bf16);
 }
 
 // A commit's cache rows: the last three rows of (cache ++ block), one thread per
@@ -178,8 +223,9 @@ int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, fl
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
         k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
     const int ch = a.nheads * 64 + 2 * a.ngroups * a.dstate;
-    hipLaunchKernelGGL(bdlm_conv_kernel, dim3((ch + 255) / 256, a.batch, (a.L + kTT - 1) / kTT),
-                       dim3(256), 0, static_cast<hipStream_t>(stream), k);
+    hipLaunchKernelGGL(bdlm_conv_kernel,
+                       dim3((ch + kCT * kCV - 1) / (kCT * kCV), a.batch, (a.L + kTT - 1) / kTT),
+                       dim3(kCT), 0, static_cast<hipStream_t>(stream), k);
     if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
     if (commit) {
         hipLaunchKernelGGL(bdlm_conv_keep_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
