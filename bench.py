@@ -652,6 +652,29 @@ def summarize_dispatches(trace_csv: str) -> str:
     return "\n".join(out)
 
 
+def summarize_counters(counter_csv: str) -> str:
+    """Markdown table of the per-dispatch medians of each counter in a rocprofv3 --pmc
+    counter_collection.csv, per bdlm kernel and launch shape."""
+    import statistics as st
+    groups, names = {}, []
+    for r in _csv_rows(counter_csv):
+        name = r["Kernel_Name"].replace("bdlm::(anonymous namespace)::", "").split("(")[0]
+        if "bdlm" not in name:
+            continue
+        key = (name, int(r["Grid_Size"]) // int(r["Workgroup_Size"]), int(r["Workgroup_Size"]))
+        c = r["Counter_Name"]
+        if c not in names:
+            names.append(c)
+        groups.setdefault(key, {}).setdefault(c, {})[r["Dispatch_Id"]] = float(r["Counter_Value"])
+    out = ["| kernel | workgroups x threads | dispatches | " + " | ".join(names) + " |",
+           "|---|---|---|" + "---|" * len(names)]
+    for (name, wgs, wg), d in groups.items():
+        n = max(len(v) for v in d.values())
+        vals = [f"{st.median(d[c].values()):.0f}" if c in d else "" for c in names]
+        out.append(f"| `{name[:60]}` | {wgs} x {wg} | {n} | " + " | ".join(vals) + " |")
+    return "\n".join(out)
+
+
 def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
                       copy_bytes=256 << 20, kernels=None) -> dict:
     """Per-launch HBM bytes of kernels (default: the block step and the commit; else a
@@ -723,6 +746,8 @@ def main():
                     help="print a markdown summary of a rocprofv3 kernel_stats.csv and exit")
     ap.add_argument("--summarize-dispatches", metavar="KERNEL_TRACE_CSV",
                     help="print per-shape kernel durations from a rocprofv3 kernel_trace.csv")
+    ap.add_argument("--summarize-counters", metavar="COUNTER_COLLECTION_CSV",
+                    help="print per-kernel medians of a rocprofv3 --pmc counter_collection.csv")
     ap.add_argument("--summarize-traffic", nargs=4,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
@@ -734,6 +759,9 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters))
         return
     if args.summarize_dispatches:
         print(summarize_dispatches(args.summarize_dispatches))
