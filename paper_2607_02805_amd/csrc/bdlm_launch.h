@@ -92,6 +92,10 @@ inline BoundaryPlan boundary_plan(int64_t batch, int64_t nheads, int64_t dstate,
     const int64_t want = units >= 4096 ? 1 : (4096 + units - 1) / units;   // segments per row
     p.blocks_per_seg = (nblocks + want - 1) / want;
     if (p.blocks_per_seg * L < 256) p.blocks_per_seg = (256 + L - 1) / L;   // >= 256 tokens
+    if (L == 16 || L == 32) {   // whole 64-token chunks per segment
+        const int64_t per = 64 / L;
+        p.blocks_per_seg = (p.blocks_per_seg + per - 1) / per * per;
+    }
     if (p.blocks_per_seg > nblocks) p.blocks_per_seg = nblocks > 0 ? nblocks : 1;
     p.nseg = nblocks > 0 ? (nblocks + p.blocks_per_seg - 1) / p.blocks_per_seg : 1;
     p.state_bytes = units * p.nseg * int64_t(BDLM_HEADDIM) * dstate * 4;

@@ -514,8 +514,12 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 }
 
 // ------------------------------------------------------------------ seg_out
-template <int NS, bool F32, bool REV>
+// SUB > 0 (forward, with an emission pool): 64-token chunks holding blocks of SUB (16
+// or 32) tokens; the state is carried block by block and the state entering every
+// block is written.  SUB == 0: one emitted block per chunk of cstride tokens.
+template <int NS, bool F32, bool REV, int SUB>
 __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(const SeqArgs a) {
+    static_assert(SUB == 0 || (!REV && (SUB == 16 || SUB == 32)), "block length");
     using G = Geo<NS, F32>;
     constexpr int QN = G::QN;
     constexpr int IMG = G::IMG;
@@ -558,7 +562,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
     float *emit_base = nullptr;
     int64_t emit_first = 0;
     if (!REV && a.emit) {
-        emit_first = (static_cast<int64_t>(un.seg) * a.S) / a.cstride;
+        emit_first = (static_cast<int64_t>(un.seg) * a.S) / (SUB > 0 ? SUB : a.cstride);
         emit_base = a.emit + (static_cast<int64_t>(un.b) * a.emit_blocks * a.nheads + un.h) * (kP * NS);
         float *dst = emit_base + emit_first * a.nheads * (kP * NS);
 #pragma unroll
@@ -746,6 +750,63 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         }
         }
 
+        if constexpr (SUB > 0) {
+            // several blocks per chunk: carry the state one block at a time and write the
+            // state entering each block of this segment (the next segment writes the one
+            // entering its own first block)
+            constexpr int NSUB = kC / SUB, JPB = SUB / 16;   // blocks, token tiles per block
+            const int64_t seg_tokens = st.s1 - st.s0;
+            const int64_t nb_seg = (seg_tokens + SUB - 1) / SUB;
+            float cs_prev = 0.f;
+#pragma unroll
+            for (int sb = 0; sb < NSUB; ++sb) {
+                if (static_cast<int64_t>(c) * kC + sb * SUB < seg_tokens) {
+                    const float cs_end = sCs[(sb + 1) * SUB - 1];
+                    const float keepb = ex2(cs_end - cs_prev);
+                    cs_prev = cs_end;
+                    // this block's tokens, weighted to its end: 2^(cs_end - cs_j) dt_j x_j
+                    WOps<F32> wb;
+#pragma unroll
+                    for (int jt = sb * JPB; jt < (sb + 1) * JPB; ++jt) {
+                        const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
+                        const f32x4 dtq = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
+                        f32x4 wv;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) wv[r] = ex2(cs_end - csq[r]) * dtq[r];
+                        w_set<F32>(wb, jt, wv * xv(jt));
+                    }
+                    BtOps<F32> cur;
+#pragma unroll
+                    for (int q = 0; q < QN; ++q) {
+                        bt_read<NS, F32>(cur, sBt, q, grp, col);
+                        f32x4 acc = S[q] * keepb;
+                        if constexpr (F32) {
+#pragma unroll
+                            for (int jt = sb * JPB; jt < (sb + 1) * JPB; ++jt)
+                                acc = mma_f32q(cur.f[jt], wb.f[jt], acc);
+                        } else if constexpr (JPB == 2) {
+                            acc = mma_k32(cur.h[2 * sb], cur.h[2 * sb + 1], wb.h[2 * sb], wb.h[2 * sb + 1], acc);
+                            acc = mma_k32(cur.h[2 * sb], cur.h[2 * sb + 1], wb.l[2 * sb], wb.l[2 * sb + 1], acc);
+                        } else {
+                            acc = mma_k16(cur.h[sb], wb.h[sb], acc);
+                            acc = mma_k16(cur.h[sb], wb.l[sb], acc);
+                        }
+                        S[q] = acc;
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                    const int64_t blk = static_cast<int64_t>(c) * NSUB + sb + 1;   // S enters it
+                    if (blk < nb_seg) {
+                        float *dst = emit_base + (emit_first + blk) * a.nheads * (kP * NS);
+#pragma unroll
+                        for (int q = 0; q < QN; ++q)
+                            *reinterpret_cast<f32x4 *>(dst + quad_off(q, grp, p)) = S[q];
+                    }
+                }
+            }
+            __syncthreads();   // LDS is rewritten by the next chunk
+            continue;
+        }
+
         // carry the state across the chunk (not after the last one unless it is kept)
         if (c + 1 == nch && !a.pool_out) break;
         const float keep = ex2(sCs[kC - 1]);
@@ -864,9 +925,21 @@ hipError_t state_launch(const SeqArgs &k, bool both, unsigned grid, hipStream_t 
 template <int NS, bool F32>
 hipError_t out_launch(const SeqArgs &k, bool rev, unsigned grid, hipStream_t s) {
     if (rev)
-        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, true>), dim3(grid), dim3(kThreads), 0, s, k);
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, true, 0>), dim3(grid), dim3(kThreads), 0, s,
+                           k);
     else
-        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false>), dim3(grid), dim3(kThreads), 0, s, k);
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false, 0>), dim3(grid), dim3(kThreads), 0,
+                           s, k);
+    return hipGetLastError();
+}
+template <int NS, bool F32>
+hipError_t out_sub_launch(const SeqArgs &k, int sub, unsigned grid, hipStream_t s) {
+    if (sub == 16)
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false, 16>), dim3(grid), dim3(kThreads), 0,
+                           s, k);
+    else
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false, 32>), dim3(grid), dim3(kThreads), 0,
+                           s, k);
     return hipGetLastError();
 }
 
@@ -877,6 +950,16 @@ hipError_t run_state(int ns, const SeqArgs &k, bool both, unsigned grid, hipStre
         case 32: return state_launch<32, F32>(k, both, grid, s);
         case 64: return state_launch<64, F32>(k, both, grid, s);
         case 128: return state_launch<128, F32>(k, both, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+template <bool F32>
+hipError_t run_out_sub(int ns, const SeqArgs &k, int sub, unsigned grid, hipStream_t s) {
+    switch (ns) {
+        case 16: return out_sub_launch<16, F32>(k, sub, grid, s);
+        case 32: return out_sub_launch<32, F32>(k, sub, grid, s);
+        case 64: return out_sub_launch<64, F32>(k, sub, grid, s);
+        case 128: return out_sub_launch<128, F32>(k, sub, grid, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1033,13 +1116,19 @@ int launch_boundary_states(const LaunchArgs &a, int64_t nblocks, const float *s_
             k.zero_init = 0;
         }
     }
-    k.cstride = a.L;
     k.emit = s_out;
     k.emit_blocks = nblocks;
     k.skip = a.D;
-    if ((f32 ? run_out<true>(a.dstate, k, false, grid, s)
-             : run_out<false>(a.dstate, k, false, grid, s)) != hipSuccess)
-        return BDLM_E_LAUNCH;
+    hipError_t e;
+    if (a.L == 16 || a.L == 32) {   // 64-token chunks carrying the state block by block
+        k.cstride = kC;
+        e = f32 ? run_out_sub<true>(a.dstate, k, a.L, grid, s)
+                : run_out_sub<false>(a.dstate, k, a.L, grid, s);
+    } else {                        // one block per chunk
+        k.cstride = a.L;
+        e = f32 ? run_out<true>(a.dstate, k, false, grid, s) : run_out<false>(a.dstate, k, false, grid, s);
+    }
+    if (e != hipSuccess) return BDLM_E_LAUNCH;
     return BDLM_OK;
 }
 
