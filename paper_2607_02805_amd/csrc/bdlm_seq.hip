@@ -157,7 +157,30 @@ constexpr int kNT = 2;   // buffer cache policy: nontemporal
 // One chunk's global loads into registers and their staging into LDS.  Local token
 // i of chunk c is the segment's token 64c + i (reverse: its 64c + i-th token from
 // the end); row(i) is its position in the chunk's memory window.
-template <int NS, bool F32, bool REV, bool LOADC>
+// Slots of the bf16 transposed images as seg_state lays them out: element (token
+// quad tq, column n) of the transposed B image at bt_slot<NS>(tq, n), of the
+// transposed x image at xt_slot(tq, p).  The column is XOR-permuted within its row so
+// that the staging writes (a task writes 8 consecutive columns of one token quad,
+// tasks ordered column piece fastest) and the operand reads (16 columns x 2 token
+// quads per half-wave) each touch every LDS bank once (checked on the CPU for every
+// dstate).  seg_out keeps the plain layout (tq * stride + column).
+template <int NS>
+__device__ __forceinline__ int bt_slot(int tq, int n) {
+    int t;
+    if constexpr (NS == 16) t = (tq >> 1) & 7;
+    else if constexpr (NS == 32) t = (tq & 7) | ((tq & 1) << 4);
+    else if constexpr (NS == 64)
+        t = ((tq & 1) << 4) | (((n >> 4) & 1) << 2) | (((tq >> 1) & 1) << 1) | ((n >> 5) & 1);
+    else t = ((tq & 1) << 4) | ((n >> 4) & 1) | (((n >> 5) & 3) << 1);
+    return tq * NS + (n ^ t);
+}
+__device__ __forceinline__ int xt_slot(int tq, int p) {
+    const int t = ((tq & 1) << 4) | ((p >> 4) & 1) | (((tq >> 1) & 1) << 1) | (((p >> 5) & 1) << 2);
+    return tq * kP + (p ^ t);
+}
+
+// SWZ: the permuted transposed layouts above (bf16 storage only).
+template <int NS, bool F32, bool REV, bool LOADC, bool SWZ = false>
 struct Stager {
     using G = Geo<NS, F32>;
     static constexpr int ES = F32 ? 4 : 2;
@@ -270,12 +293,19 @@ struct Stager {
 
     // Transposed quads: out[g * stride + col] holds the four tokens 4g .. 4g+3 of
     // column col = piece * E + e.
-    __device__ __forceinline__ static void transpose_bf16(const u32x4 (&v)[4], int base,
+    __device__ __forceinline__ static void transpose_bf16(const u32x4 (&v)[4], int g, int pc,
                                                           uint2 *out) {
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            out[base + 2 * d] = uint2{lo_pair(v[0][d], v[1][d]), lo_pair(v[2][d], v[3][d])};
-            out[base + 2 * d + 1] = uint2{hi_pair(v[0][d], v[1][d]), hi_pair(v[2][d], v[3][d])};
+            const uint2 lo = uint2{lo_pair(v[0][d], v[1][d]), lo_pair(v[2][d], v[3][d])};
+            const uint2 hi = uint2{hi_pair(v[0][d], v[1][d]), hi_pair(v[2][d], v[3][d])};
+            if constexpr (SWZ) {
+                out[bt_slot<NS>(g, pc * 8 + 2 * d)] = lo;
+                out[bt_slot<NS>(g, pc * 8 + 2 * d + 1)] = hi;
+            } else {
+                out[g * NS + pc * 8 + 2 * d] = lo;
+                out[g * NS + pc * 8 + 2 * d + 1] = hi;
+            }
         }
     }
 
@@ -299,7 +329,7 @@ struct Stager {
                             f32x4{__uint_as_float(rb[k][0][e]), __uint_as_float(rb[k][1][e]),
                                   __uint_as_float(rb[k][2][e]), __uint_as_float(rb[k][3][e])};
                 } else {
-                    transpose_bf16(rb[k], g * NS + pc * 8, bt);
+                    transpose_bf16(rb[k], g, pc, bt);
                 }
             }
         }
@@ -319,9 +349,16 @@ struct Stager {
                     uint32_t *x32 = reinterpret_cast<uint32_t *>(xt);
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {
-                        const int at = ((g >> 1) * kP + pc * 8 + 2 * d) * 2 + (g & 1);
-                        x32[at] = lo_pair(rx[k][0][d], rx[k][1][d]);
-                        x32[at + 2] = hi_pair(rx[k][0][d], rx[k][1][d]);
+                        if constexpr (SWZ) {
+                            x32[xt_slot(g >> 1, pc * 8 + 2 * d) * 2 + (g & 1)] =
+                                lo_pair(rx[k][0][d], rx[k][1][d]);
+                            x32[xt_slot(g >> 1, pc * 8 + 2 * d + 1) * 2 + (g & 1)] =
+                                hi_pair(rx[k][0][d], rx[k][1][d]);
+                        } else {
+                            const int at = ((g >> 1) * kP + pc * 8 + 2 * d) * 2 + (g & 1);
+                            x32[at] = lo_pair(rx[k][0][d], rx[k][1][d]);
+                            x32[at + 2] = hi_pair(rx[k][0][d], rx[k][1][d]);
+                        }
                     }
                 }
             }
@@ -393,11 +430,12 @@ __device__ __forceinline__ void w_set(WOps<F32> &o, int jt, f32x4 v) {
     if constexpr (F32) o.f[jt] = v;
     else split4(v, o.h[jt], o.l[jt]);
 }
-template <int NS, bool F32>
+template <int NS, bool F32, bool SWZ = false>
 __device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, int q, int grp, int col) {
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
         if constexpr (F32) o.f[jt] = f32q(bt, (4 * jt + grp) * NS + 16 * q + col);
+        else if constexpr (SWZ) o.h[jt] = as_s16x4(bt[bt_slot<NS>(4 * jt + grp, 16 * q + col)]);
         else o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
     }
 }
@@ -456,7 +494,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
     const Unit un = decode(a);
     const int g = un.h / a.heads_per_group;
 
-    Stager<NS, F32, false, false> st;
+    Stager<NS, F32, false, false, !F32> st;   // permuted transposed images (bf16)
     setup(st, a, un, g, tid, lane);
     const int nch = st.nchunks();
     const float A2 = a.A[un.h] * kLog2e;
@@ -483,7 +521,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         for (int jt = 0; jt < 4; ++jt) {
             s16x4 xh, xl;
             f32x4 xv;
-            x_operand<F32>(sXt[(4 * jt + grp) * kP + p], xh, xl, xv);
+            x_operand<F32>(sXt[F32 ? (4 * jt + grp) * kP + p : xt_slot(4 * jt + grp, p)], xh, xl, xv);
             w_set<F32>(wf, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv);
             if constexpr (BOTH)
                 w_set<F32>(wr, jt,
@@ -491,10 +529,10 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         }
         const float keep = ex2(tot);
         BtOps<F32> cur, nxt;
-        bt_read<NS, F32>(cur, sBt, 0, grp, col);
+        bt_read<NS, F32, !F32>(cur, sBt, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
-            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, grp, col);
+            if (q + 1 < QN) bt_read<NS, F32, !F32>(nxt, sBt, q + 1, grp, col);
             F[q] = bt_mma<F32>(cur, wf, F[q] * keep);
             if constexpr (BOTH) R[q] = bt_mma<F32>(cur, wr, R[q]);
             if (q + 1 < QN) cur = nxt;
