@@ -675,6 +675,43 @@ def summarize_counters(counter_csv: str) -> str:
     return "\n".join(out)
 
 
+def summarize_traffic_shapes(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
+                             copy_bytes=256 << 20) -> str:
+    """Markdown table of per-dispatch HBM bytes (medians of FETCH_SIZE / WRITE_SIZE, each
+    scaled by the same counter's reading for a plain copy of known size) per bdlm kernel
+    and launch shape."""
+    import statistics as st
+
+    def groups(path, counter):
+        d = {}
+        for r in _csv_rows(path):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"].replace("bdlm::(anonymous namespace)::", "").split("(")[0]
+            key = (name, int(r["Grid_Size"]) // int(r["Workgroup_Size"]), int(r["Workgroup_Size"]))
+            d.setdefault(key, []).append(float(r["Counter_Value"]))
+        return d
+
+    def copy_kib(path, counter):
+        return st.median(v for (n, _, _), vs in groups(path, counter).items()
+                         if "copyBuffer" in n for v in vs)
+
+    f_scale = copy_bytes / 1024 / copy_kib(copy_fetch_csv, "FETCH_SIZE")
+    w_scale = copy_bytes / 1024 / copy_kib(copy_write_csv, "WRITE_SIZE")
+    fetch, write = groups(fetch_csv, "FETCH_SIZE"), groups(write_csv, "WRITE_SIZE")
+    out = [f"FETCH_SIZE x {f_scale:.4f} KiB, WRITE_SIZE x {w_scale:.4f} KiB (copy calibration)",
+           "", "| kernel | workgroups x threads | dispatches | fetch bytes | write bytes |",
+           "|---|---|---|---|---|"]
+    for key in sorted(set(fetch) | set(write), key=lambda k: -st.median(fetch.get(k, [0]))):
+        if "bdlm" not in key[0]:
+            continue
+        fb = st.median(fetch[key]) * 1024 * f_scale if key in fetch else float("nan")
+        wb = st.median(write[key]) * 1024 * w_scale if key in write else float("nan")
+        n = max(len(fetch.get(key, [])), len(write.get(key, [])))
+        out.append(f"| `{key[0][:60]}` | {key[1]} x {key[2]} | {n} | {fb:,.0f} | {wb:,.0f} |")
+    return "\n".join(out)
+
+
 def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
                       copy_bytes=256 << 20, kernels=None) -> dict:
     """Per-launch HBM bytes of kernels (default: the block step and the commit; else a
@@ -748,6 +785,9 @@ def main():
                     help="print per-shape kernel durations from a rocprofv3 kernel_trace.csv")
     ap.add_argument("--summarize-counters", metavar="COUNTER_COLLECTION_CSV",
                     help="print per-kernel medians of a rocprofv3 --pmc counter_collection.csv")
+    ap.add_argument("--summarize-traffic-shapes", nargs=4,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="print per-dispatch HBM bytes per kernel and launch shape and exit")
     ap.add_argument("--summarize-traffic", nargs=4,
                     metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
@@ -759,6 +799,9 @@ def main():
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_traffic_shapes:
+        print(summarize_traffic_shapes(*args.summarize_traffic_shapes))
         return
     if args.summarize_counters:
         print(summarize_counters(args.summarize_counters))
