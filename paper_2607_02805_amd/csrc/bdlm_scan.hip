@@ -195,11 +195,13 @@ bdlm_block_kernel(const KArgs args) {
             xch[k] = *(j < L ? gchunk(xg + j * args.xs_t + c * E) : gzero());
         }
     }
+    // dt (lane t = token t), loaded by every wave though wave 0 alone stages it: where
+    // a load under a branch joins the other path the compiler converts its value right
+    // away, i.e. waits there for every load issued before it (the state loads of wave 0
+    // would then leave only after all of its inputs had arrived)
     typedef __attribute__((address_space(1))) const AT g_at;
-    AT dtraw = AT(0);
-    if (wave == 0)
-        dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
-                           : (const g_at *)(&kZeroChunk));
+    const AT dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
+                                : (const g_at *)(&kZeroChunk));
     // per-head parameters as vector loads in this first batch: a scalar load issued
     // later would queue behind the state loads of every workgroup
     typedef __attribute__((address_space(1))) const float g_f;
