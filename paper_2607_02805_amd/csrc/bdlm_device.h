@@ -86,6 +86,25 @@ __device__ __forceinline__ f32x4 mma_quads(const s16x4 (&a)[Q], const s16x4 (&b)
 
 __device__ __forceinline__ float shfl(float v, int src) { return __shfl(v, src, 64); }
 
+// Inclusive sum over the 64 lanes of a wave on DPP, without LDS: shifts by 1, 2, 4, 8
+// within each row of 16 lanes (lanes shifted in from outside the row read 0), then
+// row 0's total into row 1 (and row 2's into row 3), then the total of rows 0-1 into
+// rows 2-3.
+template <int CTRL, int ROW_MASK, bool BOUND_ZERO>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xf,
+                                                      BOUND_ZERO));
+}
+__device__ __forceinline__ float wave_inclusive_sum(float v) {
+    v += dpp<0x111, 0xf, true>(v);   // row_shr:1
+    v += dpp<0x112, 0xf, true>(v);   // row_shr:2
+    v += dpp<0x114, 0xf, true>(v);   // row_shr:4
+    v += dpp<0x118, 0xf, true>(v);   // row_shr:8
+    v += dpp<0x142, 0xa, false>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp<0x143, 0xc, false>(v);  // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 // Rows past the end of the block read this zero chunk instead of activations: the
 // load address is selected, never the loaded value, so every load stays an
 // unconditional instruction that can be issued ahead of any wait.

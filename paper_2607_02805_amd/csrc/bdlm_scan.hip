@@ -92,9 +92,9 @@ struct KArgs {
 //      the state, 16 bytes per quad, into registers;
 //   1. B and C are written to LDS as "register images" (the exact per-lane quads
 //      an MFMA operand needs, so reading one is a linear, conflict-free 8-byte
-//      read), x row-major, dt as floats;
-//   2. each wave runs the decay prefix sums of the block (lane t = token t);
-//      the Gram tiles are shared out over the waves, turned into the
+//      read), x row-major; wave 0 runs the decay prefix sums of the block on DPP
+//      (lane t = token t) and publishes dt, cs and ex as floats;
+//   2. the Gram tiles are shared out over the waves, turned into the
 //      decay-weighted matrix M[t,j] = G[t,j] W[t,j] dt_j, split and published in
 //      LDS;
 //   3. the first group contracts M with x (its 16 columns) and precomputes the
@@ -134,7 +134,7 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) uint2 sC[F32 ? 1 : IMG], sB[F32 ? 1 : IMG];
     __shared__ __align__(16) f32x4 sCf[F32 ? IMG : 1], sBf[F32 ? IMG : 1];
     __shared__ __align__(16) AT sX[LT * XS];
-    __shared__ __align__(16) float sDt[64];
+    __shared__ __align__(16) float sDt[64], sCs[64], sEx[64];   // dt, cs, ex per token
     __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
     __shared__ __align__(16) f32x4 sRed[(NPART > 1 ? NPART - 1 : 1) * 4 * MT * 64];
@@ -250,22 +250,22 @@ bdlm_block_kernel(const KArgs args) {
         dst[0] = uint2{v.x, v.y};
         dst[1] = uint2{v.z, v.w};
     }
-    if (tid < 64) sDt[tid] = Act<F32>::val(dtraw);
     if (tid < 3) sPar[tid] = parv;
+    if (wave == 0) {
+        // decay sums of the block in base 2 (lane t = token t; padded tokens have dt = 0):
+        // cs_t = l_0 + ... + l_t with l_t = dt_t A_h, and ex_t = cs_{t-1} (ex_0 = 0)
+        const float dtv = Act<F32>::val(dtraw);
+        const float A2 =
+            __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(parv))) * kLog2e;
+        const float cs = wave_inclusive_sum(dtv * A2);
+        const float up = __shfl_up(cs, 1, 64);
+        sDt[lane] = dtv;
+        sCs[lane] = cs;
+        sEx[lane] = lane == 0 ? 0.f : up;
+    }
     __syncthreads();
 
-    // ---- phase 2: decay prefix sums (every wave), Gram tiles (shared out)
-    const float dtv = sDt[lane];
-    const float A2 = sPar[0] * kLog2e;    // work in base 2
-    const float l2 = dtv * A2;
-    float cs = l2;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const float v = __shfl_up(cs, off, 64);
-        if (lane >= off) cs += v;
-    }
-    float ex = __shfl_up(cs, 1, 64);
-    if (lane == 0) ex = 0.f;
+    // ---- phase 2: Gram tiles (shared out)
 
     for (int tile = wave; tile < MT * MT; tile += NW) {
         const int mt = tile / MT, jt = tile % MT;
@@ -289,17 +289,20 @@ bdlm_block_kernel(const KArgs args) {
             }
         }
         const int t = 16 * mt + col;
-        const float cst = shfl(cs, t), ext = shfl(ex, t);
+        const float cst = sCs[t], ext = sEx[t];
+        const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
+        const f32x4 exj = *reinterpret_cast<const f32x4 *>(&sEx[16 * jt + 4 * grp]);
+        const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
         f32x4 m;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+            // below the diagonal the forward decay from j to t, above it the reverse decay
+            // a_t ... a_{j-1}; on it the token's own input, once per branch computed here
             const int j = 16 * jt + 4 * grp + r;
-            const float csj = shfl(cs, j), exj = shfl(ex, j), dtj = shfl(dtv, j);
-            float w;
-            if (j < t) w = DIR == kRev ? 0.f : exp2f(cst - csj);
-            else if (j == t) w = DIR == kBoth ? 2.f : 1.f;
-            else w = DIR == kFwd ? 0.f : exp2f(exj - ext);
-            m[r] = gacc[r] * w * dtj;
+            const float e = exp2f(j < t ? cst - csj[r] : exj[r] - ext);
+            const float w = j == t ? (DIR == kBoth ? 2.f : 1.f)
+                                   : (j < t ? (DIR == kRev ? 0.f : e) : (DIR == kFwd ? 0.f : e));
+            m[r] = gacc[r] * w * dtj[r];
         }
         if constexpr (F32) {
             sM[tile * 64 + lane] = __builtin_bit_cast(uint4, m);
@@ -355,10 +358,11 @@ bdlm_block_kernel(const KArgs args) {
                     ai = mma_quads<MT>(mh, xq, ai);
                     ai = mma_quads<MT>(ml, xq, ai);
                 }
+                const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs[16 * mt + 4 * grp]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     pre[mt][r] = ai[r] + skip * xv[mt][r];
-                    es[mt][r] = exp2f(shfl(cs, 16 * mt + 4 * grp + r));
+                    es[mt][r] = exp2f(csq[r]);
                     pin(pre[mt][r]);
                     pin(es[mt][r]);
                 }
@@ -460,16 +464,16 @@ bdlm_block_kernel(const KArgs args) {
         // on this wave's dstate quads.  A operand: lane (col, grp) holds the weighted
         // B[16jt + 4grp + r, 16q + col], read from the B image (element (j, n) sits in
         // the quad of tile j/16, quad n/16, group n%16/4, column j%16, at slot n%4).
-        const float cl2 = shfl(cs, 63);  // cs of the last real token (padding adds 0)
+        const float cl2 = sCs[63];  // cs of the last real token (padding adds 0)
         const float keep = exp2f(cl2);
         float wj[MT][4];
 #pragma unroll
-        for (int jt = 0; jt < MT; ++jt)
+        for (int jt = 0; jt < MT; ++jt) {
+            const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
+            const f32x4 dtq = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int j = 16 * jt + 4 * grp + r;
-                wj[jt][r] = exp2f(cl2 - shfl(cs, j)) * shfl(dtv, j);
-            }
+            for (int r = 0; r < 4; ++r) wj[jt][r] = exp2f(cl2 - csq[r]) * dtq[r];
+        }
         const uint16_t *sBh = reinterpret_cast<const uint16_t *>(sB);
         const float *sBff = reinterpret_cast<const float *>(sBf);
 #pragma unroll
