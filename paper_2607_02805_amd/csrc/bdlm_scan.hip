@@ -86,10 +86,11 @@ struct KArgs {
 //     products of the groups are summed through LDS before y is stored.
 //
 // Phases:
-//   0. every global load is issued up front and unconditionally (rows past the
-//      block read a zero chunk): B, C, x, dt and the per-head parameters in
-//      coalesced 16-byte chunks by the whole workgroup, then this wave's share of
-//      the state, 16 bytes per quad, into registers;
+//   0. every global load is issued unconditionally (rows past the block read a
+//      zero chunk): B, C, x, dt and the per-head parameters in coalesced 16-byte
+//      chunks by the whole workgroup, then the first half of this wave's share of
+//      the state, 16 bytes per quad, into registers (the second half follows the
+//      first barrier);
 //   1. B and C are written to LDS as "register images" (the exact per-lane quads
 //      an MFMA operand needs, so reading one is a linear, conflict-free 8-byte
 //      read), x row-major; wave 0 runs the decay prefix sums of the block on DPP
@@ -179,8 +180,8 @@ bdlm_block_kernel(const KArgs args) {
             const int t = i / CPR, c = i % CPR;
             const int64_t o = t * args.bcs_t + c * E;
             const bool ok = t < L;
-            cch[k] = *(ok ? gchunk(Cg + o) : gzero());
-            bch[k] = *(ok ? gchunk(Bg + o) : gzero());
+            cch[k] = __builtin_nontemporal_load(ok ? gchunk(Cg + o) : gzero());
+            bch[k] = __builtin_nontemporal_load(ok ? gchunk(Bg + o) : gzero());
         }
     }
     constexpr int X_CH = LT * (kP / E);
@@ -192,7 +193,8 @@ bdlm_block_kernel(const KArgs args) {
         for (int k = 0; k < X_PT; ++k) {
             const int i = tid + NT * k;                    // chunk fastest (coalesced)
             const int j = i / (kP / E), c = i % (kP / E);
-            xch[k] = *(j < L ? gchunk(xg + j * args.xs_t + c * E) : gzero());
+            xch[k] = __builtin_nontemporal_load(j < L ? gchunk(xg + j * args.xs_t + c * E)
+                                                      : gzero());
         }
     }
     // dt (lane t = token t), loaded by every wave though wave 0 alone stages it: where
@@ -212,12 +214,20 @@ bdlm_block_kernel(const KArgs args) {
     }
     // keep the small loads above ahead of the state loads (loads return in order)
     __builtin_amdgcn_sched_barrier(0);
+    // The state is requested in two halves: the first now, the second once the
+    // workgroup's inputs have arrived (after the first barrier).  With every state
+    // load of the chip in flight at once, the input loads of a workgroup queue behind
+    // them and hold up all the work that does not need the state; the second half
+    // still arrives before it is needed.  Everything here is read once per step and
+    // streams past the caches (nontemporal).
+    constexpr int QE = (QW + 1) / 2;   // state quads requested up front
     f32x4 hq[QW];  // state s[p, 16(q0 + k) + 4grp + r]
-#pragma unroll
-    for (int k = 0; k < QW; ++k) {  // read once per step: stream past the caches
+    auto load_state = [&](int k) {
         if constexpr (DIR == kRev) hq[k] = f32x4{0.f, 0.f, 0.f, 0.f};   // the state is not used
         else hq[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(hs + (q0 + k) * 16 * kP));
-    }
+    };
+#pragma unroll
+    for (int k = 0; k < QE; ++k) load_state(k);
 
     // ---- phase 1: LDS images
 #pragma unroll
@@ -264,6 +274,8 @@ bdlm_block_kernel(const KArgs args) {
         sEx[lane] = lane == 0 ? 0.f : up;
     }
     __syncthreads();
+#pragma unroll
+    for (int k = QE; k < QW; ++k) load_state(k);
 
     // ---- phase 2: Gram tiles (shared out)
 
