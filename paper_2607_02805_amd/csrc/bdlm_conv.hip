@@ -8,9 +8,12 @@
 // One thread per (batch row, four channels, 2-token tile); channels are contiguous
 // across threads, so a token's row is one coalesced read of 8 (bf16) or 16 (fp32) bytes
 // per thread.  A thread loads its tile with a three-row halo on each side (cached rows
-// before the block, zeros after it) and computes both branches from registers; a commit's new cache rows are written by a
-// second small kernel once every tile has read the old ones.  Outputs are fp32 in the
-// scan's input layouts (plus dt widened to fp32), consumed by the sequence kernels.
+// before the block, zeros after it) and computes both branches from registers; a
+// commit's new cache rows are written by a second small kernel once every tile has
+// read the old ones.  Every row is read as the sum of two unconditional loads, the
+// cached row and the input row, each replaced by a zero chunk where it does not apply,
+// so all loads of a thread are in flight at once.  Outputs are fp32 in the scan's
+// input layouts (plus dt widened to fp32), consumed by the block kernels.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,6 +38,25 @@ __device__ __forceinline__ float load_act(const void *p, int64_t i, int bf16) {
         return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t *>(p)[i]) << 16);
     return static_cast<const float *>(p)[i];
 }
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+__device__ const v4f kZero4 = {0.f, 0.f, 0.f, 0.f};
+typedef __attribute__((address_space(1))) const v4f g_v4f;
+typedef __attribute__((address_space(1))) const v2u g_v2u;
+typedef __attribute__((address_space(1))) const uint16_t g_u16;
+typedef __attribute__((address_space(1))) const float g_f32;
+
+// One activation (element i of p) as a float, or zero when !ok (read from a zero chunk).
+template <bool BF16>
+__device__ __forceinline__ float load_act_or_zero(const void *p, int64_t i, bool ok) {
+    if constexpr (BF16)
+        return __uint_as_float(static_cast<uint32_t>(*(ok ? (const g_u16 *)(static_cast<const uint16_t *>(p) + i)
+                                                          : (const g_u16 *)(&kZero4)))
+                               << 16);
+    else
+        return *(ok ? (const g_f32 *)(static_cast<const float *>(p) + i) : (const g_f32 *)(&kZero4));
+}
 __device__ __forceinline__ float silu(float v) { return v / (1.f + expf(-v)); }
 
 constexpr int kTT = 2;    // tokens per thread
@@ -42,24 +64,22 @@ constexpr int kCV = 4;    // channels per thread (never straddles x / B / C: the
                           // boundaries are multiples of 16 channels)
 constexpr int kCT = 256;  // threads per workgroup
 
-// Four consecutive activations of one token row as floats.
-__device__ __forceinline__ void load_act4(const void *p, int64_t i, int bf16, float (&v)[kCV]) {
-    if (bf16) {
-        const uint2 u = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(p) + i);
-        v[0] = __uint_as_float(u.x << 16);
-        v[1] = __uint_as_float(u.x & 0xffff0000u);
-        v[2] = __uint_as_float(u.y << 16);
-        v[3] = __uint_as_float(u.y & 0xffff0000u);
+// Four consecutive activations of one token row (element i of p) as floats, or zeros
+// when !ok (the load then reads a zero chunk).
+template <bool BF16>
+__device__ __forceinline__ v4f load_act4(const void *p, int64_t i, bool ok) {
+    if constexpr (BF16) {
+        const v2u u = *(ok ? (const g_v2u *)(static_cast<const uint16_t *>(p) + i)
+                           : (const g_v2u *)(&kZero4));
+        return v4f{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                   __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
     } else {
-        const float4 f = *reinterpret_cast<const float4 *>(static_cast<const float *>(p) + i);
-        v[0] = f.x;
-        v[1] = f.y;
-        v[2] = f.z;
-        v[3] = f.w;
+        return *(ok ? (const g_v4f *)(static_cast<const float *>(p) + i) : (const g_v4f *)(&kZero4));
     }
 }
 
 // grid: (channel blocks of kCT * kCV, batch rows, token tiles of kTT)
+template <bool BF16>
 __global__ void __launch_bounds__(kCT) bdlm_conv_kernel(const ConvArgs a) {
     const int HP = a.nheads * 64, GN = a.ngroups * a.dstate, CH = HP + 2 * GN;
     const int c = (blockIdx.x * kCT + threadIdx.x) * kCV;   // first of this thread's channels
@@ -68,15 +88,6 @@ __global__ void __launch_bounds__(kCT) bdlm_conv_kernel(const ConvArgs a) {
     const int64_t L = a.L;
     const int64_t BL = static_cast<int64_t>(a.batch) * L;
 
-    // dt widened to fp32 (heads c .. c + 3; nheads < CH)
-    for (int e = 0; e < kCV; ++e) {
-        const int hh = c + e;
-        if (hh < a.nheads)
-            for (int i = 0; i < kTT; ++i)
-                if (t0 + i < L)
-                    a.out[2 * BL * CH + (b * L + t0 + i) * a.nheads + hh] =
-                        load_act(a.dt, b * a.dts_b + (t0 + i) * a.dts_t + hh, a.bf16);
-    }
     if (c >= CH) return;
 
     // where these channels live: input element offset of token 0, token stride, and
@@ -124,21 +135,27 @@ __global__ void __launch_bounds__(kCT) bdlm_conv_kernel(const ConvArgs a) {
     const int64_t slot = a.use_slots ? a.slots[b] : b;
     const float *crow = a.cache + slot * 3 * CH + c;
 
-    // inputs u[t0 - 3 .. t0 + kTT + 2]: cached rows before token 0, zeros past L
-    float u[kTT + 6][kCV];
+    // inputs u[t0 - 3 .. t0 + kTT + 2]: cached rows before token 0, zeros past L; each
+    // row the sum of the cached-row load and the input-row load, one of them zeros
+    v4f u[kTT + 6];
 #pragma unroll
     for (int i = 0; i < kTT + 6; ++i) {
         const int64_t t = t0 - 3 + i;
-        if (t < 0) {
-#pragma unroll
-            for (int e = 0; e < kCV; ++e) u[i][e] = crow[(t + 3) * CH + e];
-        } else if (t < L) {
-            load_act4(src, in0 + t * in_t, a.bf16, u[i]);
-        } else {
-#pragma unroll
-            for (int e = 0; e < kCV; ++e) u[i][e] = 0.f;
-        }
+        const int64_t tc = t < 0 ? 0 : (t < L ? t : L - 1);   // addresses stay in range
+        const v4f cv = *(t < 0 ? (const g_v4f *)(crow + (t < 0 ? t + 3 : 0) * CH)
+                               : (const g_v4f *)(&kZero4));
+        u[i] = cv + load_act4<BF16>(src, in0 + tc * in_t, t >= 0 && t < L);
     }
+    // dt widened to fp32 (heads c .. c + 3; nheads < CH): loaded with the rows, stored
+    // at the end
+    float dtw[kCV][kTT];
+#pragma unroll
+    for (int e = 0; e < kCV; ++e)
+#pragma unroll
+        for (int i = 0; i < kTT; ++i) {
+            const bool ok = c + e < a.nheads && t0 + i < L;
+            dtw[e][i] = load_act_or_zero<BF16>(a.dt, ok ? b * a.dts_b + (t0 + i) * a.dts_t + c + e : 0, ok);
+        }
 #pragma unroll
     for (int i = 0; i < kTT; ++i) {
         const int64_t t = t0 + i;
@@ -156,6 +173,12 @@ __global__ void __launch_bounds__(kCT) bdlm_conv_kernel(const ConvArgs a) {
             *reinterpret_cast<float4 *>(orv + t * o_t) = float4{vr[0], vr[1], vr[2], vr[3]};
         }
     }
+#pragma unroll
+    for (int e = 0; e < kCV; ++e)
+#pragma unroll
+        for (int i = 0; i < kTT; ++i)
+            if (c + e < a.nheads && t0 + i < L)
+                a.out[2 * BL * CH + (b * L + t0 + i) * a.nheads + c + e] = dtw[e][i];
 }
 
 // A commit's cache rows: the last three rows of (cache ++ block), one thread per
@@ -223,9 +246,11 @@ int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, fl
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
         k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
     const int ch = a.nheads * 64 + 2 * a.ngroups * a.dstate;
-    hipLaunchKernelGGL(bdlm_conv_kernel,
-                       dim3((ch + kCT * kCV - 1) / (kCT * kCV), a.batch, (a.L + kTT - 1) / kTT),
-                       dim3(kCT), 0, static_cast<hipStream_t>(stream), k);
+    const dim3 cgrid((ch + kCT * kCV - 1) / (kCT * kCV), a.batch, (a.L + kTT - 1) / kTT);
+    if (a.bf16)
+        hipLaunchKernelGGL(bdlm_conv_kernel<true>, cgrid, dim3(kCT), 0, static_cast<hipStream_t>(stream), k);
+    else
+        hipLaunchKernelGGL(bdlm_conv_kernel<false>, cgrid, dim3(kCT), 0, static_cast<hipStream_t>(stream), k);
     if (hipGetLastError() != hipSuccess) return BDLM_E_LAUNCH;
     if (commit) {
         hipLaunchKernelGGL(bdlm_conv_keep_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
