@@ -26,9 +26,11 @@ struct LaunchArgs {
 int launch_block(const LaunchArgs &a, bool commit, void *stream);
 
 // A step (or commit) of a block of at most 64 tokens whose reverse branch has inputs of
-// its own: the forward branch of `fwd` from the cached state (skip fwd.D) stores y,
-// then the reverse branch of `rev` (skip rev.D_rev) adds onto it; a commit updates the
-// state from `fwd`.  want_y false (commit only): no outputs, no reverse launch.
+// its own: the forward branch of `fwd` from the cached state (skip fwd.D) plus the
+// reverse branch of `rev` (skip rev.D_rev) into y; a commit updates the state from
+// `fwd`.  A bf16 step of at most 32 tokens is one launch computing both branches;
+// otherwise the forward launch stores y and a reverse launch adds onto it.  want_y
+// false (commit only): no outputs, no reverse launch.
 int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
                       void *stream);
 

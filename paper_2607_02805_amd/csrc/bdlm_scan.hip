@@ -62,6 +62,9 @@ struct KArgs {
     const float *A, *D, *D_rev;
     float *h_pool;
     float *y;
+    // kSep: the reverse branch's own inputs (same shapes and strides as the above)
+    const void *x2, *dt2, *Bm2, *Cm2;
+    const float *A2;
     int64_t xs_b, xs_t, xs_h;
     int64_t dts_b, dts_t;
     int64_t bcs_b, bcs_t, bcs_g;
@@ -77,9 +80,12 @@ struct KArgs {
 // NS: dstate.  F32: fp32 activation storage.  COMMIT: also update the state.
 // DIR: kBoth computes both branches (one input set for both, Eq. partial-reverse);
 //     kFwd only the forward branch from the cached state (skip D) and stores y;
-//     kRev only the block-local reverse branch (skip D_rev) and adds it onto y.  A
-//     step whose branches have inputs of their own is a kFwd launch followed by a
-//     kRev launch on the same stream.
+//     kRev only the block-local reverse branch (skip D_rev) and adds it onto y;
+//     kSep both branches, each from an input set of its own (x, dt, A, B, C for the
+//     forward branch, x2, dt2, A2, B2, C2 for the reverse one; bf16 storage, no
+//     commit): two Gram matrices, two intra products, one prefix term.  A step whose
+//     branches have inputs of their own is one kSep launch, or a kFwd launch followed
+//     by a kRev launch on the same stream.
 // NPART: the state of a head is split over NPART groups of four waves along
 //     dstate (4 * NPART waves per workgroup).  Streaming the state from HBM needs
 //     many waves per CU, each with few loads in flight; the partial prefix
@@ -103,7 +109,7 @@ struct KArgs {
 //      dstate quads of the state (the only step that waits for the state loads);
 //      the partial products are summed and y is stored; a commit then adds the
 //      block to each wave's quads of the state in place.
-constexpr int kBoth = 0, kFwd = 1, kRev = 2;
+constexpr int kBoth = 0, kFwd = 1, kRev = 2, kSep = 3;
 
 // c += a b over one quad of 16 contraction indices on fp32 MFMA: instruction r takes
 // value r of every lane, i.e. index 4 grp + r of the quad layout.
@@ -113,11 +119,56 @@ __device__ __forceinline__ f32x4 mma_q32(f32x4 a, f32x4 b, f32x4 c) {
     return c;
 }
 
+// One 16 x 16 tile of the decay-weighted matrix M[t, j] = G[t, j] W[t, j] dt_j from bf16
+// operand images (rows t of token tile mt, columns j of token tile jt), held transposed
+// (lane (grp, col): j = 16 jt + 4 grp + r, t = 16 mt + col) and split into bf16 hi (xy)
+// and lo (zw).  WDIR selects the weights: kBoth both triangles and 2 on the diagonal,
+// kFwd the lower triangle, kRev the upper one (1 on the diagonal).
+template <int QN, int WDIR>
+__device__ __forceinline__ uint4 gram_tile_bf16(const uint2 *iB, const uint2 *iC, const float *dCs,
+                                                const float *dEx, const float *dDt, int mt, int jt,
+                                                int grp, int col) {
+    // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
+    f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < QN; q += 2) {   // two dstate quads per product
+        const int q1 = q + 1 < QN ? q + 1 : q;
+        const s16x4 b0 = as_s16x4(iB[img_idx<QN, false>(jt, q, grp, col)]);
+        const s16x4 b1 = as_s16x4(iB[img_idx<QN, false>(jt, q1, grp, col)]);
+        const s16x4 c0 = as_s16x4(iC[img_idx<QN, false>(mt, q, grp, col)]);
+        const s16x4 c1 = as_s16x4(iC[img_idx<QN, false>(mt, q1, grp, col)]);
+        if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
+        else gacc = mma_k16(b0, c0, gacc);
+    }
+    const int t = 16 * mt + col;
+    const float cst = dCs[t], ext = dEx[t];
+    const f32x4 csj = *reinterpret_cast<const f32x4 *>(&dCs[16 * jt + 4 * grp]);
+    const f32x4 exj = *reinterpret_cast<const f32x4 *>(&dEx[16 * jt + 4 * grp]);
+    const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&dDt[16 * jt + 4 * grp]);
+    f32x4 m;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        // below the diagonal the forward decay from j to t, above it the reverse decay
+        // a_t ... a_{j-1}; on it the token's own input, once per branch computed here
+        const int j = 16 * jt + 4 * grp + r;
+        const float e = exp2f(j < t ? cst - csj[r] : exj[r] - ext);
+        const float w = j == t ? (WDIR == kBoth ? 2.f : 1.f)
+                               : (j < t ? (WDIR == kRev ? 0.f : e) : (WDIR == kFwd ? 0.f : e));
+        m[r] = gacc[r] * w * dtj[r];
+    }
+    s16x4 mh, ml;
+    split4(m, mh, ml);
+    const uint2 a = as_u2(mh), c2 = as_u2(ml);
+    return uint4{a.x, a.y, c2.x, c2.y};
+}
+
 template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR>
 __global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
-    static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev, "direction");
+    static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep, "direction");
     static_assert(!(COMMIT && DIR == kRev), "a commit updates the forward state");
+    constexpr bool SEP = DIR == kSep;
+    static_assert(!(SEP && (F32 || COMMIT)), "separate inputs: bf16 storage, step only");
     constexpr int NT = 256 * NPART;       // threads
     constexpr int NW = 4 * NPART;         // waves
     constexpr int MT = LT / 16;           // token tiles = quads along the block
@@ -138,6 +189,11 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) float sDt[64], sCs[64], sEx[64];   // dt, cs, ex per token
     __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
+    // kSep: the reverse branch's images, x, decay sums and matrix
+    __shared__ __align__(16) uint2 sC2[SEP ? IMG : 1], sB2[SEP ? IMG : 1];
+    __shared__ __align__(16) AT sX2[SEP ? LT * XS : 1];
+    __shared__ __align__(16) float sDt2[SEP ? 64 : 1], sCs2[SEP ? 64 : 1], sEx2[SEP ? 64 : 1];
+    __shared__ __align__(16) uint4 sM2[SEP ? MT * MT * 64 : 1];
     __shared__ __align__(16) f32x4 sRed[(NPART > 1 ? NPART - 1 : 1) * 4 * MT * 64];
 
     const int tid = threadIdx.x;
@@ -197,6 +253,32 @@ bdlm_block_kernel(const KArgs args) {
                                                       : gzero());
         }
     }
+    u32x4 cch2[SEP ? BC_PT : 1], bch2[SEP ? BC_PT : 1], xch2[SEP ? X_PT : 1];
+    if constexpr (SEP) {
+        const AT *Bg2 = static_cast<const AT *>(args.Bm2) + b * args.bcs_b + g * args.bcs_g;
+        const AT *Cg2 = static_cast<const AT *>(args.Cm2) + b * args.bcs_b + g * args.bcs_g;
+        const AT *xg2 = static_cast<const AT *>(args.x2) + b * args.xs_b + h * args.xs_h;
+        if (bc_owner) {
+#pragma unroll
+            for (int k = 0; k < BC_PT; ++k) {
+                const int i = tid + NT * k;
+                const int t = i / CPR, c = i % CPR;
+                const int64_t o = t * args.bcs_t + c * E;
+                const bool ok = t < L;
+                cch2[k] = __builtin_nontemporal_load(ok ? gchunk(Cg2 + o) : gzero());
+                bch2[k] = __builtin_nontemporal_load(ok ? gchunk(Bg2 + o) : gzero());
+            }
+        }
+        if (x_owner) {
+#pragma unroll
+            for (int k = 0; k < X_PT; ++k) {
+                const int i = tid + NT * k;
+                const int j = i / (kP / E), c = i % (kP / E);
+                xch2[k] = __builtin_nontemporal_load(j < L ? gchunk(xg2 + j * args.xs_t + c * E)
+                                                           : gzero());
+            }
+        }
+    }
     // dt (lane t = token t), loaded by every wave though wave 0 alone stages it: where
     // a load under a branch joins the other path the compiler converts its value right
     // away, i.e. waits there for every load issued before it (the state loads of wave 0
@@ -204,12 +286,18 @@ bdlm_block_kernel(const KArgs args) {
     typedef __attribute__((address_space(1))) const AT g_at;
     const AT dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
                                 : (const g_at *)(&kZeroChunk));
+    AT dtraw2 = AT(0);
+    if constexpr (SEP) {
+        const AT *dtg2 = static_cast<const AT *>(args.dt2) + b * args.dts_b + h;
+        dtraw2 = *(lane < L ? (const g_at *)(dtg2 + lane * args.dts_t) : (const g_at *)(&kZeroChunk));
+    }
     // per-head parameters as vector loads in this first batch: a scalar load issued
     // later would queue behind the state loads of every workgroup
     typedef __attribute__((address_space(1))) const float g_f;
     float parv = 0.f;
     if (wave == 0) {
-        const float *par = tid == 0 ? args.A : (tid == 1 ? args.D : args.D_rev);
+        const float *par = tid == 0 ? args.A
+                                    : (tid == 1 ? args.D : (SEP && tid == 3 ? args.A2 : args.D_rev));
         parv = *(const g_f *)(par + h);
     }
     // keep the small loads above ahead of the state loads (loads return in order)
@@ -260,6 +348,31 @@ bdlm_block_kernel(const KArgs args) {
         dst[0] = uint2{v.x, v.y};
         dst[1] = uint2{v.z, v.w};
     }
+    if constexpr (SEP) {
+#pragma unroll
+        for (int k = 0; k < BC_PT; ++k) {
+            if (!bc_owner) break;
+            const int i = tid + NT * k;
+            const int t = i / CPR, c = i % CPR;
+            const u32x4 cz = cch2[k], bz = bch2[k];
+            const int at = img_idx<QN, false>(t >> 4, c >> 1, 2 * (c & 1), t & 15);
+            sC2[at] = uint2{cz.x, cz.y};
+            sC2[at + 16] = uint2{cz.z, cz.w};
+            sB2[at] = uint2{bz.x, bz.y};
+            sB2[at + 16] = uint2{bz.z, bz.w};
+        }
+#pragma unroll
+        for (int k = 0; k < X_PT; ++k) {
+            if (!x_owner) break;
+            const int i = tid + NT * k;
+            const int j = i / (kP / E), c = i % (kP / E);
+            const u32x4 v = xch2[k];
+            uint2 *dst = reinterpret_cast<uint2 *>(&sX2[j * XS + c * E]);
+            dst[0] = uint2{v.x, v.y};
+            dst[1] = uint2{v.z, v.w};
+        }
+        if (tid == 3) sPar[3] = parv;   // A of the reverse branch
+    }
     if (tid < 3) sPar[tid] = parv;
     if (wave == 0) {
         // decay sums of the block in base 2 (lane t = token t; padded tokens have dt = 0):
@@ -272,6 +385,16 @@ bdlm_block_kernel(const KArgs args) {
         sDt[lane] = dtv;
         sCs[lane] = cs;
         sEx[lane] = lane == 0 ? 0.f : up;
+        if constexpr (SEP) {   // the reverse branch's decay sums (its own dt and A)
+            const float dtv2 = Act<F32>::val(dtraw2);
+            const float Ar2 =
+                __int_as_float(__builtin_amdgcn_readlane(__float_as_int(parv), 3)) * kLog2e;
+            const float cs2 = wave_inclusive_sum(dtv2 * Ar2);
+            const float up2 = __shfl_up(cs2, 1, 64);
+            sDt2[lane] = dtv2;
+            sCs2[lane] = cs2;
+            sEx2[lane] = lane == 0 ? 0.f : up2;
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -279,50 +402,46 @@ bdlm_block_kernel(const KArgs args) {
 
     // ---- phase 2: Gram tiles (shared out)
 
-    for (int tile = wave; tile < MT * MT; tile += NW) {
-        const int mt = tile / MT, jt = tile % MT;
-        // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
-        f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (F32) {
+    if constexpr (SEP) {
+        // forward tiles from the first input set, reverse tiles from the second
+        for (int tile = wave; tile < 2 * MT * MT; tile += NW) {
+            const int tt = tile < MT * MT ? tile : tile - MT * MT;
+            const int mt = tt / MT, jt = tt % MT;
+            if (tile < MT * MT)
+                sM[tt * 64 + lane] = gram_tile_bf16<QN, kFwd>(sB, sC, sCs, sEx, sDt, mt, jt, grp, col);
+            else
+                sM2[tt * 64 + lane] = gram_tile_bf16<QN, kRev>(sB2, sC2, sCs2, sEx2, sDt2, mt, jt, grp, col);
+        }
+    } else if constexpr (!F32) {
+        for (int tile = wave; tile < MT * MT; tile += NW)
+            sM[tile * 64 + lane] =
+                gram_tile_bf16<QN, DIR>(sB, sC, sCs, sEx, sDt, tile / MT, tile % MT, grp, col);
+    } else {   // fp32 storage: fp32 MFMA, fp32 matrix
+        for (int tile = wave; tile < MT * MT; tile += NW) {
+            const int mt = tile / MT, jt = tile % MT;
+            // accumulator holds G[t, j] for t = 16mt + col, j = 16jt + 4grp + r
+            f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int q = 0; q < QN; ++q)
                 gacc = mma_q32(sBf[img_idx<QN, F32>(jt, q, grp, col)],
                                sCf[img_idx<QN, F32>(mt, q, grp, col)], gacc);
-        } else {
+            const int t = 16 * mt + col;
+            const float cst = sCs[t], ext = sEx[t];
+            const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
+            const f32x4 exj = *reinterpret_cast<const f32x4 *>(&sEx[16 * jt + 4 * grp]);
+            const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
+            f32x4 m;
 #pragma unroll
-            for (int q = 0; q < QN; q += 2) {   // two dstate quads per product
-                const int q1 = q + 1 < QN ? q + 1 : q;
-                const s16x4 b0 = as_s16x4(sB[img_idx<QN, F32>(jt, q, grp, col)]);
-                const s16x4 b1 = as_s16x4(sB[img_idx<QN, F32>(jt, q1, grp, col)]);
-                const s16x4 c0 = as_s16x4(sC[img_idx<QN, F32>(mt, q, grp, col)]);
-                const s16x4 c1 = as_s16x4(sC[img_idx<QN, F32>(mt, q1, grp, col)]);
-                if (q + 1 < QN) gacc = mma_k32(b0, b1, c0, c1, gacc);
-                else gacc = mma_k16(b0, c0, gacc);
+            for (int r = 0; r < 4; ++r) {
+                // below the diagonal the forward decay from j to t, above it the reverse decay
+                // a_t ... a_{j-1}; on it the token's own input, once per branch computed here
+                const int j = 16 * jt + 4 * grp + r;
+                const float e = exp2f(j < t ? cst - csj[r] : exj[r] - ext);
+                const float w = j == t ? (DIR == kBoth ? 2.f : 1.f)
+                                       : (j < t ? (DIR == kRev ? 0.f : e) : (DIR == kFwd ? 0.f : e));
+                m[r] = gacc[r] * w * dtj[r];
             }
-        }
-        const int t = 16 * mt + col;
-        const float cst = sCs[t], ext = sEx[t];
-        const f32x4 csj = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
-        const f32x4 exj = *reinterpret_cast<const f32x4 *>(&sEx[16 * jt + 4 * grp]);
-        const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&sDt[16 * jt + 4 * grp]);
-        f32x4 m;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            // below the diagonal the forward decay from j to t, above it the reverse decay
-            // a_t ... a_{j-1}; on it the token's own input, once per branch computed here
-            const int j = 16 * jt + 4 * grp + r;
-            const float e = exp2f(j < t ? cst - csj[r] : exj[r] - ext);
-            const float w = j == t ? (DIR == kBoth ? 2.f : 1.f)
-                                   : (j < t ? (DIR == kRev ? 0.f : e) : (DIR == kFwd ? 0.f : e));
-            m[r] = gacc[r] * w * dtj[r];
-        }
-        if constexpr (F32) {
             sM[tile * 64 + lane] = __builtin_bit_cast(uint4, m);
-        } else {
-            s16x4 mh, ml;
-            split4(m, mh, ml);
-            const uint2 a = as_u2(mh), c2 = as_u2(ml);
-            sM[tile * 64 + lane] = uint4{a.x, a.y, c2.x, c2.y};
         }
     }
     __syncthreads();
@@ -341,6 +460,17 @@ bdlm_block_kernel(const KArgs args) {
         }
     }
     auto xquad = [&](int jt) { return f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}; };
+    float xv2[SEP ? MT : 1][4];
+    s16x4 xq2[SEP ? MT : 1];
+    if constexpr (SEP) {
+#pragma unroll
+        for (int jt = 0; jt < MT; ++jt) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) xv2[jt][r] = Act<F32>::val(sX2[(16 * jt + 4 * grp + r) * XS + p]);
+            s16x4 lo;
+            split4(f32x4{xv2[jt][0], xv2[jt][1], xv2[jt][2], xv2[jt][3]}, xq2[jt], lo);
+        }
+    }
 
     float *yb = args.y;
     const bool want_y = !COMMIT || yb != nullptr;
@@ -350,7 +480,7 @@ bdlm_block_kernel(const KArgs args) {
         float pre[MT][4], es[MT][4];
         if (part == 0) {
             const float skip =
-                DIR == kBoth ? sPar[1] + sPar[2] : (DIR == kFwd ? sPar[1] : sPar[2]);
+                DIR == kBoth ? sPar[1] + sPar[2] : (DIR == kFwd || SEP ? sPar[1] : sPar[2]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 f32x4 ai = {0.f, 0.f, 0.f, 0.f};
@@ -369,6 +499,18 @@ bdlm_block_kernel(const KArgs args) {
                     }
                     ai = mma_quads<MT>(mh, xq, ai);
                     ai = mma_quads<MT>(ml, xq, ai);
+                    if constexpr (SEP) {   // + the reverse branch's intra product and skip
+#pragma unroll
+                        for (int jt = 0; jt < MT; ++jt) {
+                            const uint4 v = sM2[(mt * MT + jt) * 64 + lane];
+                            mh[jt] = as_s16x4(uint2{v.x, v.y});
+                            ml[jt] = as_s16x4(uint2{v.z, v.w});
+                        }
+                        ai = mma_quads<MT>(mh, xq2, ai);
+                        ai = mma_quads<MT>(ml, xq2, ai);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) ai[r] += sPar[2] * xv2[mt][r];
+                    }
                 }
                 const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs[16 * mt + 4 * grp]);
 #pragma unroll
@@ -602,6 +744,8 @@ KArgs kargs(const LaunchArgs &a) {
     k.D_rev = a.D_rev;
     k.h_pool = a.h_pool;
     k.y = a.y;
+    k.x2 = k.dt2 = k.Bm2 = k.Cm2 = nullptr;
+    k.A2 = nullptr;
     k.xs_b = a.xs_b;
     k.xs_t = a.xs_t;
     k.xs_h = a.xs_h;
@@ -656,6 +800,21 @@ int launch_block(const LaunchArgs &a, bool commit, void *stream) {
 int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
                       void *stream) {
     if (fwd.batch == 0 || fwd.L == 0) return BDLM_OK;
+    if (!commit && want_y && fwd.bf16 && fwd.L <= 32) {
+        // one launch: both branches, each from its own input set
+        KArgs k = kargs(fwd);
+        k.x2 = rev.x;
+        k.dt2 = rev.dt;
+        k.Bm2 = rev.Bm;
+        k.Cm2 = rev.Cm;
+        k.A2 = rev.A;
+        k.D_rev = rev.D_rev;
+        const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(fwd.batch) * fwd.nheads);
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        const hipError_t e = fwd.L <= 16 ? by_ns<16, false, false, kSep>(fwd.dstate, k, grid, s)
+                                         : by_ns<32, false, false, kSep>(fwd.dstate, k, grid, s);
+        return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+    }
     LaunchArgs f = fwd;
     if (!want_y) f.y = nullptr;
     int rc = launch_dir(f, kFwd, commit, stream);

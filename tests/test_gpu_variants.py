@@ -83,7 +83,11 @@ def sep_inputs(w, seed):
 
 
 @pytest.mark.parametrize("H,N,L,bf16", [(32, 128, 32, True), (4, 64, 256, True), (3, 16, 50, False),
-                                        (8, 128, 64, True)])
+                                        (8, 128, 64, True),
+                                        # one fused launch (bf16, L <= 32): 16-token tile,
+                                        # ragged lengths, every dstate
+                                        (8, 64, 13, True), (6, 16, 27, True), (4, 32, 16, True),
+                                        (5, 128, 1, True)])
 def test_step_separate_reverse_inputs(H, N, L, bf16):
     import paper_2607_02805_amd as bd
     w = bi.Workload("t", 2, H, 64, N, 1, L, 0, bf16, 1, 10200 + H + L)
@@ -100,6 +104,28 @@ def test_step_separate_reverse_inputs(H, N, L, bf16):
     e = rel_err(y, yf + yr)
     say("  rel err", e)
     assert e <= REL_TOL
+
+
+def test_step_separate_reverse_inputs_groups_and_slots():
+    """The fused separate-input launch with two groups and a slot map: rows read the
+    states of their slots, the pool is not written."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 3, 8, 64, 64, 2, 24, 0, True, 1, 10500)
+    fwd, rev = sep_inputs(w, 10510)
+    pool = bi.random_state(w, 5, 11, 0.5).astype(np.float64)
+    slots = np.array([4, 0, 2], dtype=np.int32)
+    vf, vr = to_dev(fwd), to_dev(rev)
+    h = pool_dev(pool)
+    before = from_pool(h).copy()
+    say("separate reverse inputs, groups and slots", dict(H=8, N=64, G=2, L=24))
+    y = bd.scan_block_step_sep((vf["x"], vf["dt"], vf["A"], vf["B"], vf["C"], vf["D"]),
+                               (vr["x"], vr["dt"], vr["A"], vr["B"], vr["C"], vr["D_rev"]),
+                               h, slot_idx=slots)
+    torch.cuda.synchronize()
+    _, yf, _ = oracle.block_step(fwd, pool[slots], parts=True)
+    _, _, yr = oracle.block_step(rev, np.zeros_like(pool[slots]), parts=True)
+    assert rel_err(y, yf + yr) <= REL_TOL
+    np.testing.assert_array_equal(from_pool(h), before)
 
 
 def test_step_separate_with_shared_inputs_equals_step():
