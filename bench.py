@@ -39,8 +39,8 @@ HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_02805_amd", "csrc", f)
                for f in ("bdlm_scan.hip", "bdlm_device.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_block_step_350m_b16_L32.md")
-STEP_KERNEL = "bdlm_block_kernel<32, 128, false, false, 2, 0>"
-COMMIT_KERNEL = "bdlm_block_kernel<32, 128, false, true, 2, 0>"
+STEP_KERNEL = "bdlm_block_kernel<32, 128, false, false, 2, 0, false>"
+COMMIT_KERNEL = "bdlm_block_kernel<32, 128, false, true, 2, 0, false>"
 
 
 def step_bytes(batch, H, P, N, G, L, in_bytes=2):

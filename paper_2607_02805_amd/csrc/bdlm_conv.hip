@@ -246,6 +246,15 @@ int launch_conv_block(const LaunchArgs &a, const float *w, const float *bias, fl
     for (int i = 0; i < BDLM_MAX_SLOT_ROWS; ++i)
         k.slots[i] = (a.slots && i < a.batch) ? a.slots[i] : 0;
     const int ch = a.nheads * 64 + 2 * a.ngroups * a.dstate;
+    if (a.bf16 && a.L <= 32) {
+        // bf16 blocks of at most 32 tokens: the block kernels convolve while staging (no
+        // workspace); a commit's cache rows are replaced once both launches have read them
+        const int rc = launch_conv_fused(a, w, bias, conv_pool, commit, a.y != nullptr, stream);
+        if (rc != BDLM_OK || !commit) return rc;
+        hipLaunchKernelGGL(bdlm_conv_keep_kernel, dim3((ch + 255) / 256, a.batch), dim3(256), 0,
+                           static_cast<hipStream_t>(stream), k);
+        return hipGetLastError() == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+    }
     const dim3 cgrid((ch + kCT * kCV - 1) / (kCT * kCV), a.batch, (a.L + kTT - 1) / kTT);
     if (a.bf16)
         hipLaunchKernelGGL(bdlm_conv_kernel<true>, cgrid, dim3(kCT), 0, static_cast<hipStream_t>(stream), k);

@@ -34,6 +34,16 @@ int launch_block(const LaunchArgs &a, bool commit, void *stream);
 int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
                       void *stream);
 
+// A step (or commit) of a block of at most 32 tokens with the convolution part of the
+// boundary state, bf16 inputs before the convolution: the convolution runs while each
+// launch stages its inputs (forward launch from the cached rows conv_pool, then the
+// reverse launch zero-padded past the block), with no workspace.  The forward launch
+// stores y (none when want_y is false) and a commit updates the state; the reverse
+// launch adds onto y.  conv_pool is only read: a commit's new cache rows are written
+// by the caller afterwards.
+int launch_conv_fused(const LaunchArgs &a, const float *w, const float *bias, const float *conv_pool,
+                      bool commit, bool want_y, void *stream);
+
 // How the sequence kernels cut T tokens into segments (one workgroup per batch row,
 // head and segment) and the device workspace they need: per (row, head, segment)
 // `dirs` states of 64 x dstate fp32, then one fp32 log-decay, rounded up to 256

@@ -72,6 +72,11 @@ struct KArgs {
     int32_t xcd_remap;   // 1: group consecutive units per XCD (grid % 8 == 0)
     int32_t use_slots;
     int32_t slots[BDLM_MAX_SLOT_ROWS];
+    // convolution staging: x, B, C are the block's bf16 inputs before the mixer's
+    // width-4 depthwise convolution; weights [channels][4], bias [channels], cached
+    // last three input rows [slot][3][channels] (fp32)
+    const float *conv_w, *conv_b, *conv_pool;
+    int32_t conv_ch;
 };
 
 // ------------------------------------------------------------------- the kernel
@@ -162,10 +167,14 @@ __device__ __forceinline__ uint4 gram_tile_bf16(const uint2 *iB, const uint2 *iC
     return uint4{a.x, a.y, c2.x, c2.y};
 }
 
-template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR>
+// CV: the block's x, B and C are convolved while they are staged (bf16 inputs before
+// the mixer's convolution, fp32 operands after it; forward: the convolution continues
+// from the cached rows, reverse: zero past the block's end).
+template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR, bool CV>
 __global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
     static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep, "direction");
+    static_assert(!CV || (F32 && (DIR == kFwd || DIR == kRev) && LT <= 32), "convolution staging");
     static_assert(!(COMMIT && DIR == kRev), "a commit updates the forward state");
     constexpr bool SEP = DIR == kSep;
     static_assert(!(SEP && (F32 || COMMIT)), "separate inputs: bf16 storage, step only");
@@ -186,6 +195,7 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) uint2 sC[F32 ? 1 : IMG], sB[F32 ? 1 : IMG];
     __shared__ __align__(16) f32x4 sCf[F32 ? IMG : 1], sBf[F32 ? IMG : 1];
     __shared__ __align__(16) AT sX[LT * XS];
+    using DT = typename Act<F32 && !CV>::T;   // dt storage (bf16 under convolution staging)
     __shared__ __align__(16) float sDt[64], sCs[64], sEx[64];   // dt, cs, ex per token
     __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
@@ -215,7 +225,7 @@ bdlm_block_kernel(const KArgs args) {
     const int q0 = part * QW;             // first dstate quad of this wave
 
     const AT *xg = static_cast<const AT *>(args.x) + b * args.xs_b + h * args.xs_h;
-    const AT *dtg = static_cast<const AT *>(args.dt) + b * args.dts_b + h;
+    const DT *dtg = static_cast<const DT *>(args.dt) + b * args.dts_b + h;
     const AT *Bg = static_cast<const AT *>(args.Bm) + b * args.bcs_b + g * args.bcs_g;
     const AT *Cg = static_cast<const AT *>(args.Cm) + b * args.bcs_b + g * args.bcs_g;
     // this lane's quads of the state: s[p, 16q + 4grp + r] at hs + q * 1024
@@ -229,7 +239,7 @@ bdlm_block_kernel(const KArgs args) {
     constexpr int BC_PT = BC_CH >= NT ? BC_CH / NT : 1;
     const bool bc_owner = tid < BC_CH;
     u32x4 cch[BC_PT], bch[BC_PT];
-    if (bc_owner) {
+    if (!CV && bc_owner) {
 #pragma unroll
         for (int k = 0; k < BC_PT; ++k) {
             const int i = tid + NT * k;                    // chunk fastest (coalesced)
@@ -244,7 +254,7 @@ bdlm_block_kernel(const KArgs args) {
     constexpr int X_PT = X_CH >= NT ? X_CH / NT : 1;
     const bool x_owner = tid < X_CH;
     u32x4 xch[X_PT];
-    if (x_owner) {
+    if (!CV && x_owner) {
 #pragma unroll
         for (int k = 0; k < X_PT; ++k) {
             const int i = tid + NT * k;                    // chunk fastest (coalesced)
@@ -284,8 +294,9 @@ bdlm_block_kernel(const KArgs args) {
     // away, i.e. waits there for every load issued before it (the state loads of wave 0
     // would then leave only after all of its inputs had arrived)
     typedef __attribute__((address_space(1))) const AT g_at;
-    const AT dtraw = *(lane < L ? (const g_at *)(dtg + lane * args.dts_t)
-                                : (const g_at *)(&kZeroChunk));
+    typedef __attribute__((address_space(1))) const DT g_dt;
+    const DT dtraw = *(lane < L ? (const g_dt *)(dtg + lane * args.dts_t)
+                                : (const g_dt *)(&kZeroChunk));
     AT dtraw2 = AT(0);
     if constexpr (SEP) {
         const AT *dtg2 = static_cast<const AT *>(args.dt2) + b * args.dts_b + h;
@@ -299,6 +310,49 @@ bdlm_block_kernel(const KArgs args) {
         const float *par = tid == 0 ? args.A
                                     : (tid == 1 ? args.D : (SEP && tid == 3 ? args.A2 : args.D_rev));
         parv = *(const g_f *)(par + h);
+    }
+    // Convolution staging: task (matrix, channel quad, 8-token group) loads the 11 input
+    // rows its 8 outputs need (each row the sum of a cached-row load and an input-row
+    // load, the one that does not apply reading a zero chunk), the 4 channels' weights
+    // and biases.
+    constexpr int CQX = kP / 4, CQB = NS / 4, TG = LT / 8;
+    constexpr int CV_TASKS = (CQX + 2 * CQB) * TG;
+    static_assert(!CV || CV_TASKS <= NT, "one convolution task per thread");
+    f32x4 cu[CV ? 11 : 1], cw[CV ? 4 : 1], cb = {0.f, 0.f, 0.f, 0.f};
+    int cv_m = 0, cv_q = 0, cv_t0 = 0;   // matrix (0 x, 1 B, 2 C), channel quad, first token
+    if constexpr (CV) {
+        typedef unsigned v2u __attribute__((ext_vector_type(2)));
+        typedef __attribute__((address_space(1))) const f32x4 g_f4;
+        typedef __attribute__((address_space(1))) const v2u g_u2;
+        const int task = tid < CV_TASKS ? tid : 0;   // threads past the tasks repeat task 0
+        const int per_tg = CQX + 2 * CQB;
+        cv_t0 = 8 * (task / per_tg);
+        const int r = task % per_tg;
+        cv_m = r < CQX ? 0 : (r < CQX + CQB ? 1 : 2);
+        cv_q = r < CQX ? r : (r < CQX + CQB ? r - CQX : r - CQX - CQB);
+        const int HP = args.nheads * kP, GN = (args.nheads / args.heads_per_group) * NS;
+        const int c = cv_m == 0 ? h * kP + 4 * cv_q : HP + (cv_m - 1) * GN + g * NS + 4 * cv_q;
+        const uint16_t *src = static_cast<const uint16_t *>(cv_m == 0 ? args.x : (cv_m == 1 ? args.Bm : args.Cm)) +
+                              b * (cv_m == 0 ? args.xs_b : args.bcs_b) +
+                              (cv_m == 0 ? h * args.xs_h : g * args.bcs_g) + 4 * cv_q;
+        const int64_t rs = cv_m == 0 ? args.xs_t : args.bcs_t;
+        const float *crow = args.conv_pool + slot * 3 * static_cast<int64_t>(args.conv_ch) + c;
+#pragma unroll
+        for (int i = 0; i < 11; ++i) {
+            // forward rows t0-3 .. t0+7 (before the block: the cache), reverse t0 .. t0+10
+            const int rr = DIR == kFwd ? cv_t0 - 3 + i : cv_t0 + i;
+            const bool in_blk = rr >= 0 && rr < L;
+            const v2u u = *(in_blk ? (const g_u2 *)(src + rr * rs) : (const g_u2 *)(&kZeroChunk));
+            f32x4 v = f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                            __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+            if constexpr (DIR == kFwd)
+                v += *(rr < 0 ? (const g_f4 *)(crow + (rr < 0 ? rr + 3 : 0) * args.conv_ch)
+                              : (const g_f4 *)(&kZeroChunk));
+            cu[i] = v;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cw[e] = *(const g_f4 *)(args.conv_w + 4 * static_cast<int64_t>(c + e));
+        cb = *(const g_f4 *)(args.conv_b + c);
     }
     // keep the small loads above ahead of the state loads (loads return in order)
     __builtin_amdgcn_sched_barrier(0);
@@ -318,9 +372,38 @@ bdlm_block_kernel(const KArgs args) {
     for (int k = 0; k < QE; ++k) load_state(k);
 
     // ---- phase 1: LDS images
+    if constexpr (CV) {
+        if (tid < CV_TASKS) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int t = cv_t0 + i;
+                f32x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    // forward: w0 u[t-3] + ... + w3 u[t]; reverse: w0 u[t+3] + ... + w3 u[t]
+                    float a = cb[e];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) a += cw[e][k] * cu[DIR == kFwd ? i + k : i + 3 - k][e];
+                    // SiLU a / (1 + e^-a) on the hardware exp2 and reciprocal (each within
+                    // a few ulp; the B and C channels are convolved by every head's
+                    // workgroup, so this runs 5x more often than one pass over the
+                    // channels); padded rows stay zero
+                    const float sg = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-a * kLog2e));
+                    o[e] = t < L ? a * sg : 0.f;
+                }
+                if (cv_m == 0) {
+                    *reinterpret_cast<f32x4 *>(&sX[t * XS + 4 * cv_q]) = o;
+                } else {
+                    const int at = img_idx<QN, true>(t >> 4, cv_q >> 2, cv_q & 3, t & 15);
+                    if (cv_m == 1) sBf[at] = o;
+                    else sCf[at] = o;
+                }
+            }
+        }
+    }
 #pragma unroll
     for (int k = 0; k < BC_PT; ++k) {
-        if (!bc_owner) break;
+        if (CV || !bc_owner) break;
         const int i = tid + NT * k;
         const int t = i / CPR, c = i % CPR;
         const u32x4 cz = cch[k], bz = bch[k];
@@ -340,7 +423,7 @@ bdlm_block_kernel(const KArgs args) {
     }
 #pragma unroll
     for (int k = 0; k < X_PT; ++k) {
-        if (!x_owner) break;
+        if (CV || !x_owner) break;
         const int i = tid + NT * k;
         const int j = i / (kP / E), c = i % (kP / E);
         const u32x4 v = xch[k];
@@ -377,7 +460,7 @@ bdlm_block_kernel(const KArgs args) {
     if (wave == 0) {
         // decay sums of the block in base 2 (lane t = token t; padded tokens have dt = 0):
         // cs_t = l_0 + ... + l_t with l_t = dt_t A_h, and ex_t = cs_{t-1} (ex_0 = 0)
-        const float dtv = Act<F32>::val(dtraw);
+        const float dtv = Act<F32 && !CV>::val(dtraw);
         const float A2 =
             __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(parv))) * kLog2e;
         const float cs = wave_inclusive_sum(dtv * A2);
@@ -710,7 +793,7 @@ constexpr int nparts() {
 template <int LT, int NS, bool F32, bool COMMIT, int DIR>
 hipError_t launch_t(const KArgs &k, unsigned grid, hipStream_t s) {
     constexpr int NP = nparts<LT, NS>();
-    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT, NP, DIR>), dim3(grid),
+    hipLaunchKernelGGL((bdlm_block_kernel<LT, NS, F32, COMMIT, NP, DIR, false>), dim3(grid),
                        dim3(256 * NP), 0, s, k);
     return hipGetLastError();
 }
@@ -746,6 +829,8 @@ KArgs kargs(const LaunchArgs &a) {
     k.y = a.y;
     k.x2 = k.dt2 = k.Bm2 = k.Cm2 = nullptr;
     k.A2 = nullptr;
+    k.conv_w = k.conv_b = k.conv_pool = nullptr;
+    k.conv_ch = 0;
     k.xs_b = a.xs_b;
     k.xs_t = a.xs_t;
     k.xs_h = a.xs_h;
@@ -820,6 +905,48 @@ int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit,
     int rc = launch_dir(f, kFwd, commit, stream);
     if (rc != BDLM_OK || !want_y) return rc;
     return launch_dir(rev, kRev, false, stream);
+}
+
+template <int LT, bool COMMIT, int DIR>
+hipError_t conv_by_ns(int ns, const KArgs &k, unsigned grid, hipStream_t s) {
+    switch (ns) {
+#define BDLM_CONV_NS(N)                                                                          \
+    case N: {                                                                                    \
+        constexpr int NP = nparts<LT, N>();                                                      \
+        hipLaunchKernelGGL((bdlm_block_kernel<LT, N, true, COMMIT, NP, DIR, true>), dim3(grid),   \
+                           dim3(256 * NP), 0, s, k);                                             \
+        return hipGetLastError();                                                                \
+    }
+        BDLM_CONV_NS(16)
+        BDLM_CONV_NS(32)
+        BDLM_CONV_NS(64)
+        BDLM_CONV_NS(128)
+#undef BDLM_CONV_NS
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int launch_conv_fused(const LaunchArgs &a, const float *w, const float *bias, const float *conv_pool,
+                      bool commit, bool want_y, void *stream) {
+    if (a.batch == 0 || a.L == 0) return BDLM_OK;
+    KArgs k = kargs(a);
+    k.conv_w = w;
+    k.conv_b = bias;
+    k.conv_pool = conv_pool;
+    k.conv_ch = a.nheads * kP + 2 * a.ngroups * a.dstate;
+    const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    KArgs f = k;
+    if (!want_y) f.y = nullptr;
+    hipError_t e;
+    if (a.L <= 16)
+        e = commit ? conv_by_ns<16, true, kFwd>(a.dstate, f, grid, s) : conv_by_ns<16, false, kFwd>(a.dstate, f, grid, s);
+    else
+        e = commit ? conv_by_ns<32, true, kFwd>(a.dstate, f, grid, s) : conv_by_ns<32, false, kFwd>(a.dstate, f, grid, s);
+    if (e != hipSuccess) return BDLM_E_LAUNCH;
+    if (!want_y) return BDLM_OK;
+    e = a.L <= 16 ? conv_by_ns<16, false, kRev>(a.dstate, k, grid, s) : conv_by_ns<32, false, kRev>(a.dstate, k, grid, s);
+    return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
 }
 
 int launch_state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
