@@ -45,11 +45,16 @@ def oracle_step(d, cw, cb, cache, pool, slots):
     return yf + yr, fin
 
 
-@pytest.mark.parametrize("H,N,L,bf16", [(4, 16, 1, True), (4, 64, 2, True), (32, 128, 32, True),
-                                        (8, 128, 64, False), (4, 32, 256, True), (3, 64, 17, False)])
-def test_conv_step(H, N, L, bf16):
+@pytest.mark.parametrize("H,N,L,bf16,G", [(4, 16, 1, True, 1), (4, 64, 2, True, 1), (32, 128, 32, True, 1),
+                                          (8, 128, 64, False, 1), (4, 32, 256, True, 1),
+                                          (3, 64, 17, False, 1),
+                                          # convolution inside the block kernel's staging
+                                          # (bf16, L <= 32): ragged tiles, two groups
+                                          (6, 32, 27, True, 1), (5, 128, 9, True, 1),
+                                          (8, 64, 24, True, 2)])
+def test_conv_step(H, N, L, bf16, G):
     import paper_2607_02805_amd as bd
-    w = bi.Workload("t", 3, H, 64, N, 1, L, 0, bf16, 1, 11000 + H + N + L)
+    w = bi.Workload("t", 3, H, 64, N, G, L, 0, bf16, 1, 11000 + H + N + L)
     d = bi.block_inputs(w, 0)
     d["D_rev"] = (d["D"] * 0.5).astype(np.float32)
     cw, cb = conv_params(w, 11100 + L)
@@ -59,7 +64,7 @@ def test_conv_step(H, N, L, bf16):
     slots = [3, 0, 3]
     y_ref, _ = oracle_step(d, cw, cb, cache.astype(np.float64), pool, slots)
     v = to_dev(d)
-    say("conv step", dict(H=H, N=N, L=L, bf16=bf16))
+    say("conv step", dict(H=H, N=N, L=L, bf16=bf16, G=G))
     y = bd.conv_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"],
                            torch.from_numpy(cw).to(DEV), torch.from_numpy(cb).to(DEV),
                            torch.from_numpy(cache).to(DEV), pool_dev(pool), slot_idx=slots)
