@@ -318,6 +318,10 @@ def run_contrast(args, block: dict) -> dict:
                                  "block_restricted": None if t_seq_block is None
                                  else round(t_seq_block * 1e6, 4)},
         "ratio": None if t_seq_block is None else round(t_seq_full / t_seq_block, 1),
+        # the same ratio against a full window that moved only its algorithmic bytes at the
+        # HBM peak: a lower bound on the contrast that no full-window kernel can beat
+        "ratio_vs_full_window_hbm_floor": None if t_seq_block is None
+        else round(fb / (HBM_PEAK_GBS * 1e9) / w.batch / t_seq_block, 1),
     }
 
 
@@ -524,6 +528,42 @@ def run_variants(args) -> dict:
         "step_plus_norm_us": round(t_sn * 1e6, 2)}
     del ys, zs, outs, pools
     torch.cuda.empty_cache()
+    return out
+
+
+def run_batch_sweep(args, batches=(16, 32, 64, 128), nl=24) -> dict:
+    """The block step at the 350M layer shape (L 32) at several batch sizes, each layer of
+    a ring with its own state, inputs and outputs (cold reads), beside a plain device copy
+    of the same byte count: how far the step's bandwidth is set by its launch size."""
+    import dataclasses
+
+    import torch
+
+    import bdlm_inputs as bi
+    import paper_2607_02805_amd as bd
+    dev = "cuda:0"
+    out = {"batch": list(batches), "step_us": [], "step_gbs": [], "frac": [], "copy_us": [],
+           "copy_gbs": []}
+    for b in batches:
+        w = dataclasses.replace(bi.WORKLOADS[3], batch=b)
+        base = to_dev(bi.block_inputs(w, 0), dev)
+        lay = [{k: v.clone() for k, v in base.items()} for _ in range(nl)]
+        pools = [torch.randn(bd.pool_shape(b, 32, 128), device=dev) for _ in range(nl)]
+        ys = [torch.empty((b, 32, 32, 64), device=dev) for _ in range(nl)]
+        t = _graph_time(lambda li: bd.scan_block_step(
+            lay[li]["x"], lay[li]["dt"], lay[li]["A"], lay[li]["B"], lay[li]["C"], lay[li]["D"],
+            lay[li]["D_rev"], pools[li], y=ys[li]), nl, reps=20)
+        del base, lay, pools, ys
+        torch.cuda.empty_cache()
+        sb = step_bytes(b, 32, 64, 128, 1, 32)
+        cp = run_copy_reference(sb)
+        out["step_us"].append(round(t * 1e6, 3))
+        out["step_gbs"].append(round(sb / t / 1e9, 1))
+        out["frac"].append(round(sb / t / 1e9 / HBM_PEAK_GBS, 4))
+        out["copy_us"].append(cp["us_per_launch"])
+        out["copy_gbs"].append(cp["gbs"])
+        print(f"[bench] batch {b}: step {t * 1e6:.2f} us ({sb / t / 1e9:.0f} GB/s), "
+              f"copy of the same bytes {cp['us_per_launch']:.2f} us", flush=True)
     return out
 
 
@@ -843,6 +883,7 @@ def main():
         extras["prefill"] = run_prefill(args)
         extras["all_block"] = run_all_block(args)
         extras["variants"] = run_variants(args)
+        extras["batch_sweep"] = run_batch_sweep(args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, args.cpu_budget)
     s = r["shape"]
     line = {
