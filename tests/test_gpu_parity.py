@@ -3,6 +3,7 @@ same seeded bytes.  Bar: max relative error 2e-3 on y and on committed states (t
 error measure is in tests/gpu_util.py); bookkeeping (tokens and blocks committed
 per slot) bit-exact; outputs deterministic bit for bit.
 """
+import dataclasses
 import sys
 
 import numpy as np
@@ -97,6 +98,12 @@ def test_350m_layer_other_block_lengths(L):
     check_step(w)
 
 
+def test_350m_layer_batch_128():
+    """The 350M layer shape at batch 128: 4,096 workgroups over the remapped grid (the
+    largest launch the bench's batch sweep times), every element against the oracle."""
+    check_step(dataclasses.replace(bi.WORKLOADS[3], batch=128))
+
+
 # ------------------------------------------------------------- shapes and edges
 @pytest.mark.parametrize("N", [16, 32, 64, 128])
 @pytest.mark.parametrize("L", [1, 5, 16, 17, 31, 33, 47, 64])
@@ -117,6 +124,14 @@ def test_groups():
 def test_slot_mapping_with_repeats():
     w = wl(5, 8, 64, 32, seed=7400)
     check_step(w, nslots=9, slot_idx=[8, 0, 3, 3, 7])
+
+
+def test_slot_mapping_at_max_rows():
+    """A slot map over the largest batch it accepts, rows drawn with repeats from a
+    larger pool."""
+    w = wl(256, 4, 16, 16, seed=7410)
+    slots = np.random.default_rng(7411).integers(0, 300, size=256).tolist()
+    check_step(w, nslots=300, slot_idx=slots)
 
 
 def test_strided_views():
