@@ -93,12 +93,19 @@ def lib():
         for f in ("bdlm_oracle_block_step", "bdlm_oracle_commit", "bdlm_oracle_scan_forward",
                   "bdlm_oracle_full_window", "bdlm_oracle_num_threads"):
             getattr(L, f).restype = ctypes.c_int
+        L.bdlm_oracle_set_num_threads.argtypes = [ctypes.c_int]
+        L.bdlm_oracle_set_num_threads.restype = None
         _lib = L
     return _lib
 
 
 def num_threads() -> int:
     return int(lib().bdlm_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Thread count of the oracle's loops over (batch, head) (timing only)."""
+    lib().bdlm_oracle_set_num_threads(ctypes.c_int(int(n)))
 
 
 # ---------------------------------------------------------------- marshalling

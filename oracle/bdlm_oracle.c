@@ -416,3 +416,14 @@ int bdlm_oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Thread count of the OpenMP loops over (batch, head) from now on; n <= 0 changes
+ * nothing.  Timing only: every result is the same at any thread count. */
+void bdlm_oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
