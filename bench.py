@@ -531,7 +531,7 @@ def run_variants(args) -> dict:
     return out
 
 
-def run_warm(args, reps: int = 200) -> dict:
+def run_warm(args, nodes: int = 32, reps: int = 20) -> dict:
     """The block step of one layer replayed back to back: its 16.8 MB state and its
     inputs stay resident in the Infinity Cache between launches.  Context for the cold
     figure (every read from HBM), which is the one reported."""
@@ -544,8 +544,10 @@ def run_warm(args, reps: int = 200) -> dict:
     d = to_dev(bi.block_inputs(w, 0), dev)
     pool = torch.randn(bd.pool_shape(w.batch, w.nheads, w.dstate), device=dev)
     y = torch.empty((w.batch, w.block_len, w.nheads, w.headdim), device=dev)
+    # one graph of `nodes` steps of the same layer (a graph of one node would time the
+    # graph launch, not the step)
     t = _graph_time(lambda li: bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"],
-                                                  d["D_rev"], pool, y=y), 1, reps=reps)
+                                                  d["D_rev"], pool, y=y), nodes, reps=reps)
     del d, pool, y
     torch.cuda.empty_cache()
     sb = step_bytes(w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, w.block_len)
