@@ -184,7 +184,8 @@ int bdlm_prefill_workspace(const bdlm_desc_t *desc, int64_t *bytes);
  * C) from the cached state with skip D, the reverse branch on (x_rev, dt_rev, A_rev,
  * B_rev, C_rev) from zero with skip D_rev, and y is their sum.  Both input sets share
  * desc's shapes and strides; everything else as bdlm_scan_block_step (any block
- * length; two launches: forward, then reverse adding into y).
+ * length; bf16 blocks of up to 32 tokens in one launch, otherwise two: forward, then
+ * reverse adding into y).
  * Errors: as bdlm_scan_block_step.
  */
 int bdlm_scan_block_step_sep(const bdlm_desc_t *desc, const void *x, const void *dt,
@@ -212,9 +213,12 @@ int bdlm_scan_block_step_sep(const bdlm_desc_t *desc, const void *x, const void 
  * conv_w       device fp32 [channels][4], 16-byte aligned; conv_b fp32 [channels].
  * conv_pool    device fp32 [nslots][3][channels] (same slots as h_pool).
  * workspace    at least bdlm_conv_workspace bytes (the convolved inputs, fp32),
- *              256-byte aligned.
- * Any block length; two or three launches.  Errors: as bdlm_scan_block_step /
- * bdlm_commit_boundary, and BDLM_E_WORKSPACE.
+ *              256-byte aligned; bf16 blocks of up to 32 tokens convolve inside
+ *              the scan kernel's staging and leave it untouched.
+ * Any block length.  Launches: a forward and a reverse scan launch, preceded by a
+ * convolution launch into the workspace unless the block convolves in the staging;
+ * a commit adds one launch that replaces the cached rows.  Errors: as
+ * bdlm_scan_block_step / bdlm_commit_boundary, and BDLM_E_WORKSPACE.
  */
 int bdlm_conv_workspace(const bdlm_desc_t *desc, int64_t *bytes);
 int bdlm_conv_block_step(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
