@@ -1,0 +1,55 @@
+"""Host-side parts of bench.py: the one-GPU contract, the algorithmic byte counts the
+roofline divides by, and the profile summaries (no GPU needed)."""
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_algorithmic_bytes_at_the_350m_layer_shape():
+    # state 16 x 32 x 64 x 128 fp32, x 16 x 32 x 32 x 64 bf16, dt 16 x 32 x 32 bf16,
+    # B and C 2 x 16 x 32 x 128 bf16, y 16 x 32 x 32 x 64 fp32, A / D / D_rev 3 x 32 fp32
+    state, x, dt, bc, y, par = 16777216, 2097152, 32768, 262144, 4194304, 384
+    assert bench.step_bytes(16, 32, 64, 128, 1, 32) == state + x + dt + bc + y + par == 23363968
+    assert bench.commit_bytes(16, 32, 64, 128, 1, 32) == 23363968 + state == 40141184
+    # the full window reads its inputs and writes y once, and has no state
+    assert bench.full_window_bytes(4, 32, 64, 128, 1, 65536) == 3372220800
+    # bytes grow with the block's tokens only, never with the prefix
+    assert (bench.step_bytes(16, 32, 64, 128, 1, 64) - bench.step_bytes(16, 32, 64, 128, 1, 32)
+            == x + dt + bc + y)
+
+
+def test_dispatch_summary_groups_by_kernel_and_shape(tmp_path):
+    p = tmp_path / "trace.csv"
+    rows = ["Kernel_Name,Grid_Size_X,Workgroup_Size_X,Start_Timestamp,End_Timestamp"]
+    for i, (grid, dur) in enumerate([(262144, 6000), (262144, 7000), (262144, 8000),
+                                     (2097152, 40000)]):
+        rows.append(f"\"void bdlm::(anonymous namespace)::bdlm_k<32, 128>(x)\",{grid},512,"
+                    f"{1000 * i},{1000 * i + dur}")
+    rows.append("\"elementwise_other\",1024,256,0,5000")
+    p.write_text("\n".join(rows) + "\n")
+    table = bench.summarize_dispatches(str(p)).splitlines()
+    assert len(table) == 4                       # header, rule, one row per launch shape
+    assert "| 4096 x 512 | 1 | 40.00 | 40.00 | 40.00 |" in table[2]
+    assert "| 512 x 512 | 3 | 7.00 | 7.00 | 6.00 |" in table[3]
+    assert not any("elementwise_other" in t for t in table)
+
+
+def test_traffic_is_dropped_once_the_kernel_source_changes(monkeypatch):
+    good = bench.kernel_source_sha()
+    value = bench.measured_traffic()
+    if value is not None:                          # summary taken on the current source
+        assert value > bench.step_bytes(16, 32, 64, 128, 1, 32) * 0.9
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda: "0" * 16 if good != "0" * 16 else "1" * 16)
+    assert bench.measured_traffic() is None
