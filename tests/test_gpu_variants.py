@@ -73,6 +73,37 @@ def test_long_block_commit(H, N, L, want_y):
         assert rel_err(out, y_ref) <= REL_TOL
 
 
+def test_paper_geometry_full_size():
+    """The paper's 350M geometry at the size the bench times it (batch 16, 26 heads,
+    dstate 128, 256-token blocks, identity slots: 416 workgroups per launch): the step,
+    then the commit with the clean-block outputs, every element against the oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("350m-paper-geometry", 16, 26, 64, 128, 1, 256, 0, True, 1, 6000)
+    d, c = bi.block_inputs(w, 0), bi.commit_inputs(w)
+    pool = bi.random_state(w, 16, 7, 0.5).astype(np.float64)
+    h = pool_dev(pool)
+    v = to_dev(d)
+    say("paper geometry step", w)
+    y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], h)
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.block_step(d, pool))
+    say("  rel err", e)
+    assert e <= REL_TOL
+    nc, nb = np.zeros(16, np.int64), np.zeros(16, np.int64)
+    ref_pool, ref_nc, ref_nb = pool.copy(), nc.copy(), nb.copy()
+    rc, y_ref = oracle.commit(c, ref_pool, ref_nc, ref_nb, expected_block_index=0, want_y=True)
+    assert rc == 0
+    vc = to_dev(c)
+    say("paper geometry commit", w)
+    out = bd.commit_boundary(vc["x"], vc["dt"], vc["A"], vc["B"], vc["C"], vc["D"], vc["D_rev"], h,
+                             nc, nb, 0, y_clean=True)
+    torch.cuda.synchronize()
+    eh, ey = rel_err(from_pool(h), ref_pool), rel_err(out, y_ref)
+    say("  state rel err", eh, "y_clean rel err", ey)
+    assert eh <= REL_TOL and ey <= REL_TOL
+    assert nc.tolist() == ref_nc.tolist() and nb.tolist() == ref_nb.tolist()
+
+
 def sep_inputs(w, seed):
     """Forward inputs and independent reverse inputs (own x, dt, B, C, A, D)."""
     fwd = bi.block_inputs(w, 0)
