@@ -74,6 +74,29 @@ def test_conv_step(H, N, L, bf16, G):
     assert e <= REL_TOL
 
 
+def test_conv_step_full_size():
+    """The convolution-state step at the size the bench times it (350M layer shape: batch
+    16, 32 heads, dstate 128, 32-token bf16 blocks; the convolution inside the block
+    kernel's staging, 512 workgroups per launch), every element against the oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 16, 32, 64, 128, 1, 32, 0, True, 1, 11500)
+    d = bi.block_inputs(w, 0)
+    cw, cb = conv_params(w, 11501)
+    ch = cw.shape[0]
+    cache = np.random.Generator(np.random.PCG64(11502)).standard_normal((16, 3, ch)).astype(np.float32)
+    pool = bi.random_state(w, 16, 3, 0.5).astype(np.float64)
+    y_ref, _ = oracle_step(d, cw, cb, cache.astype(np.float64), pool, list(range(16)))
+    v = to_dev(d)
+    say("conv step, full size", w)
+    y = bd.conv_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"],
+                           torch.from_numpy(cw).to(DEV), torch.from_numpy(cb).to(DEV),
+                           torch.from_numpy(cache).to(DEV), pool_dev(pool))
+    torch.cuda.synchronize()
+    e = rel_err(y, y_ref)
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
 @pytest.mark.parametrize("L,want_y", [(32, True), (2, True), (64, False)])
 def test_conv_commit(L, want_y):
     import paper_2607_02805_amd as bd

@@ -137,6 +137,27 @@ def test_step_separate_reverse_inputs(H, N, L, bf16):
     assert e <= REL_TOL
 
 
+def test_step_separate_reverse_inputs_full_size():
+    """Separate reverse inputs at the size the bench times them (350M layer shape: batch
+    16, 32 heads, dstate 128, 32-token bf16 blocks; one launch of 512 workgroups staging
+    both input sets), every element against the oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 16, 32, 64, 128, 1, 32, 0, True, 1, 10400)
+    fwd, rev = sep_inputs(w, 10401)
+    pool = bi.random_state(w, 16, 7, 0.5).astype(np.float64)
+    vf, vr = to_dev(fwd), to_dev(rev)
+    say("separate reverse inputs, full size", w)
+    y = bd.scan_block_step_sep((vf["x"], vf["dt"], vf["A"], vf["B"], vf["C"], vf["D"]),
+                               (vr["x"], vr["dt"], vr["A"], vr["B"], vr["C"], vr["D_rev"]),
+                               pool_dev(pool))
+    torch.cuda.synchronize()
+    _, yf, _ = oracle.block_step(fwd, pool, parts=True)
+    _, _, yr = oracle.block_step(rev, np.zeros_like(pool), parts=True)
+    e = rel_err(y, yf + yr)
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
 def test_step_separate_reverse_inputs_groups_and_slots():
     """The fused separate-input launch with two groups and a slot map: rows read the
     states of their slots, the pool is not written."""
