@@ -61,3 +61,11 @@ def commit(d: dict, h_pool, nc, nb, expected=-1, slot_idx=None, y_clean=None, st
     import paper_2607_02805_amd as bd
     return bd.commit_boundary(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
                               h_pool, nc, nb, expected, slot_idx, y_clean, stream)
+
+
+def to_host(t):
+    """GPU tensor -> the stored bytes as numpy (bf16 bit patterns as uint16)."""
+    t = t.contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16).copy()
+    return t.numpy().copy()

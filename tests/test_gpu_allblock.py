@@ -15,7 +15,7 @@ import torch
 
 import bdlm_inputs as bi
 import oracle
-from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev
+from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -106,6 +106,42 @@ def test_all_block_forward_equals_sampler():
         assert rel_err(y[:, sl], ys.cpu().double().numpy()) <= REL_TOL
         cache.commit(vc["x"][:, sl].contiguous(), vc["dt"][:, sl].contiguous(), vc["A"],
                      vc["B"][:, sl].contiguous(), vc["C"][:, sl].contiguous(), vc["D"], vc["D_rev"], k)
+
+
+def test_all_block_forward_full_size_sampled():
+    """The all-block forward at the size the bench times it (350M layer shape, batch 8, an
+    8,192-token window of 256 blocks of 32 tokens, inputs drawn on the GPU): for sampled
+    (row, head) pairs, the states entering all 256 blocks, the clean stream's forward
+    outputs and the noised stream's outputs against the oracle run on those slices."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("350m-train-window", 8, 32, 64, 128, 1, 32, 8192, True, 1, 5000)
+    T, L, K = 8192, 32, 256
+    c = bi.tokens_device(w, T, w.base_seed + 1)
+    n = bi.tokens_device(w, T, w.base_seed + 10)
+    hp = bi.head_params(w)
+    dhp = {k: torch.from_numpy(a).to(DEV) for k, a in hp.items()}
+    say("all-block forward, full size", w)
+    y, s_out, yc = bd.all_block_forward((c["x"], c["dt"], c["B"], c["C"]),
+                                        (n["x"], n["dt"], n["B"], n["C"]),
+                                        dhp["A"], dhp["D"], dhp["D_rev"], L, want_clean_y=True)
+    torch.cuda.synchronize()
+    states = from_pool(s_out).reshape(8, K, 32, 64, 128)
+    for b, h in ((0, 0), (5, 13), (7, 31)):
+        def part(v):
+            s = {"x": to_host(v["x"][b:b + 1, :, h:h + 1]), "dt": to_host(v["dt"][b:b + 1, :, h:h + 1]),
+                 "B": to_host(v["B"][b:b + 1]), "C": to_host(v["C"][b:b + 1])}
+            s.update({k: hp[k][h:h + 1] for k in ("A", "D", "D_rev")})
+            return s
+        cs, ns = part(c), part(n)
+        ref_states, ref_yc = oracle_states(cs, K, L, np.zeros((1, 1, 64, 128)))
+        # the noised blocks as K rows of one block each, stepped from the states entering them
+        rows = {k: (ns[k].reshape(K, L, *ns[k].shape[2:]) if k in ("x", "dt", "B", "C") else ns[k])
+                for k in ns}
+        ref_y = oracle.block_step(rows, ref_states[:, 0])
+        e = (rel_err(states[b, :, h], ref_states[:, 0, 0]), rel_err(yc[b:b + 1, :, h:h + 1], ref_yc),
+             rel_err(y[b:b + 1, :, h:h + 1].reshape(K, L, 1, 64), ref_y))
+        say("  (b, h) =", (b, h), "rel err states, clean y, noised y", e)
+        assert max(e) <= REL_TOL
 
 
 def test_boundary_states_many_workgroups_deterministic():

@@ -19,7 +19,7 @@ import torch
 
 import bdlm_inputs as bi
 import oracle
-from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev
+from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -128,14 +128,6 @@ def test_full_window_groups_and_long():
     y = full_window(d)
     torch.cuda.synchronize()
     assert rel_err(y, oracle.full_window(d)) <= REL_TOL
-
-
-def to_host(t):
-    """GPU tensor -> the stored bytes as numpy (bf16 bit patterns as uint16)."""
-    t = t.contiguous().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16).copy()
-    return t.numpy().copy()
 
 
 def test_full_window_contrast_shape_sampled():
