@@ -239,6 +239,31 @@ def test_prefill_rejects_wrong_block_index():
     assert cache.n_blocks.tolist() == [0]
 
 
+def test_prefill_bench_shape_sampled():
+    """The prefill the bench times: 350M layer shape, batch 16, a 16,384-token clean
+    prefix drawn on the GPU, states only.  The committed states of sampled (row, head)
+    pairs against the oracle's prefix scan of those slices."""
+    import paper_2607_02805_amd as bd
+    w = bi.WORKLOADS[3]
+    T = 16384
+    v = bi.tokens_device(w, T, w.base_seed + 1)
+    hp = bi.head_params(w)
+    dhp = {k: torch.from_numpy(a).to(DEV) for k, a in hp.items()}
+    cache = bd.Cache(w.batch, w.nheads, w.dstate)
+    say("prefill, bench shape", w)
+    cache.prefill(v["x"], v["dt"], dhp["A"], v["B"], v["C"], dhp["D"])
+    torch.cuda.synchronize()
+    got = from_pool(cache.h)
+    for b, h in ((0, 0), (9, 20), (15, 31)):
+        sub = {"x": to_host(v["x"][b:b + 1, :, h:h + 1]), "dt": to_host(v["dt"][b:b + 1, :, h:h + 1]),
+               "B": to_host(v["B"][b:b + 1]), "C": to_host(v["C"][b:b + 1])}
+        sub.update({k: hp[k][h:h + 1] for k in ("A", "D", "D_rev")})
+        e = rel_err(got[b, h], oracle.scan_forward(sub)[0, 0])
+        say("  (b, h) =", (b, h), "state rel err", e)
+        assert e <= REL_TOL
+    assert cache.n_committed.tolist() == [T] * w.batch
+
+
 def test_prefill_states_bitwise_repeatable_many_workgroups():
     """Batch 8 x 256 heads x 1024 tokens (more workgroups than CUs): the committed states
     are bitwise equal across calls, and sampled heads match the oracle's prefix scan."""
