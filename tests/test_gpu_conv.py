@@ -129,6 +129,39 @@ def test_conv_commit(L, want_y):
         assert rel_err(out, y_ref) <= REL_TOL
 
 
+def test_conv_commit_full_size():
+    """The convolution-state commit at the size the bench times it (350M layer shape:
+    batch 16, 32 heads, dstate 128, a 32-token bf16 block, identity slots): the new
+    states, the kept convolution rows and the clean-block outputs against the oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 16, 32, 64, 128, 1, 32, 0, True, 1, 11600)
+    d = bi.commit_inputs(w)
+    cw, cb = conv_params(w, 11601)
+    ch = cw.shape[0]
+    cache = np.random.Generator(np.random.PCG64(11602)).standard_normal((16, 3, ch)).astype(np.float32)
+    pool = bi.random_state(w, 16, 4, 0.5).astype(np.float64)
+    slots = list(range(16))
+    y_ref, fin = oracle_step(d, cw, cb, cache.astype(np.float64), pool, slots)
+    *_, s_ref = oracle.block_step(fin, pool, slot_idx=slots, parts=True, final_state=True)
+    cache_ref = cache.astype(np.float64)
+    oracle.conv(d, cw, cb, cache_ref, slot_idx=slots, commit=True)
+    nb = np.zeros(16, np.int64)
+    nc = np.zeros(16, np.int64)
+    v = to_dev(d)
+    h = pool_dev(pool)
+    cp = torch.from_numpy(cache).to(DEV)
+    say("conv commit, full size", w)
+    out = bd.conv_commit_boundary(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"],
+                                  torch.from_numpy(cw).to(DEV), torch.from_numpy(cb).to(DEV), cp, h,
+                                  nc, nb, 0, y_clean=True)
+    torch.cuda.synchronize()
+    assert nb.tolist() == [1] * 16 and nc.tolist() == [32] * 16
+    e = (rel_err(from_pool(h), s_ref), rel_err(out, y_ref))
+    say("  state, clean y rel err", e)
+    assert max(e) <= REL_TOL
+    np.testing.assert_array_equal(cp.cpu().numpy(), cache_ref.astype(np.float32))
+
+
 def test_conv_commits_then_step_equal_oracle_history():
     """Three conv commits, then a conv step: the cached convolution rows and SSM states
     carry the history exactly as the oracle's composition does."""
