@@ -202,7 +202,7 @@ def run_gpu(args):
     prefill_s = ring.extend_prefix(args.prefix)
     print(f"[bench] prefix of {args.prefix} tokens committed ({args.prefix // L} commits) in "
           f"{prefill_s:.2f}s; ring of {nl} layers, state {nl * Bsz * H * P * N * 4 / 2**20:.0f} MiB",
-          flush=True)
+          file=sys.stderr, flush=True)
     stream = torch.cuda.Stream()
     ring.capture(stream)
     t = ring.time_cycles(stream, args.steps, args.warmup)
@@ -256,7 +256,7 @@ def run_flatness(args, prefixes=(4096, 65536, 262144), block_lens=(16, 32, 64)) 
                         "step_gbs": [round(step_bytes(16, 32, 64, 128, 1, L) / (u * 1e3), 1)
                                      for u in st]}
         spreads.append((max(st) - min(st)) / min(st))
-        print(f"[bench] flatness L={L}: step us {st}, commit us {cm}", flush=True)
+        print(f"[bench] flatness L={L}: step us {st}, commit us {cm}", file=sys.stderr, flush=True)
         del ring
         torch.cuda.empty_cache()
     out["max_step_spread"] = round(max(spreads), 4)
@@ -588,7 +588,7 @@ def run_batch_sweep(args, batches=(16, 32, 64, 128), nl=24) -> dict:
         out["copy_us"].append(cp["us_per_launch"])
         out["copy_gbs"].append(cp["gbs"])
         print(f"[bench] batch {b}: step {t * 1e6:.2f} us ({sb / t / 1e9:.0f} GB/s), "
-              f"copy of the same bytes {cp['us_per_launch']:.2f} us", flush=True)
+              f"copy of the same bytes {cp['us_per_launch']:.2f} us", file=sys.stderr, flush=True)
     return out
 
 
