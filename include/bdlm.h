@@ -122,9 +122,10 @@ int bdlm_desc_init(bdlm_desc_t *desc, int64_t batch, int64_t nheads, int64_t hea
  * h_pool       device fp32 state pool, nslots x nheads states of 64 x dstate,
  *              16-byte aligned, in the pool layout (see bdlm_state_pack).  Read
  *              only (the cache is never written by a step).
- * slot_idx     host int32 [batch] mapping batch row -> cache slot, or NULL for
- *              slot(b) = b.  Non-NULL requires batch <= BDLM_MAX_SLOT_ROWS.
- *              Rows may share a slot.
+ * slot_idx     host int32 array of exactly batch entries mapping batch row -> cache
+ *              slot (entry b is row b's slot; the library reads entries 0 .. batch-1
+ *              and nothing beyond), or NULL for slot(b) = b.  Non-NULL requires
+ *              batch <= BDLM_MAX_SLOT_ROWS.  Rows may share a slot.
  * y            device fp32 [batch][block_len][nheads][64], contiguous, 16-byte
  *              aligned.  Fully overwritten.  Must not overlap any input.
  * Alignment: x, B and C base pointers 16-byte aligned, and every x_stride and
@@ -210,8 +211,10 @@ int bdlm_scan_block_step_sep(const bdlm_desc_t *desc, const void *x, const void 
  * Cf, D) from the cached state and the reverse branch on (xr, dt, A, Br, Cr, D_rev)
  * from zero.  A commit also replaces the slot's conv_pool rows by the last three rows
  * of (cached rows ++ block) and updates h_pool from the forward branch.
- * conv_w       device fp32 [channels][4], 16-byte aligned; conv_b fp32 [channels].
+ * conv_w       device fp32 [channels][4]; conv_b fp32 [channels].
  * conv_pool    device fp32 [nslots][3][channels] (same slots as h_pool).
+ *              conv_w, conv_b and conv_pool are read as 16-byte vectors: all three
+ *              must be 16-byte aligned (else BDLM_E_ALIGN).
  * workspace    at least bdlm_conv_workspace bytes (the convolved inputs, fp32),
  *              256-byte aligned; bf16 blocks of up to 32 tokens convolve inside
  *              the scan kernel's staging and leave it untouched.

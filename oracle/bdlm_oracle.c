@@ -24,8 +24,9 @@
  *     causal convolution with SiLU over the x, B, C channels (App. C: Mamba
  *     convolution width 4), continued from the cached last three input rows in
  *     the forward branch and zero-padded inside the block in the reverse branch
- *     (Sec. 2 and Sec. 4: the cached boundary state includes the convolution
- *     state; the reverse scan is local to the active block)
+ *     (Sec. 2 and Sec. 4, Eq. partial-reverse: the cached boundary state carries
+ *     the convolution rows as well as the SSM state, and the right-to-left scan
+ *     never reads tokens outside the block being denoised)
  *   - the gated RMS normalisation that follows the scan in a Mamba-2 mixer
  *     (App. C: the paper's Mamba layers are Mamba-2 mixers; the paper gives no
  *     formula, so the Mamba-2 mixer's output path is taken as written there:

@@ -225,11 +225,31 @@ def _pool(h_pool, H, N):
     return _dev_ptr(h_pool, "h_pool")
 
 
-def _slots(slot_idx):
+def _slots(slot_idx, rows: int):
+    """Host int32 copy of ``slot_idx`` (one cache slot per batch row) and its pointer.
+    The C ABI reads exactly ``rows`` entries, so any other length is refused here."""
     if slot_idx is None:
         return None, None
     arr = np.ascontiguousarray(np.asarray(slot_idx, dtype=np.int32))
+    if arr.ndim != 1 or arr.shape[0] != rows:
+        raise ValueError(f"slot_idx must be a 1-D sequence of exactly {rows} slot indices, "
+                         f"got shape {arr.shape}")
     return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _out(t, shape: tuple, what: str, device=None):
+    """A float32 output: allocated when ``t`` is None or True, else checked to be a
+    contiguous float32 tensor of exactly ``shape`` (the kernels write every element of
+    that shape; a smaller buffer would be written past its end)."""
+    torch = _torch()
+    if t is None or t is True:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    if not torch.is_tensor(t) or t.dtype != torch.float32 or not t.is_contiguous() \
+            or tuple(t.shape) != tuple(shape):
+        got = (tuple(t.shape), t.dtype, t.is_contiguous()) if torch.is_tensor(t) else type(t)
+        raise ValueError(f"{what} must be a contiguous float32 tensor of shape {tuple(shape)}, "
+                         f"got {got}")
+    return t
 
 
 def scan_block_step(x, dt, A, B, C, D, D_rev, h_pool, y=None, slot_idx=None, stream=None):
@@ -241,12 +261,8 @@ def scan_block_step(x, dt, A, B, C, D, D_rev, h_pool, y=None, slot_idx=None, str
     torch = _torch()
     d = _desc(x, dt, B, C)
     H, N = d.nheads, d.dstate
-    if y is None:
-        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
-    elif y.dtype != torch.float32 or not y.is_contiguous() \
-            or tuple(y.shape) != (d.batch, d.block_len, H, HEADDIM):
-        raise ValueError("y must be a contiguous float32 [B, L, H, 64] tensor")
-    keep, sp = _slots(slot_idx)
+    y = _out(y, (d.batch, d.block_len, H, HEADDIM), "y", x.device)
+    keep, sp = _slots(slot_idx, d.batch)
     rc = lib().bdlm_scan_block_step(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
         _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
@@ -265,15 +281,19 @@ def scan_block_step_sep(fwd, rev, h_pool, y=None, slot_idx=None, stream=None):
     torch = _torch()
     x, dt, A, B, C, D = fwd
     xr, dtr, Ar, Br, Cr, Dr = rev
+    for a, b, what in ((x, xr, "x"), (dt, dtr, "dt"), (A, Ar, "A"), (B, Br, "B"), (C, Cr, "C"),
+                       (D, Dr, "D")):
+        if tuple(a.shape) != tuple(b.shape) or a.dtype != b.dtype:
+            raise ValueError(f"forward and reverse {what} must have the same shape and dtype, got "
+                             f"{tuple(a.shape)} {a.dtype} and {tuple(b.shape)} {b.dtype}")
     d = _desc(x, dt, B, C)
     dr = _desc(xr, dtr, Br, Cr)
     if (list(d.x_stride), list(d.dt_stride), list(d.bc_stride), d.in_dtype) != \
             (list(dr.x_stride), list(dr.dt_stride), list(dr.bc_stride), dr.in_dtype):
         raise ValueError("forward and reverse inputs must share shapes, strides and dtype")
     H, N = d.nheads, d.dstate
-    if y is None:
-        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
-    keep, sp = _slots(slot_idx)
+    y = _out(y, (d.batch, d.block_len, H, HEADDIM), "y", x.device)
+    keep, sp = _slots(slot_idx, d.batch)
     rc = lib().bdlm_scan_block_step_sep(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
         _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _dev_ptr(xr, "x_rev"),
@@ -313,12 +333,11 @@ def conv_block_step(x, dt, A, B, C, D, D_rev, conv_w, conv_b, conv_pool, h_pool,
     torch = _torch()
     d = _desc(x, dt, B, C)
     H, N = d.nheads, d.dstate
-    if y is None:
-        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
+    y = _out(y, (d.batch, d.block_len, H, HEADDIM), "y", x.device)
     if conv_pool.shape[0] != h_pool.shape[0]:
         raise ValueError("conv_pool and h_pool must have the same slots")
     wp, wb, wkeep = _conv_args(d, conv_w, conv_b, conv_pool, workspace, x.device)
-    keep, sp = _slots(slot_idx)
+    keep, sp = _slots(slot_idx, d.batch)
     rc = lib().bdlm_conv_block_step(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
         _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
@@ -344,11 +363,10 @@ def conv_commit_boundary(x, dt, A, B, C, D, D_rev, conv_w, conv_b, conv_pool, h_
     for a in (n_committed, n_blocks):
         if not isinstance(a, np.ndarray) or a.dtype != np.int64 or a.shape != (nslots,):
             raise ValueError(f"n_committed / n_blocks must be numpy int64 [{nslots}]")
-    if y_clean is True:
-        y_clean = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
-                              device=x.device)
+    if y_clean is not None:
+        y_clean = _out(y_clean, (d.batch, d.block_len, H, HEADDIM), "y_clean", x.device)
     wp, wb, wkeep = _conv_args(d, conv_w, conv_b, conv_pool, workspace, x.device)
-    keep, sp = _slots(slot_idx)
+    keep, sp = _slots(slot_idx, d.batch)
     i64p = ctypes.POINTER(ctypes.c_int64)
     rc = lib().bdlm_conv_commit_boundary(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
@@ -379,16 +397,11 @@ def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
         if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
                 or a.shape != (nslots,):
             raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
-    if y_clean is True:
-        y_clean = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
-                              device=x.device)
     yp = None
     if y_clean is not None:
-        if y_clean.dtype != torch.float32 or not y_clean.is_contiguous() \
-                or tuple(y_clean.shape) != (d.batch, d.block_len, H, HEADDIM):
-            raise ValueError("y_clean must be a contiguous float32 [B, L, H, 64] tensor")
+        y_clean = _out(y_clean, (d.batch, d.block_len, H, HEADDIM), "y_clean", x.device)
         yp = _dev_ptr(y_clean, "y_clean")
-    keep, sp = _slots(slot_idx)
+    keep, sp = _slots(slot_idx, d.batch)
     i64p = ctypes.POINTER(ctypes.c_int64)
     rc = lib().bdlm_commit_boundary(
         ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
@@ -443,11 +456,7 @@ def scan_full_window(x, dt, A, B, C, D, D_rev, y=None, stream=None, workspace=No
     torch = _torch()
     d = _desc(x, dt, B, C)
     H = d.nheads
-    if y is None:
-        y = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32, device=x.device)
-    elif y.dtype != torch.float32 or not y.is_contiguous() \
-            or tuple(y.shape) != (d.batch, d.block_len, H, HEADDIM):
-        raise ValueError("y must be a contiguous float32 [B, W, H, 64] tensor")
+    y = _out(y, (d.batch, d.block_len, H, HEADDIM), "y", x.device)
     L = lib()
     wp, wb, keep = _workspace(L.bdlm_full_window_workspace, d, workspace, x.device)
     rc = L.bdlm_scan_full_window(
@@ -474,11 +483,10 @@ def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_ind
         if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
                 or a.shape != (nslots,):
             raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
-    if y_fwd is True:
-        y_fwd = torch.empty((d.batch, d.block_len, H, HEADDIM), dtype=torch.float32,
-                            device=x.device)
+    if y_fwd is not None:
+        y_fwd = _out(y_fwd, (d.batch, d.block_len, H, HEADDIM), "y_fwd", x.device)
     yp = None if y_fwd is None else _dev_ptr(y_fwd, "y_fwd")
-    keep, sp = _slots(slot_idx)
+    keep, sp = _slots(slot_idx, d.batch)
     L = lib()
     wp, wb, wkeep = _workspace(L.bdlm_prefill_workspace, d, workspace, x.device)
     i64p = ctypes.POINTER(ctypes.c_int64)
@@ -514,8 +522,8 @@ def block_boundary_states(x, dt, A, B, C, D, block_len, s_init=None, s_out=None,
     if s_init is not None and (s_init.dtype != torch.float32 or not s_init.is_contiguous()
                                or s_init.numel() != d.batch * H * HEADDIM * N):
         raise ValueError(f"s_init must be a contiguous float32 tensor of {d.batch * H} states")
-    if y_fwd is True:
-        y_fwd = torch.empty((d.batch, T, H, HEADDIM), dtype=torch.float32, device=x.device)
+    if y_fwd is not None:
+        y_fwd = _out(y_fwd, (d.batch, T, H, HEADDIM), "y_fwd", x.device)
     L = lib()
     need = ctypes.c_int64(0)
     rc = L.bdlm_boundary_states_workspace(ctypes.byref(d), K, ctypes.byref(need))
@@ -609,7 +617,7 @@ def cache_reset(h_pool, slots=None, n_committed=None, n_blocks=None, stream=None
         raise ValueError("h_pool must be a contiguous float32 tensor")
     nslots = h_pool.shape[0]
     elems = h_pool[0].numel() if nslots else 0
-    keep, sp = _slots(slots)
+    keep, sp = (None, None) if slots is None else _slots(slots, len(slots))
     i64p = ctypes.POINTER(ctypes.c_int64)
     rc = lib().bdlm_cache_reset(
         _dev_ptr(h_pool, "h_pool"), nslots, elems, sp, 0 if keep is None else len(keep),

@@ -7,6 +7,7 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -36,17 +37,24 @@ def _run(cmd: list[str]) -> None:
             sys.stderr.write(line + "\n")
 
 
+HIP_SRCS = ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip", "bdlm_norm.hip")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
-    for src in ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip", "bdlm_norm.hip"):
+    cmds, objs = [], []
+    for src in HIP_SRCS:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),
-              "-o", obj])
+        cmds.append([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+                     os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     a_obj = os.path.join(BUILD, "bdlm_api.o")
-    _run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", f"-I{INCLUDE}", f"-I{CSRC}",
-          "-c", os.path.join(CSRC, "bdlm_api.cpp"), "-o", a_obj])
+    cmds.append(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", f"-I{INCLUDE}",
+                 f"-I{CSRC}", "-c", os.path.join(CSRC, "bdlm_api.cpp"), "-o", a_obj])
+    # the translation units are independent: compile them side by side
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
+        for f in [ex.submit(_run, c) for c in cmds]:
+            f.result()
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs, a_obj])
     os.replace(tmp, LIB)

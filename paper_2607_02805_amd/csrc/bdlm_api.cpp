@@ -399,7 +399,8 @@ int bdlm_conv_workspace(const bdlm_desc_t *d, int64_t *bytes) {
 static int check_conv(const bdlm_desc_t *d, const float *conv_w, const float *conv_b,
                       const float *conv_pool, const void *ws, int64_t ws_bytes) {
     if (!conv_w || !conv_b || !conv_pool) return BDLM_E_NULL;
-    if (!aligned(conv_w, 16) || !aligned(conv_b, 4) || !aligned(conv_pool, 4)) return BDLM_E_ALIGN;
+    // the kernels read weights, biases and cached rows as 16-byte vectors
+    if (!aligned(conv_w, 16) || !aligned(conv_b, 16) || !aligned(conv_pool, 16)) return BDLM_E_ALIGN;
     // the convolved inputs are scanned from the (fp32, contiguous) workspace
     if (d->nheads * BDLM_HEADDIM * 4 > (int64_t(1) << 24)) return BDLM_E_SHAPE;
     return check_workspace(ws, ws_bytes,

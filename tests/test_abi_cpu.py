@@ -422,6 +422,9 @@ def test_conv_entry_point_checks(L):
     assert step() == bd.OK
     assert step(cw=None) == bd.E_NULL and step(cb=None) == bd.E_NULL and step(cp=None) == bd.E_NULL
     assert step(cw=cw + 8) == bd.E_ALIGN
+    # biases and cached rows are read as 16-byte vectors too
+    assert step(cb=cb + 4) == bd.E_ALIGN and step(cb=cb + 8) == bd.E_ALIGN
+    assert step(cp=cp + 4) == bd.E_ALIGN and step(cp=cp + 8) == bd.E_ALIGN
     assert step(wsb=n.value - 4) == bd.E_WORKSPACE
     nc, nb = np.zeros(4, np.int64), np.array([1, 1, 2, 2], np.int64)
     rc = L.bdlm_check_conv_commit(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"], p["D"],
@@ -472,3 +475,82 @@ def test_gated_rmsnorm_checks(L):
     assert check_norm(L, out=FAKE + 0x100000 - 0x1000) == bd.E_SHAPE
     assert check_norm(L, out=FAKE + 0x200000) == bd.E_SHAPE
     assert check_norm(L, out=FAKE + 0x100000 - 0x4000) == bd.OK      # ends where z starts
+
+
+# ----------------------------------------------------------------- binding checks
+# The binding refuses mis-shaped tensors and slot lists before it takes any device
+# pointer, so CPU tensors reach these checks (a well-formed CPU call would instead be
+# refused for not being on the GPU).
+def _blk(batch=2, Lb=16, H=H, N=N, dtype=None):
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    f32 = torch.float32
+    return dict(x=torch.zeros(batch, Lb, H, 64, dtype=dtype), dt=torch.zeros(batch, Lb, H, dtype=dtype),
+                A=torch.zeros(H, dtype=f32), B=torch.zeros(batch, Lb, 1, N, dtype=dtype),
+                C=torch.zeros(batch, Lb, 1, N, dtype=dtype), D=torch.zeros(H, dtype=f32),
+                D_rev=torch.zeros(H, dtype=f32))
+
+
+def _args(v):
+    return v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"]
+
+
+@pytest.mark.parametrize("shape", [(2, 16, H, 32), (1, 16, H, 64), (2, 15, H, 64), (2, 16, H * 64)])
+def test_binding_rejects_misshaped_outputs(shape):
+    import torch
+    v = _blk()
+    pool = torch.zeros(bd.pool_shape(4, H, N))
+    bad = torch.zeros(shape)
+    nc, nb = np.zeros(4, np.int64), np.zeros(4, np.int64)
+    cw, cb = torch.zeros(bd.conv_channels(H, 1, N), 4), torch.zeros(bd.conv_channels(H, 1, N))
+    cpool = torch.zeros(4, 3, bd.conv_channels(H, 1, N))
+    calls = {
+        "step": lambda: bd.scan_block_step(*_args(v), pool, y=bad),
+        "sep": lambda: bd.scan_block_step_sep(_args(v)[:6], _args(v)[:5] + (v["D_rev"],), pool,
+                                              y=bad),
+        "commit": lambda: bd.commit_boundary(*_args(v), pool, nc, nb, y_clean=bad),
+        "conv_step": lambda: bd.conv_block_step(*_args(v), cw, cb, cpool, pool, y=bad),
+        "conv_commit": lambda: bd.conv_commit_boundary(*_args(v), cw, cb, cpool, pool, nc, nb,
+                                                       y_clean=bad),
+        "full_window": lambda: bd.scan_full_window(*_args(v), y=bad),
+        "prefill": lambda: bd.prefill(*_args(v)[:6], pool, nc, nb, y_fwd=bad),
+        "boundary": lambda: bd.block_boundary_states(*_args(v)[:6], 16, y_fwd=bad),
+    }
+    for name, fn in calls.items():
+        with pytest.raises(ValueError, match="float32 tensor of shape"):
+            fn()
+    # wrong dtype or a non-contiguous view of the right shape are refused too
+    with pytest.raises(ValueError, match="float32 tensor of shape"):
+        bd.scan_block_step(*_args(v), pool, y=torch.zeros(2, 16, H, 64, dtype=torch.float64))
+    with pytest.raises(ValueError, match="float32 tensor of shape"):
+        bd.scan_block_step(*_args(v), pool, y=torch.zeros(2, 16, 64, H).transpose(2, 3))
+
+
+@pytest.mark.parametrize("field", ["x", "dt", "A", "B", "C", "D"])
+def test_binding_sep_rejects_reverse_shape_mismatch(field):
+    import torch
+    v = _blk(batch=2)
+    small = _blk(batch=1)
+    fwd = (v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"])
+    rev = dict(zip(("x", "dt", "A", "B", "C", "D"), fwd))
+    if field in ("A", "D"):
+        rev[field] = torch.zeros(H + 1)
+    else:
+        rev[field] = small[field]
+    pool = torch.zeros(bd.pool_shape(4, H, N))
+    with pytest.raises(ValueError, match="same shape"):
+        bd.scan_block_step_sep(fwd, tuple(rev[k] for k in ("x", "dt", "A", "B", "C", "D")), pool)
+
+
+@pytest.mark.parametrize("slots", [[0], [0, 1, 2], [[0, 1]], np.zeros((2, 1), np.int32)])
+def test_binding_rejects_slot_list_of_wrong_length(slots):
+    import torch
+    v = _blk(batch=2)
+    pool = torch.zeros(bd.pool_shape(4, H, N))
+    nc, nb = np.zeros(4, np.int64), np.zeros(4, np.int64)
+    with pytest.raises(ValueError, match="exactly 2 slot indices"):
+        bd.scan_block_step(*_args(v), pool, slot_idx=slots)
+    with pytest.raises(ValueError, match="exactly 2 slot indices"):
+        bd.commit_boundary(*_args(v), pool, nc, nb, slot_idx=slots)
+    with pytest.raises(ValueError, match="exactly 2 slot indices"):
+        bd.prefill(*_args(v)[:6], pool, nc, nb, slot_idx=slots)
