@@ -36,9 +36,21 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, GB/s
-KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_02805_amd", "csrc", f)
-               for f in ("bdlm_scan.hip", "bdlm_device.h")]
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_block_step_350m_b16_L32.md")
+CSRC = os.path.join(ROOT, "paper_2607_02805_amd", "csrc")
+# the sources each profiled kernel family is compiled from (a summary under profiles/
+# records their hash; a figure is read back only while the hash still matches)
+SOURCE_SETS = {
+    "block": ("bdlm_scan.hip", "bdlm_device.h", "bdlm_launch.h"),
+    "seq": ("bdlm_seq.hip", "bdlm_device.h", "bdlm_launch.h"),
+    "all": ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip", "bdlm_norm.hip", "bdlm_device.h",
+            "bdlm_launch.h"),
+}
+KERNEL_SRCS = [os.path.join(CSRC, f) for f in SOURCE_SETS["block"]]
+PROFILES = os.path.join(ROOT, "profiles")
+TRAFFIC_SUMMARY = os.path.join(PROFILES, "hbm_traffic_block_step_350m_b16_L32.md")
+TRACE_SUMMARY = os.path.join(PROFILES, "block_step_350m_b16_L32_kernel_trace.md")
+SQ_SUMMARY = os.path.join(PROFILES, "sq_counters_block_step_350m_b16_L32.md")
+PROBE_LIB = os.path.join(ROOT, "paper_2607_02805_amd", "libbdlm_probe.so")
 STEP_KERNEL = "bdlm_block_kernel<32, 128, false, false, 2, 0, false>"
 COMMIT_KERNEL = "bdlm_block_kernel<32, 128, false, true, 2, 0, false>"
 
@@ -150,6 +162,30 @@ class Ring:
         torch.cuda.synchronize()
         self.graphs = (g_steps, g_commit)
 
+    def parity_sample(self, stream) -> dict:
+        """One eager step and one eager commit of layer 0 on its step-0 and clean inputs,
+        from the layer's current cached state (the one the timed steps read), into fresh
+        buffers: the GPU side of the bench's parity check against the oracle."""
+        import torch
+
+        import paper_2607_02805_amd as bd
+        c, lay = self.caches[0], self.layers[0]
+        d, cl = lay["steps"][0], lay["clean"]
+        with torch.cuda.stream(stream):
+            before = bd.state_unpack(c.h, stream=stream)
+            y = bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"],
+                                   c.h, stream=stream)
+            h = c.h.clone()
+            nb = c.n_blocks.copy()
+            yc = bd.commit_boundary(cl["x"], cl["dt"], cl["A"], cl["B"], cl["C"], cl["D"],
+                                    cl["D_rev"], h, c.n_committed.copy(), nb, int(nb[0]),
+                                    y_clean=True, stream=stream)
+            after = bd.state_unpack(h, stream=stream)
+        stream.synchronize()
+        return {"state": before.cpu().numpy(), "y": y.cpu().numpy(),
+                "y_clean": yc.cpu().numpy(), "state_after": after.cpu().numpy(),
+                "prefix_tokens": int(c.n_committed[0])}
+
     def advance_books(self):
         for c in self.caches:
             c.n_committed += self.w.block_len
@@ -187,37 +223,41 @@ class Ring:
                 "wall_s": wall_s, "prefix_tokens": int(self.caches[0].n_committed[0])}
 
 
-def run_gpu(args):
+def ring_layers(w, min_bytes: int = 512 << 20, least: int = 32) -> int:
+    """Layers in a cold ring: enough that their states alone exceed twice the 256 MB
+    Infinity Cache, so no step finds its state there."""
+    per = w.batch * w.nheads * w.headdim * w.dstate * 4
+    return max(least, -(-min_bytes // per))
+
+
+def run_config(w, p: int, nl: int, prefix: int, steps: int, warmup: int,
+               parity: bool = False) -> dict:
+    """Block cycles (``p`` denoising steps + the commit) of a ring of ``nl`` layers at
+    workload ``w`` with a ``prefix``-token committed prefix, replayed from HIP graphs."""
     import torch
-
-    import bdlm_inputs as bi
-
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    w = bi.WORKLOADS[3].with_block_len(args.block_len)
     Bsz, H, P, N, G, L = w.batch, w.nheads, w.headdim, w.dstate, w.ngroups, w.block_len
-    nl, p = args.layers, args.denoise
-
     ring = Ring(w, nl, p, dev)
-    prefill_s = ring.extend_prefix(args.prefix)
-    print(f"[bench] prefix of {args.prefix} tokens committed ({args.prefix // L} commits) in "
+    prefill_s = ring.extend_prefix(prefix)
+    print(f"[bench] {w.name}: prefix of {prefix} tokens committed ({prefix // L} commits) in "
           f"{prefill_s:.2f}s; ring of {nl} layers, state {nl * Bsz * H * P * N * 4 / 2**20:.0f} MiB",
           file=sys.stderr, flush=True)
     stream = torch.cuda.Stream()
     ring.capture(stream)
-    t = ring.time_cycles(stream, args.steps, args.warmup)
-
+    t = ring.time_cycles(stream, steps, warmup)
+    sample = ring.parity_sample(stream) if parity else None
     avg_step_s = float(t["step_us"].mean()) * 1e-6
     avg_commit_s = float(t["commit_us"].mean()) * 1e-6
-    per_layer_cycle_s = t["t_total"] / (args.steps * nl)
-    tokens = p * Bsz * L
+    per_layer_cycle_s = t["t_total"] / (steps * nl)
     sb = step_bytes(Bsz, H, P, N, G, L)
     cb = commit_bytes(Bsz, H, P, N, G, L)
     del ring
     torch.cuda.empty_cache()
     return {
-        "value": tokens / per_layer_cycle_s,
-        "ms_per_step": t["t_total"] / args.steps * 1e3,
+        "value": p * Bsz * L / per_layer_cycle_s,
+        "finalised_tokens_per_s": Bsz * L / per_layer_cycle_s,
+        "ms_per_step": t["t_total"] / steps * 1e3,
         "wall_s": t["wall_s"],
         "avg_step_us": avg_step_s * 1e6,
         "median_step_us": float(np.median(t["step_us"])),
@@ -228,8 +268,81 @@ def run_gpu(args):
         "achieved_gbs": sb / avg_step_s / 1e9,
         "commit_gbs": cb / avg_commit_s / 1e9,
         "prefix_tokens": t["prefix_tokens"],
+        "layers": nl,
+        "denoise_steps": p,
         "shape": dict(batch=Bsz, nheads=H, headdim=P, dstate=N, ngroups=G, block_len=L),
+        "sample": sample,
     }
+
+
+def run_gpu(args):
+    import bdlm_inputs as bi
+    w = bi.WORKLOADS[3].with_block_len(args.block_len)
+    return run_config(w, args.denoise, args.layers, args.prefix, args.steps, args.warmup,
+                      parity=not args.no_cpu_baseline)
+
+
+def config_line(r: dict, name: str) -> dict:
+    """A benched configuration in the headline's format (no roofline extras)."""
+    s = r["shape"]
+    return {
+        "workload": name,
+        "value": round(r["value"], 1), "unit": "tokens/s",
+        "finalised_tokens_per_s": round(r["finalised_tokens_per_s"], 1),
+        "ms_per_step": round(r["ms_per_step"], 4),
+        "batch": s["batch"], "nheads": s["nheads"], "dstate": s["dstate"],
+        "block_len": s["block_len"], "prefix_tokens": r["prefix_tokens"],
+        "denoise_steps": r["denoise_steps"], "layer_ring": r["layers"],
+        "step_us": round(r["avg_step_us"], 3), "commit_us": round(r["avg_commit_us"], 3),
+        "step_bytes": r["step_bytes"], "step_gbs": round(r["achieved_gbs"], 1),
+        "frac": round(r["achieved_gbs"] / HBM_PEAK_GBS, 4),
+        "commit_gbs": round(r["commit_gbs"], 1),
+    }
+
+
+def run_other_configs(args) -> dict:
+    """The 87M layer (batch 8, 24 heads, dstate 64, L 32, 8,192-token prefix, one
+    denoising step + commit per block) and the 350M layer at a 65,536-token prefix
+    (batch 16, 8 steps + commit), each over its own cold ring."""
+    import bdlm_inputs as bi
+    out = {}
+    w1 = bi.WORKLOADS[1]
+    r1 = run_config(w1, 1, ring_layers(w1), w1.prefix, args.steps, args.warmup)
+    out["87m_b8_prefix8192"] = config_line(
+        r1, f"87m-mamba-layer-b{w1.batch}-L{w1.block_len}-prefix{w1.prefix}-1step+commit")
+    w2 = bi.WORKLOADS[2]
+    r2 = run_config(w2, w2.steps, ring_layers(w2), w2.prefix, args.steps, args.warmup)
+    out["350m_b16_prefix65536"] = config_line(
+        r2, f"350m-mamba-layer-b{w2.batch}-L{w2.block_len}-prefix{w2.prefix}"
+            f"-{w2.steps}steps+commit")
+    for k, v in out.items():
+        print(f"[bench] {k}: {v['value']:.4g} tokens/s, step {v['step_us']} us "
+              f"({v['step_gbs']} GB/s), commit {v['commit_us']} us", file=sys.stderr, flush=True)
+    return out
+
+
+def parity_vs_oracle(w, sample: dict) -> dict:
+    """The benched step and commit of one layer (the GPU outputs of ``sample``) against the
+    oracle on the same inputs and the same cached state: max relative error per output,
+    max_i |gpu_i - ref_i| / max(|ref_i|, 1e-2 rms(ref))."""
+    import bdlm_inputs as bi
+    import oracle
+
+    def rel(g, r):
+        floor = 1e-2 * np.sqrt(np.mean(r * r))
+        return float(np.max(np.abs(g.astype(np.float64) - r) / np.maximum(np.abs(r), floor)))
+    d, c = bi.block_inputs(w, 0), bi.commit_inputs(w)
+    h = sample["state"].astype(np.float64)
+    y_ref = oracle.block_step(d, h)
+    nc, nb = np.zeros(w.batch, np.int64), np.zeros(w.batch, np.int64)
+    rc, yc_ref = oracle.commit(c, h, nc, nb, want_y=True)
+    if rc != 0:
+        raise RuntimeError(f"oracle commit failed: {rc}")
+    return {"y": rel(sample["y"], y_ref), "state": rel(sample["state_after"], h),
+            "y_clean": rel(sample["y_clean"], yc_ref), "tol": 2e-3,
+            "sample": f"layer 0 of the ring at prefix {sample['prefix_tokens']}: one step (step-0 "
+                      "inputs) and one commit (clean block, with its outputs) from the cached "
+                      "state the timed steps read, against the fp64 oracle on the same bytes"}
 
 
 def run_flatness(args, prefixes=(4096, 65536, 262144), block_lens=(16, 32, 64)) -> dict:
@@ -679,31 +792,95 @@ def cpu_baseline(args, budget_s: float):
             "cpu_model": model}
 
 
-def kernel_source_sha() -> str:
-    """Hash of the sources the block-step kernel is compiled from."""
+def kernel_source_sha(which: str = "block") -> str:
+    """Hash of the sources a kernel family is compiled from (SOURCE_SETS)."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SRCS:
-        h.update(open(f, "rb").read())
+    for f in SOURCE_SETS[which]:
+        h.update(open(os.path.join(CSRC, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+def profile_fields(path: str, which: str = "block") -> dict:
+    """The ``- key: value`` lines of a committed profile summary, or {} when it is missing
+    or was taken on other kernel sources (its kernel_source_sha256_16 no longer matches)."""
+    if not os.path.exists(path):
+        return {}
+    kv = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            kv[k.strip()] = v.strip().strip("`")
+    return kv if kv.get("kernel_source_sha256_16") == kernel_source_sha(which) else {}
+
+
+def _num(kv: dict, key: str, cast=float):
+    try:
+        return cast(kv[key])
+    except (KeyError, ValueError):
+        return None
 
 
 def measured_traffic():
     """HBM bytes per step launch from the committed counter summary, or None when the
     kernel source changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
+    return _num(profile_fields(TRAFFIC_SUMMARY), "step_hbm_bytes_per_launch", int)
+
+
+def run_stream_ceiling(unit_bytes: tuple, units: int, nbuf: int = 32, reps: int = 20) -> dict:
+    """A plain streaming kernel (libbdlm_probe.so) with the block step's byte shape: per
+    unit a state slab read, an input slab read and an output slab written, over a ring of
+    ``nbuf`` buffer sets (every launch misses the Infinity Cache), replayed from a HIP
+    graph like the step; the fastest of its launch shapes.  What a launch of this size
+    reaches here with no arithmetic at all."""
+    import ctypes
+
+    import torch
+    if not os.path.exists(PROBE_LIB):
         return None
-    kv = {}
-    for line in open(TRAFFIC_SUMMARY):
-        if line.startswith("- ") and ":" in line:
-            k, v = line[2:].split(":", 1)
-            kv[k.strip()] = v.strip().strip("`")
-    if kv.get("kernel_source_sha256_16") != kernel_source_sha():
-        return None
-    try:
-        return int(kv["step_hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    lib = ctypes.CDLL(PROBE_LIB)
+    vp, i64 = ctypes.c_void_p, ctypes.c_int64
+    lib.bdlm_probe_stream.argtypes = [vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp]
+    lib.bdlm_probe_stream.restype = ctypes.c_int
+    dev = "cuda:0"
+    st_b, in_b, out_b = unit_bytes
+    bufs = [(torch.rand(units * st_b // 4, device=dev), torch.rand(units * in_b // 4, device=dev),
+             torch.empty(units * out_b // 4, device=dev)) for _ in range(nbuf)]
+    stream = torch.cuda.Stream()
+    best = None
+    for cfg in range(lib.bdlm_probe_configs()):
+        def launch(b):
+            rc = lib.bdlm_probe_stream(b[0].data_ptr(), b[1].data_ptr(), b[2].data_ptr(), units,
+                                       st_b, in_b, out_b, cfg, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"probe launch failed: {rc}")
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            for b in bufs:
+                launch(b)
+        stream.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for b in bufs:
+                launch(b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            g.replay()
+            e0.record(stream)
+            for _ in range(reps):
+                g.replay()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (reps * nbuf)
+        if best is None or us < best[0]:
+            best = (us, cfg)
+        del g
+    del bufs
+    torch.cuda.empty_cache()
+    nbytes = units * (st_b + in_b + out_b)
+    return {"bytes_per_launch": nbytes, "unit_bytes": list(unit_bytes), "units": units,
+            "us_per_launch": round(best[0], 3), "gbs": round(nbytes / best[0] / 1e3, 1),
+            "config": best[1]}
 
 
 def _csv_rows(path):
@@ -926,7 +1103,13 @@ def main():
 
     r = run_gpu(args)
     extras = {}
+    s = r["shape"]
+    unit = (s["headdim"] * s["dstate"] * 4, 0, s["block_len"] * s["headdim"] * 4)
+    units = s["batch"] * s["nheads"]
+    unit = (unit[0], (r["step_bytes"] - units * (unit[0] + unit[2])) // units // 64 * 64, unit[2])
+    ceiling = run_stream_ceiling(unit, units)
     if not args.no_extras:
+        extras["configs"] = run_other_configs(args)
         extras["copy_reference"] = run_copy_reference(r["step_bytes"])
         extras["warm"] = run_warm(args)
         extras["flatness"] = run_flatness(args)
@@ -936,12 +1119,22 @@ def main():
         extras["variants"] = run_variants(args)
         extras["batch_sweep"] = run_batch_sweep(args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, args.cpu_budget)
-    s = r["shape"]
+    parity = None
+    if r["sample"] is not None:
+        import bdlm_inputs as bi
+        parity = parity_vs_oracle(bi.WORKLOADS[3].with_block_len(args.block_len), r["sample"])
+        print(f"[bench] parity vs oracle: {parity}", file=sys.stderr, flush=True)
+    trace = profile_fields(TRACE_SUMMARY)
+    sq = profile_fields(SQ_SUMMARY)
+    rocprof_us = _num(trace, "step_kernel_mean_us")
     line = {
         "metric": "active-block tokens/s per Mamba layer (350M layer shape, batch 16, 262K "
                   "prefix); % of HBM roofline of the block step",
         "value": round(r["value"], 1),
         "unit": "tokens/s",
+        # every token of the active block counts once per denoising step (the metric); a
+        # block of L tokens is finalised once per cycle of p steps: value / p
+        "finalised_tokens_per_s": round(r["finalised_tokens_per_s"], 1),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -952,7 +1145,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"350m-mamba-layer-b{s['batch']}-L{s['block_len']}-prefix{r['prefix_tokens']}"
+            "workload": f"350m-mamba-layer-b{s['batch']}-L{s['block_len']}-prefix{args.prefix}"
                         f"-{args.denoise}steps+commit",
             "batch": s["batch"], "nheads": s["nheads"], "headdim": s["headdim"],
             "dstate": s["dstate"], "ngroups": s["ngroups"], "block_len": s["block_len"],
@@ -974,9 +1167,23 @@ def main():
             "frac": round(r["achieved_gbs"] / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic() if args.block_len == 32 else None,
             "bytes_per_launch": r["step_bytes"],
+            "frac_source": "hip events on the replay stream: algorithmic bytes / mean time per "
+                           "step node over the timed graph replays",
+            # the same kernel's mean dispatch duration in the committed rocprofv3 kernel trace
+            # of this command (null once the kernel sources differ from the traced ones)
+            "kernel_us_rocprof": rocprof_us,
+            "frac_rocprof": None if rocprof_us is None
+            else round(r["step_bytes"] / (rocprof_us * 1e3) / HBM_PEAK_GBS, 4),
+            "mfma_busy_pct": _num(sq, "step_mfma_busy_pct"),
+            "stream_ceiling_gbs": None if ceiling is None else ceiling["gbs"],
+            "frac_of_stream_ceiling": None if ceiling is None
+            else round(r["achieved_gbs"] / ceiling["gbs"], 4),
         },
+        "max_rel_err": parity,
         "cpu_baseline": cpu,
     }
+    if ceiling is not None:
+        line["stream_ceiling"] = ceiling
     if "copy_reference" in extras:
         cr = extras["copy_reference"]
         line["roofline"]["copy_same_bytes_gbs"] = cr["gbs"]

@@ -54,8 +54,9 @@ extern "C" {
 #define BDLM_MAX_BLOCK_LEN 64
 /* Longest sequence of bdlm_scan_full_window and bdlm_prefill. */
 #define BDLM_MAX_SEQ_LEN (((int64_t)1 << 31) - 1)
-/* Largest batch for which an explicit slot_idx may be given (it is passed to
-   the kernels by value). */
+/* Rows per launch when an explicit slot_idx is given: the kernels receive the slot
+   table by value, so a call with a longer table is enqueued as consecutive launches of
+   at most this many rows (no limit on batch results from it). */
 #define BDLM_MAX_SLOT_ROWS 256
 /* Most heads (nheads * 64 channels) bdlm_gated_rmsnorm takes per token. */
 #define BDLM_NORM_MAX_HEADS 256
@@ -124,8 +125,9 @@ int bdlm_desc_init(bdlm_desc_t *desc, int64_t batch, int64_t nheads, int64_t hea
  *              only (the cache is never written by a step).
  * slot_idx     host int32 array of exactly batch entries mapping batch row -> cache
  *              slot (entry b is row b's slot; the library reads entries 0 .. batch-1
- *              and nothing beyond), or NULL for slot(b) = b.  Non-NULL requires
- *              batch <= BDLM_MAX_SLOT_ROWS.  Rows may share a slot.
+ *              and nothing beyond), or NULL for slot(b) = b.  With more than
+ *              BDLM_MAX_SLOT_ROWS rows the step is enqueued as one launch per run
+ *              of that many rows.  Rows may share a slot.
  * y            device fp32 [batch][block_len][nheads][64], contiguous, 16-byte
  *              aligned.  Fully overwritten.  Must not overlap any input.
  * Alignment: x, B and C base pointers 16-byte aligned, and every x_stride and

@@ -15,6 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libbdlm.so")
+PROBE_LIB = os.path.join(HERE, "libbdlm_probe.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -58,6 +59,10 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs, a_obj])
     os.replace(tmp, LIB)
+    # the benchmark's streaming probe: a library of its own, outside the product ABI
+    ptmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-shared", "-o", ptmp, os.path.join(CSRC, "bdlm_probe.hip")])
+    os.replace(ptmp, PROBE_LIB)
     if verbose:
         print(f"built {LIB}")
     return LIB

@@ -5,6 +5,9 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "bdlm.h"
 #include "bdlm_launch.h"
 
@@ -48,7 +51,6 @@ int check_common(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     if (need_pool && nslots <= 0) return BDLM_E_SHAPE;
     if (need_pool && nslots > (int64_t(1) << 40) / (d->nheads * BDLM_HEADDIM * d->dstate))
         return BDLM_E_SHAPE;
-    if (slot_idx && d->batch > BDLM_MAX_SLOT_ROWS) return BDLM_E_SHAPE;
     // With no token to read, the activation pointers may be NULL (an empty tensor
     // can have no storage).
     const bool empty = d->batch == 0 || d->block_len == 0;
@@ -119,6 +121,42 @@ bdlm::LaunchArgs make_args(const bdlm_desc_t *d, const void *x, const void *dt, 
     return a;
 }
 
+// Rows [r0, r0 + n) of a call as a call of its own: the activations and outputs
+// advanced by r0 rows (y_row floats of output per row), the slot table by r0 entries.
+bdlm::LaunchArgs rows_of(const bdlm::LaunchArgs &a, int64_t r0, int64_t n, int64_t y_row) {
+    bdlm::LaunchArgs s = a;
+    const int64_t es = a.bf16 ? 2 : 4;
+    auto adv = [&](const void *p, int64_t elems) {
+        return p ? static_cast<const void *>(static_cast<const char *>(p) + elems * es) : p;
+    };
+    s.x = adv(a.x, r0 * a.xs_b);
+    s.dt = adv(a.dt, r0 * a.dts_b);
+    s.Bm = adv(a.Bm, r0 * a.bcs_b);
+    s.Cm = adv(a.Cm, r0 * a.bcs_b);
+    if (a.y) s.y = a.y + r0 * y_row;
+    if (a.slots) s.slots = a.slots + r0;
+    s.batch = static_cast<int32_t>(n);
+    return s;
+}
+
+// The kernels take an explicit slot table by value, BDLM_MAX_SLOT_ROWS rows per launch:
+// a call with a longer table runs as consecutive launches over row ranges (on one
+// stream, in order, so a workspace is reused safely).  launch(args...) receives the
+// sliced arguments.
+template <class F>
+int by_row_chunks(const bdlm::LaunchArgs &a, int64_t y_row, F &&launch) {
+    if (!a.slots || a.batch <= BDLM_MAX_SLOT_ROWS) return launch(a);
+    for (int64_t r0 = 0; r0 < a.batch; r0 += BDLM_MAX_SLOT_ROWS) {
+        const int64_t n = std::min<int64_t>(BDLM_MAX_SLOT_ROWS, a.batch - r0);
+        const int rc = launch(rows_of(a, r0, n, y_row));
+        if (rc != BDLM_OK) return rc;
+    }
+    return BDLM_OK;
+}
+
+// Output floats per batch row of a block (or sequence) of len tokens.
+int64_t y_row_floats(const bdlm_desc_t *d, int64_t len) { return len * d->nheads * BDLM_HEADDIM; }
+
 }  // namespace
 
 extern "C" {
@@ -185,11 +223,13 @@ int bdlm_check_block_step(const bdlm_desc_t *d, const void *x, const void *dt, c
 static int check_books(const bdlm_desc_t *d, const int32_t *slot_idx, const int64_t *n_committed,
                        const int64_t *n_blocks, int64_t expected_block_index) {
     if (!n_committed || !n_blocks) return BDLM_E_NULL;
+    if (slot_idx && d->batch > 1) {   // the rows of a commit write distinct slots
+        std::vector<int32_t> sorted(slot_idx, slot_idx + d->batch);
+        std::sort(sorted.begin(), sorted.end());
+        if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end()) return BDLM_E_SLOT;
+    }
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;
-        if (slot_idx)
-            for (int64_t c = 0; c < b; ++c)
-                if (slot_idx[c] == s) return BDLM_E_SLOT;
         if (expected_block_index >= 0 && n_blocks[s] != expected_block_index) return BDLM_E_OFFSET;
     }
     return BDLM_OK;
@@ -327,8 +367,10 @@ int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, co
     // argument block as a commit, with the state update compiled out.
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
-    if (d->block_len > BDLM_MAX_BLOCK_LEN) return bdlm::launch_block_long(a, a, false, true, stream);
-    return bdlm::launch_block(a, false, stream);
+    return by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
+        return d->block_len > BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_long(c, c, false, true, stream)
+                                                 : bdlm::launch_block(c, false, stream);
+    });
 }
 
 int bdlm_check_block_step_sep(const bdlm_desc_t *d, const void *x, const void *dt,
@@ -361,8 +403,13 @@ int bdlm_scan_block_step_sep(const bdlm_desc_t *d, const void *x, const void *dt
         make_args(d, x, dt, A, B, C, D, D, const_cast<float *>(h_pool), slot_idx, y);
     const bdlm::LaunchArgs r =
         make_args(d, x_rev, dt_rev, A_rev, B_rev, C_rev, D_rev, D_rev, nullptr, slot_idx, y);
-    return d->block_len <= BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_pair(f, r, false, true, stream)
-                                              : bdlm::launch_block_long(f, r, false, true, stream);
+    const int64_t yr = y_row_floats(d, d->block_len);
+    return by_row_chunks(f, yr, [&](const bdlm::LaunchArgs &fc) {
+        const int64_t r0 = fc.slots ? fc.slots - f.slots : 0;
+        const bdlm::LaunchArgs rc = rows_of(r, r0, fc.batch, yr);
+        return d->block_len <= BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_pair(fc, rc, false, true, stream)
+                                                  : bdlm::launch_block_long(fc, rc, false, true, stream);
+    });
 }
 
 int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
@@ -376,9 +423,11 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
     if (y_clean && !aligned(y_clean, 16)) return BDLM_E_ALIGN;
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
-    rc = d->block_len > BDLM_MAX_BLOCK_LEN
-             ? bdlm::launch_block_long(a, a, true, y_clean != nullptr, stream)
-             : bdlm::launch_block(a, true, stream);
+    rc = by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
+        return d->block_len > BDLM_MAX_BLOCK_LEN
+                   ? bdlm::launch_block_long(c, c, true, y_clean != nullptr, stream)
+                   : bdlm::launch_block(c, true, stream);
+    });
     if (rc != BDLM_OK) return rc;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;
@@ -432,8 +481,10 @@ int bdlm_conv_block_step(const bdlm_desc_t *d, const void *x, const void *dt, co
     if (rc != BDLM_OK) return rc;
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
-    return bdlm::launch_conv_block(a, conv_w, conv_b, const_cast<float *>(conv_pool), false,
-                                   workspace, stream);
+    return by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
+        return bdlm::launch_conv_block(c, conv_w, conv_b, const_cast<float *>(conv_pool), false,
+                                       workspace, stream);
+    });
 }
 
 int bdlm_check_conv_commit(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
@@ -463,7 +514,9 @@ int bdlm_conv_commit_boundary(const bdlm_desc_t *d, const void *x, const void *d
                                     y_clean, workspace, workspace_bytes);
     if (rc != BDLM_OK) return rc;
     const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
-    rc = bdlm::launch_conv_block(a, conv_w, conv_b, conv_pool, true, workspace, stream);
+    rc = by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
+        return bdlm::launch_conv_block(c, conv_w, conv_b, conv_pool, true, workspace, stream);
+    });
     if (rc != BDLM_OK) return rc;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;
@@ -493,7 +546,9 @@ int bdlm_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const floa
                                 workspace, workspace_bytes);
     if (rc != BDLM_OK) return rc;
     const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D, h_pool, slot_idx, y_fwd);
-    rc = bdlm::launch_prefill(a, d->block_len, workspace, stream);
+    rc = by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
+        return bdlm::launch_prefill(c, d->block_len, workspace, stream);
+    });
     if (rc != BDLM_OK) return rc;
     for (int64_t b = 0; b < d->batch; ++b) {
         const int64_t s = slot_idx ? slot_idx[b] : b;

@@ -48,6 +48,18 @@ __device__ __forceinline__ void split4(f32x4 v, s16x4 &hi, s16x4 &lo) {
     lo = __builtin_bit_cast(s16x4, uint2{cvt_pk_bf16(r0, r1), cvt_pk_bf16(r2, r3)});
 }
 
+// v = hi + mid + lo + O(2^-26 |v|): three bf16 terms, each the rounded remainder of the
+// previous ones (the remainders v - hi and v - hi - mid are exact in fp32).  Operands of
+// state updates whose results are carried over many blocks use three terms: the
+// two-term residual (2^-18 per input) adds up across the tokens a state remembers.
+__device__ __forceinline__ void split4x3(f32x4 v, s16x4 &hi, s16x4 &mid, s16x4 &lo) {
+    split4(v, hi, mid);
+    f32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = (v[i] - bf16_to_f32(hi[i])) - bf16_to_f32(mid[i]);
+    lo = __builtin_bit_cast(s16x4, uint2{cvt_pk_bf16(r[0], r[1]), cvt_pk_bf16(r[2], r[3])});
+}
+
 // Materialise v here: later code depends on this point, so the compiler can neither
 // sink the computation of v below it nor hoist its uses above it.
 __device__ __forceinline__ void pin(float &v) { asm volatile("" : "+v"(v)); }

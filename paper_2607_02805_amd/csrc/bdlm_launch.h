@@ -76,7 +76,14 @@ inline int64_t full_window_workspace(int64_t batch, int64_t nheads, int64_t dsta
 }
 inline int64_t prefill_workspace(int64_t batch, int64_t nheads, int64_t dstate, int64_t T) {
     if (batch == 0 || T == 0) return 0;
-    return seq_plan(batch, nheads, dstate, T, 1).total_bytes;
+    const int64_t full = seq_plan(batch, nheads, dstate, T, 1).total_bytes;
+    if (batch <= BDLM_MAX_SLOT_ROWS) return full;
+    // a slot-mapped call runs in launches of BDLM_MAX_SLOT_ROWS rows, each planned (and
+    // reusing the workspace from its start) on its own
+    const int64_t chunk = seq_plan(BDLM_MAX_SLOT_ROWS, nheads, dstate, T, 1).total_bytes;
+    const int64_t tail_rows = batch % BDLM_MAX_SLOT_ROWS;
+    const int64_t tail = tail_rows ? seq_plan(tail_rows, nheads, dstate, T, 1).total_bytes : 0;
+    return full > chunk ? (full > tail ? full : tail) : (chunk > tail ? chunk : tail);
 }
 
 // Full-window bidirectional scan over T tokens (a.L is ignored): forward pass,

@@ -1,0 +1,75 @@
+// bdlm_probe.hip -- measurement only, not part of libbdlm: a plain streaming kernel with
+// the byte shape of a block-step launch, built into libbdlm_probe.so for the benchmark.
+//
+// Per unit (one (batch row, head) of a block step) it reads a state slab and an input
+// slab and writes an output slab, with the access pattern a bandwidth-bound kernel
+// would use on gfx950 (16-byte nontemporal vector loads, several in flight per lane,
+// 16-byte stores) and no arithmetic beyond folding the loaded values into what it
+// stores.  The time of a launch over the same bytes as a block step is the ceiling a
+// launch of that size reaches here; the benchmark reports it beside the step.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Workgroup `split * unit + part` streams part `part` of unit `unit`'s three slabs.
+// Slab sizes are in 16-byte vectors and divisible by split (checked on the host).
+template <int TPB, int UNR>
+__global__ void __launch_bounds__(TPB) probe_kernel(const f32x4 *st, const f32x4 *in, f32x4 *out,
+                                                    int64_t st_n, int64_t in_n, int64_t out_n,
+                                                    int split) {
+    const int64_t unit = blockIdx.x / split, part = blockIdx.x % split;
+    const int64_t sn = st_n / split, qn = in_n / split, on = out_n / split;
+    const f32x4 *s = st + unit * st_n + part * sn;
+    const f32x4 *q = in + unit * in_n + part * qn;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t i0 = threadIdx.x; i0 < sn; i0 += TPB * UNR) {
+        f32x4 v[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const int64_t i = i0 + u * TPB;
+            v[u] = i < sn ? __builtin_nontemporal_load(s + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) acc += v[u];
+    }
+    for (int64_t i = threadIdx.x; i < qn; i += TPB) acc += __builtin_nontemporal_load(q + i);
+    f32x4 *o = out + unit * out_n + part * on;
+    for (int64_t i = threadIdx.x; i < on; i += TPB) __builtin_nontemporal_store(acc, o + i);
+}
+
+}  // namespace
+
+extern "C" {
+
+// Launch configurations the probe offers (the benchmark keeps the fastest).
+int bdlm_probe_configs(void) { return 6; }
+
+// Enqueue one probe launch: `units` units of st_bytes / in_bytes / out_bytes each
+// (multiples of 16 * split), launch configuration `cfg` (0 .. bdlm_probe_configs() - 1):
+// threads per workgroup and workgroups per unit.  Device pointers, 16-byte aligned.
+// Returns 0, or -1 for a bad argument, -2 if the launch failed.
+int bdlm_probe_stream(const void *st, const void *in, void *out, int64_t units, int64_t st_bytes,
+                      int64_t in_bytes, int64_t out_bytes, int cfg, void *stream) {
+    static const int kSplit[] = {1, 2, 4, 1, 2, 4};
+    static const int kTpb[] = {256, 256, 256, 512, 512, 512};
+    if (cfg < 0 || cfg >= 6 || units <= 0 || !st || !in || !out) return -1;
+    const int split = kSplit[cfg];
+    const int64_t q = 16 * split;
+    if (st_bytes % q || in_bytes % q || out_bytes % q || units * split > (int64_t(1) << 30)) return -1;
+    const dim3 grid(static_cast<unsigned>(units * split));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const f32x4 *S = static_cast<const f32x4 *>(st), *I = static_cast<const f32x4 *>(in);
+    f32x4 *O = static_cast<f32x4 *>(out);
+    if (kTpb[cfg] == 256)
+        hipLaunchKernelGGL((probe_kernel<256, 8>), grid, dim3(256), 0, s, S, I, O, st_bytes / 16,
+                           in_bytes / 16, out_bytes / 16, split);
+    else
+        hipLaunchKernelGGL((probe_kernel<512, 4>), grid, dim3(512), 0, s, S, I, O, st_bytes / 16,
+                           in_bytes / 16, out_bytes / 16, split);
+    return hipGetLastError() == hipSuccess ? 0 : -2;
+}
+
+}  // extern "C"

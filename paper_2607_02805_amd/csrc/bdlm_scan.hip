@@ -716,10 +716,8 @@ bdlm_block_kernel(const KArgs args) {
 #pragma unroll
         for (int k = 0; k < QW; ++k) {
             const int q = q0 + k;
-            s16x4 th[MT], tl[MT];
-            f32x4 tf[MT];
-#pragma unroll
-            for (int jt = 0; jt < MT; ++jt) {
+            // weighted B quad of token tile jt: B[16jt + 4grp + r, 16q + col] w_j
+            auto bw = [&](int jt) {
                 f32x4 v;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -727,16 +725,32 @@ bdlm_block_kernel(const KArgs args) {
                     const float bv = F32 ? sBff[e] : bf16_to_f32(static_cast<short>(sBh[e]));
                     v[r] = bv * wj[jt][r];
                 }
-                if constexpr (F32) tf[jt] = v;
-                else split4(v, th[jt], tl[jt]);
-            }
+                return v;
+            };
             f32x4 acc = hq[k] * keep;
             if constexpr (F32) {
 #pragma unroll
-                for (int jt = 0; jt < MT; ++jt) acc = mma_q32(tf[jt], xquad(jt), acc);
+                for (int jt = 0; jt < MT; ++jt) acc = mma_q32(bw(jt), xquad(jt), acc);
             } else {
-                acc = mma_quads<MT>(th, xq, acc);
-                acc = mma_quads<MT>(tl, xq, acc);
+                // the weighted B is split into three bf16 terms (the committed state is
+                // carried over every later block, so its error must stay at fp32 level),
+                // one pair of token tiles at a time
+#pragma unroll
+                for (int jt = 0; jt < MT; jt += 2) {
+                    s16x4 h0, m0, l0;
+                    split4x3(bw(jt), h0, m0, l0);
+                    if (jt + 1 < MT) {
+                        s16x4 h1, m1, l1;
+                        split4x3(bw(jt + 1), h1, m1, l1);
+                        acc = mma_k32(h0, h1, xq[jt], xq[jt + 1], acc);
+                        acc = mma_k32(m0, m1, xq[jt], xq[jt + 1], acc);
+                        acc = mma_k32(l0, l1, xq[jt], xq[jt + 1], acc);
+                    } else {
+                        acc = mma_k16(h0, xq[jt], acc);
+                        acc = mma_k16(m0, xq[jt], acc);
+                        acc = mma_k16(l0, xq[jt], acc);
+                    }
+                }
             }
             __builtin_nontemporal_store(acc, reinterpret_cast<f32x4 *>(hs + q * 16 * kP));
         }

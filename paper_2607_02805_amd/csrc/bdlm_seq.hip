@@ -402,13 +402,17 @@ __device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4
 template <bool F32> struct BtOps;
 template <> struct BtOps<false> { s16x4 h[4]; };
 template <> struct BtOps<true> { f32x4 f[4]; };
-// weighted x quads: bf16 hi + lo (bf16 storage) or fp32 (fp32 storage)
-template <bool F32> struct WOps;
-template <> struct WOps<false> { s16x4 h[4], l[4]; };
-template <> struct WOps<true> { f32x4 f[4]; };
-template <bool F32>
-__device__ __forceinline__ void w_set(WOps<F32> &o, int jt, f32x4 v) {
+// weighted x quads: bf16 hi + lo, or hi + mid + lo when T3 (bf16 storage), or fp32 (fp32
+// storage).  T3 is used where the updated state leaves the kernels (a cache, the states
+// entering blocks): carried over many blocks, a two-term split's 2^-18 residual per
+// input adds up to more than the parity bar allows on states near zero.
+template <bool F32, bool T3 = false> struct WOps;
+template <bool T3> struct WOps<false, T3> { s16x4 h[4], l[4], m[T3 ? 4 : 1]; };
+template <bool T3> struct WOps<true, T3> { f32x4 f[4]; };
+template <bool F32, bool T3>
+__device__ __forceinline__ void w_set(WOps<F32, T3> &o, int jt, f32x4 v) {
     if constexpr (F32) o.f[jt] = v;
+    else if constexpr (T3) split4x3(v, o.h[jt], o.m[jt], o.l[jt]);
     else split4(v, o.h[jt], o.l[jt]);
 }
 template <int NS, bool F32, bool SWZ = false>
@@ -420,8 +424,8 @@ __device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, int q, i
         else o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
     }
 }
-template <bool F32>
-__device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const WOps<F32> &w, f32x4 acc) {
+template <bool F32, bool T3>
+__device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const WOps<F32, T3> &w, f32x4 acc) {
     if constexpr (F32) {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) acc = mma_f32q(o.f[jt], w.f[jt], acc);
@@ -430,6 +434,7 @@ __device__ __forceinline__ f32x4 bt_mma(const BtOps<F32> &o, const WOps<F32> &w,
         for (int jt = 0; jt < 4; jt += 2) {
             acc = mma_k32(o.h[jt], o.h[jt + 1], w.h[jt], w.h[jt + 1], acc);
             acc = mma_k32(o.h[jt], o.h[jt + 1], w.l[jt], w.l[jt + 1], acc);
+            if constexpr (T3) acc = mma_k32(o.h[jt], o.h[jt + 1], w.m[jt], w.m[jt + 1], acc);
         }
     }
     return acc;
@@ -487,6 +492,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         if constexpr (BOTH) R[q] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     float off = 0.f;   // log2-decay of the segment's tokens before the current chunk
+    // forward-only segment states become cached or emitted states: three-term splits
+    constexpr bool T3 = !BOTH;
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
@@ -497,15 +504,15 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
 
         const float tot = sCs[kC - 1];
-        WOps<F32> wf, wr;
+        WOps<F32, T3> wf, wr;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             s16x4 xh, xl;
             f32x4 xv;
             x_operand<F32>(sXt[F32 ? (4 * jt + grp) * kP + p : xt_slot(4 * jt + grp, p)], xh, xl, xv);
-            w_set<F32>(wf, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv);
+            w_set(wf, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv);
             if constexpr (BOTH)
-                w_set<F32>(wr, jt,
+                w_set(wr, jt,
                            *reinterpret_cast<const f32x4 *>(&sWr[16 * jt + 4 * grp]) * xv * ex2(off));
         }
         const float keep = ex2(tot);
@@ -514,8 +521,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
             if (q + 1 < QN) bt_read<NS, F32, !F32>(nxt, sBt, q + 1, grp, col);
-            F[q] = bt_mma<F32>(cur, wf, F[q] * keep);
-            if constexpr (BOTH) R[q] = bt_mma<F32>(cur, wr, R[q]);
+            F[q] = bt_mma(cur, wf, F[q] * keep);
+            if constexpr (BOTH) R[q] = bt_mma(cur, wr, R[q]);
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -536,9 +543,13 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 // SUB > 0 (forward, with an emission pool): 64-token chunks holding blocks of SUB (16
 // or 32) tokens; the state is carried block by block and the state entering every
 // block is written.  SUB == 0: one emitted block per chunk of cstride tokens.
-template <int NS, bool F32, bool REV, int SUB>
+// T3PAR: the carried state is written out (a cache commit or emitted block states), so
+// its updates use three-term splits (always for SUB > 0).
+template <int NS, bool F32, bool REV, int SUB, bool T3PAR = false>
 __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(const SeqArgs a) {
     static_assert(SUB == 0 || (!REV && (SUB == 16 || SUB == 32)), "block length");
+    static_assert(!(REV && T3PAR), "the reverse pass keeps no state");
+    constexpr bool T3 = T3PAR || SUB > 0;
     using G = Geo<NS, F32>;
     constexpr int QN = G::QN;
     constexpr int IMG = G::IMG;
@@ -784,7 +795,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     const float keepb = ex2(cs_end - cs_prev);
                     cs_prev = cs_end;
                     // this block's tokens, weighted to its end: 2^(cs_end - cs_j) dt_j x_j
-                    WOps<F32> wb;
+                    WOps<F32, T3> wb;
 #pragma unroll
                     for (int jt = sb * JPB; jt < (sb + 1) * JPB; ++jt) {
                         const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs[16 * jt + 4 * grp]);
@@ -792,7 +803,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                         f32x4 wv;
 #pragma unroll
                         for (int r = 0; r < 4; ++r) wv[r] = ex2(cs_end - csq[r]) * dtq[r];
-                        w_set<F32>(wb, jt, wv * xv(jt));
+                        w_set(wb, jt, wv * xv(jt));
                     }
                     BtOps<F32> cur;
 #pragma unroll
@@ -805,9 +816,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                                 acc = mma_f32q(cur.f[jt], wb.f[jt], acc);
                         } else if constexpr (JPB == 2) {
                             acc = mma_k32(cur.h[2 * sb], cur.h[2 * sb + 1], wb.h[2 * sb], wb.h[2 * sb + 1], acc);
+                            acc = mma_k32(cur.h[2 * sb], cur.h[2 * sb + 1], wb.m[2 * sb], wb.m[2 * sb + 1], acc);
                             acc = mma_k32(cur.h[2 * sb], cur.h[2 * sb + 1], wb.l[2 * sb], wb.l[2 * sb + 1], acc);
                         } else {
                             acc = mma_k16(cur.h[sb], wb.h[sb], acc);
+                            acc = mma_k16(cur.h[sb], wb.m[sb], acc);
                             acc = mma_k16(cur.h[sb], wb.l[sb], acc);
                         }
                         S[q] = acc;
@@ -829,17 +842,17 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         // carry the state across the chunk (not after the last one unless it is kept)
         if (c + 1 == nch && !a.pool_out) break;
         const float keep = ex2(sCs[kC - 1]);
-        WOps<F32> wx;
+        WOps<F32, T3> wx;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
-            w_set<F32>(wx, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv(jt));
+            w_set(wx, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv(jt));
         BtOps<F32> cur, nxt;
         bt_read<NS, F32>(cur, sBt, 0, grp, col);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
             // the next tile's operands are read while this tile's MFMAs run
             if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, grp, col);
-            S[q] = bt_mma<F32>(cur, wx, S[q] * keep);
+            S[q] = bt_mma(cur, wx, S[q] * keep);
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -946,6 +959,9 @@ hipError_t out_launch(const SeqArgs &k, bool rev, unsigned grid, hipStream_t s) 
     if (rev)
         hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, true, 0>), dim3(grid), dim3(kThreads), 0, s,
                            k);
+    else if (k.pool_out || k.emit)   // the carried state is written out
+        hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false, 0, true>), dim3(grid), dim3(kThreads),
+                           0, s, k);
     else
         hipLaunchKernelGGL((bdlm_seg_out_kernel<NS, F32, false, 0>), dim3(grid), dim3(kThreads), 0,
                            s, k);

@@ -69,3 +69,36 @@ def to_host(t):
     if t.dtype == torch.bfloat16:
         return t.view(torch.int16).numpy().view(np.uint16).copy()
     return t.numpy().copy()
+
+
+def edge_cover(batch: int, nheads: int) -> list:
+    """(rows, heads) index sets covering every head of the first and last batch rows and
+    every batch row of the first and last heads (each pair once): a full-size parity
+    check on them meets every XCD's share of the remapped grid at its ends."""
+    rows = sorted({0, batch - 1})
+    mid = [b for b in range(batch) if b not in rows]
+    cover = [(rows, list(range(nheads)))]
+    if mid:
+        cover.append((mid, sorted({0, nheads - 1})))
+    return cover
+
+
+def host_slice(v: dict, rows: list, heads: list, hp: dict) -> dict:
+    """Stored bytes of batch rows ``rows`` and heads ``heads`` of device inputs ``v`` (x, dt,
+    B, C; one group), with the per-head parameters ``hp`` of those heads."""
+    r = torch.as_tensor(rows, device=v["x"].device)
+    h = torch.as_tensor(heads, device=v["x"].device)
+    out = {"x": to_host(v["x"].index_select(0, r).index_select(2, h)),
+           "dt": to_host(v["dt"].index_select(0, r).index_select(2, h)),
+           "B": to_host(v["B"].index_select(0, r)), "C": to_host(v["C"].index_select(0, r))}
+    for k in ("A", "D", "D_rev"):
+        a = hp[k]
+        out[k] = (a.cpu().numpy() if torch.is_tensor(a) else np.asarray(a))[heads].copy()
+    return out
+
+
+def pick(t, rows: list, heads: list, head_dim: int = 2):
+    """Rows ``rows`` and heads ``heads`` (on axis ``head_dim``) of a device tensor."""
+    r = torch.as_tensor(rows, device=t.device)
+    h = torch.as_tensor(heads, device=t.device)
+    return t.index_select(0, r).index_select(head_dim, h)

@@ -147,9 +147,18 @@ def test_slots(L):
     assert check_step(L, d, ptrs(), nslots=4, slots=np.array([-1, 0, 1], np.int32)) == bd.E_SLOT
     assert check_step(L, d, ptrs(), nslots=2) == bd.E_SLOT        # identity needs batch <= nslots
     assert check_step(L, d, ptrs(), nslots=0) == bd.E_SHAPE
-    big = desc(batch=bd.MAX_SLOT_ROWS + 1)
-    slots = np.zeros(bd.MAX_SLOT_ROWS + 1, np.int32)
-    assert check_step(L, big, ptrs(), nslots=4, slots=slots) == bd.E_SHAPE
+    # slot tables longer than one launch's table are accepted (the call is split into
+    # launches of MAX_SLOT_ROWS rows); duplicates anywhere in a commit's table are refused
+    big = desc(batch=4 * bd.MAX_SLOT_ROWS + 7)
+    slots = np.arange(4 * bd.MAX_SLOT_ROWS + 7, dtype=np.int32)[::-1].copy()
+    assert check_step(L, big, ptrs(), nslots=len(slots), slots=slots) == bd.OK
+    assert check_commit(L, big, ptrs(), nslots=len(slots), slots=slots) == bd.OK
+    dup = slots.copy()
+    dup[-1] = dup[3]
+    assert check_step(L, big, ptrs(), nslots=len(slots), slots=dup) == bd.OK
+    assert check_commit(L, big, ptrs(), nslots=len(slots), slots=dup) == bd.E_SLOT
+    slots[600] = len(slots)
+    assert check_step(L, big, ptrs(), nslots=len(slots), slots=slots) == bd.E_SLOT
     # repeated slots are fine for a step, not for a commit
     assert check_commit(L, d, ptrs(), slots=np.array([3, 0, 3], np.int32)) == bd.E_SLOT
     assert check_commit(L, d, ptrs(), slots=np.array([3, 0, 1], np.int32)) == bd.OK

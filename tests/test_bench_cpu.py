@@ -51,5 +51,25 @@ def test_traffic_is_dropped_once_the_kernel_source_changes(monkeypatch):
     value = bench.measured_traffic()
     if value is not None:                          # summary taken on the current source
         assert value > bench.step_bytes(16, 32, 64, 128, 1, 32) * 0.9
-    monkeypatch.setattr(bench, "kernel_source_sha", lambda: "0" * 16 if good != "0" * 16 else "1" * 16)
+    monkeypatch.setattr(bench, "kernel_source_sha",
+                        lambda which="block": "0" * 16 if good != "0" * 16 else "1" * 16)
     assert bench.measured_traffic() is None
+
+
+def test_profile_fields_need_a_matching_source_hash(tmp_path, monkeypatch):
+    p = tmp_path / "summary.md"
+    p.write_text(f"# x\n\n- kernel_source_sha256_16: `{bench.kernel_source_sha()}`\n"
+                 "- step_kernel_mean_us: 6.25\n- note: a: b\n")
+    kv = bench.profile_fields(str(p))
+    assert bench._num(kv, "step_kernel_mean_us") == 6.25 and kv["note"] == "a: b"
+    assert bench._num(kv, "missing") is None
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda which="block": "f" * 16)
+    assert bench.profile_fields(str(p)) == {}
+    assert bench.profile_fields(str(tmp_path / "absent.md")) == {}
+
+
+def test_source_sets_name_existing_files():
+    for which, files in bench.SOURCE_SETS.items():
+        for f in files:
+            assert os.path.exists(os.path.join(bench.CSRC, f)), (which, f)
+        assert len(bench.kernel_source_sha(which)) == 16

@@ -15,7 +15,8 @@ import torch
 
 import bdlm_inputs as bi
 import oracle
-from tests.gpu_util import DEV, REL_TOL, from_pool, pool_dev, rel_err, to_dev, to_host
+from tests.gpu_util import (DEV, REL_TOL, edge_cover, from_pool, host_slice, pick, pool_dev,
+                            rel_err, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -110,9 +111,10 @@ def test_all_block_forward_equals_sampler():
 
 def test_all_block_forward_full_size_sampled():
     """The all-block forward at the size the bench times it (350M layer shape, batch 8, an
-    8,192-token window of 256 blocks of 32 tokens, inputs drawn on the GPU): for sampled
-    (row, head) pairs, the states entering all 256 blocks, the clean stream's forward
-    outputs and the noised stream's outputs against the oracle run on those slices."""
+    8,192-token window of 256 blocks of 32 tokens, inputs drawn on the GPU): for every head
+    of batch rows 0 and 7 and every row of heads 0 and 31, the states entering all 256
+    blocks, the clean stream's forward outputs and the noised stream's outputs against the
+    oracle run on those slices."""
     import paper_2607_02805_amd as bd
     w = bi.Workload("350m-train-window", 8, 32, 64, 128, 1, 32, 8192, True, 1, 5000)
     T, L, K = 8192, 32, 256
@@ -126,21 +128,19 @@ def test_all_block_forward_full_size_sampled():
                                         dhp["A"], dhp["D"], dhp["D_rev"], L, want_clean_y=True)
     torch.cuda.synchronize()
     states = from_pool(s_out).reshape(8, K, 32, 64, 128)
-    for b, h in ((0, 0), (5, 13), (7, 31)):
-        def part(v):
-            s = {"x": to_host(v["x"][b:b + 1, :, h:h + 1]), "dt": to_host(v["dt"][b:b + 1, :, h:h + 1]),
-                 "B": to_host(v["B"][b:b + 1]), "C": to_host(v["C"][b:b + 1])}
-            s.update({k: hp[k][h:h + 1] for k in ("A", "D", "D_rev")})
-            return s
-        cs, ns = part(c), part(n)
-        ref_states, ref_yc = oracle_states(cs, K, L, np.zeros((1, 1, 64, 128)))
-        # the noised blocks as K rows of one block each, stepped from the states entering them
-        rows = {k: (ns[k].reshape(K, L, *ns[k].shape[2:]) if k in ("x", "dt", "B", "C") else ns[k])
-                for k in ns}
-        ref_y = oracle.block_step(rows, ref_states[:, 0])
-        e = (rel_err(states[b, :, h], ref_states[:, 0, 0]), rel_err(yc[b:b + 1, :, h:h + 1], ref_yc),
-             rel_err(y[b:b + 1, :, h:h + 1].reshape(K, L, 1, 64), ref_y))
-        say("  (b, h) =", (b, h), "rel err states, clean y, noised y", e)
+    for rows, heads in edge_cover(w.batch, w.nheads):
+        cs, ns = host_slice(c, rows, heads, hp), host_slice(n, rows, heads, hp)
+        R, Hs = len(rows), len(heads)
+        ref_states, ref_yc = oracle_states(cs, K, L, np.zeros((R, Hs, 64, 128)))   # [K, R, Hs, ..]
+        # the noised blocks as R * K rows of one block each, stepped from their entering states
+        blk = {k: (ns[k].reshape(R * K, L, *ns[k].shape[2:]) if k in ("x", "dt", "B", "C") else ns[k])
+               for k in ns}
+        ref_y = oracle.block_step(blk, np.ascontiguousarray(ref_states.swapaxes(0, 1)).reshape(
+            R * K, Hs, 64, 128))
+        got_states = states[rows][:, :, heads]                                        # [R, K, Hs, ..]
+        e = (rel_err(got_states, ref_states.swapaxes(0, 1)), rel_err(pick(yc, rows, heads), ref_yc),
+             rel_err(pick(y, rows, heads).reshape(R * K, L, Hs, 64), ref_y))
+        say("  rows", rows, "heads", heads, "rel err states, clean y, noised y", e)
         assert max(e) <= REL_TOL
 
 
