@@ -287,6 +287,28 @@ int bdlm_prefill(const bdlm_desc_t *desc, const void *x, const void *dt, const f
                  void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
+ * bdlm_prefill without a workspace argument, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments, semantics, bookkeeping and errors as bdlm_prefill; the
+ * segment states live in a device array the library owns (BDLM_SCRATCH_BYTES per
+ * device, held from the time the library's code is loaded on a device until the
+ * process ends).  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).  When the standard segment plan needs more than BDLM_SCRATCH_BYTES it uses
+ * fewer, longer segments; a call whose batch * nheads states do not fit even with one
+ * segment (batch * nheads * 64 * dstate * 4 bytes above BDLM_SCRATCH_BYTES, per run of
+ * BDLM_MAX_SLOT_ROWS rows when slot_idx is given) returns BDLM_E_WORKSPACE and
+ * enqueues nothing.  Nothing in the scratch needs to start at zero: every value a call
+ * reads was written by that call.  All calls on one device share its scratch, so calls
+ * that may run concurrently on one device (on different streams) race; serialise them.
+ */
+#define BDLM_SCRATCH_BYTES ((int64_t)64 << 20)
+int bdlm_prefill_noalloc(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, float *h_pool,
+                         int64_t nslots, const int32_t *slot_idx, int64_t *n_committed,
+                         int64_t *n_blocks, int64_t expected_block_index,
+                         int64_t blocks_in_prefix, float *y_fwd, void *stream);
+
+/*
  * All-block states of a clean sequence (the training computation of Fig. 1: every
  * block of a training window is denoised from the forward boundary state of its
  * clean prefix, Eq. prefix-cache-loss).  The clean sequence is n_blocks blocks of

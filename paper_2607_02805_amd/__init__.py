@@ -34,6 +34,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "bdlm.h")
 HEADDIM = 64
 MAX_BLOCK_LEN = 64
 MAX_SLOT_ROWS = 256
+SCRATCH_BYTES = 64 << 20     # BDLM_SCRATCH_BYTES: the no-allocation prefill's device scratch
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 
@@ -118,6 +119,8 @@ def lib() -> ctypes.CDLL:
                                          i64, i64, fp, vp, i64]
         L.bdlm_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p, i64,
                                    i64, fp, vp, i64, vp]
+        L.bdlm_prefill_noalloc.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p,
+                                           i64, i64, fp, vp]
         f32 = ctypes.c_float
         L.bdlm_check_gated_rmsnorm.argtypes = [i64, i64, i64, i64, ctypes.c_int32, fp, vp, i64,
                                                i64, fp, f32, fp]
@@ -133,7 +136,8 @@ def lib() -> ctypes.CDLL:
                      "bdlm_block_boundary_states", "bdlm_check_block_step_sep",
                      "bdlm_scan_block_step_sep", "bdlm_conv_workspace",
                      "bdlm_check_conv_block_step", "bdlm_conv_block_step",
-                     "bdlm_check_conv_commit", "bdlm_conv_commit_boundary"):
+                     "bdlm_check_conv_commit", "bdlm_conv_commit_boundary",
+                     "bdlm_prefill_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -498,6 +502,38 @@ def prefill(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_ind
     del keep, wkeep
     if rc != OK:
         raise BdlmError(rc, "bdlm_prefill")
+    return y_fwd
+
+
+def prefill_noalloc(x, dt, A, B, C, D, h_pool, n_committed, n_blocks, expected_block_index=-1,
+                    blocks_in_prefix=0, slot_idx=None, y_fwd=None, stream=None):
+    """:func:`prefill` through ``bdlm_prefill_noalloc``: no workspace and no allocation, by
+    the library or here (``y_fwd`` is None or a caller tensor), so it can run inside a HIP
+    graph capture or a loop that must not allocate.  The segment states use the device
+    scratch the library owns (``SCRATCH_BYTES`` per device); calls that overlap on one
+    device race."""
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    nslots = h_pool.shape[0]
+    for a in (n_committed, n_blocks):
+        if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
+                or a.shape != (nslots,):
+            raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
+    if y_fwd is True:
+        raise ValueError("prefill_noalloc allocates nothing: pass y_fwd as a tensor or None")
+    if y_fwd is not None:
+        y_fwd = _out(y_fwd, (d.batch, d.block_len, H, HEADDIM), "y_fwd")
+    yp = None if y_fwd is None else _dev_ptr(y_fwd, "y_fwd")
+    keep, sp = _slots(slot_idx, d.batch)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_prefill_noalloc(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _pool(h_pool, H, N), nslots,
+        sp, n_committed.ctypes.data_as(i64p), n_blocks.ctypes.data_as(i64p),
+        int(expected_block_index), int(blocks_in_prefix), yp, _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_prefill_noalloc")
     return y_fwd
 
 

@@ -558,6 +558,47 @@ int bdlm_prefill(const bdlm_desc_t *d, const void *x, const void *dt, const floa
     return BDLM_OK;
 }
 
+int bdlm_prefill_noalloc(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                         const void *B, const void *C, const float *D, float *h_pool,
+                         int64_t nslots, const int32_t *slot_idx, int64_t *n_committed,
+                         int64_t *n_blocks, int64_t expected_block_index,
+                         int64_t blocks_in_prefix, float *y_fwd, void *stream) {
+    // the checks of bdlm_prefill with the workspace test replaced by the scratch plan
+    void *const any = reinterpret_cast<void *>(uintptr_t(256));
+    int rc = bdlm_check_prefill(d, x, dt, A, B, C, D, h_pool, nslots, slot_idx, n_committed,
+                                n_blocks, expected_block_index, blocks_in_prefix, y_fwd, any,
+                                INT64_MAX);
+    if (rc != BDLM_OK) return rc;
+    const int64_t rows = slot_idx && d->batch > BDLM_MAX_SLOT_ROWS ? BDLM_MAX_SLOT_ROWS : d->batch;
+    bdlm::SeqPlan plan;
+    if (d->batch > 0 && d->block_len > 0 &&
+        !bdlm::prefill_plan_capped(rows, d->nheads, d->dstate, d->block_len, BDLM_SCRATCH_BYTES,
+                                   &plan))
+        return BDLM_E_WORKSPACE;
+    void *ws = nullptr;
+    if (d->batch > 0 && d->block_len > 0) {
+        rc = bdlm::scratch_pointer(&ws);
+        if (rc != BDLM_OK) return rc;
+    }
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D, h_pool, slot_idx, y_fwd);
+    rc = by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) -> int {
+        if (c.batch == 0 || d->block_len == 0) return BDLM_OK;   // nothing to enqueue
+        bdlm::SeqPlan p;
+        // a shorter last run of rows fits whenever a full one does
+        if (!bdlm::prefill_plan_capped(c.batch, d->nheads, d->dstate, d->block_len,
+                                       BDLM_SCRATCH_BYTES, &p))
+            return BDLM_E_WORKSPACE;
+        return bdlm::launch_prefill(c, d->block_len, ws, stream, &p);
+    });
+    if (rc != BDLM_OK) return rc;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        n_committed[s] += d->block_len;
+        n_blocks[s] += blocks_in_prefix;
+    }
+    return BDLM_OK;
+}
+
 static int state_permute(const float *src, float *dst, int64_t nstates, int64_t dstate,
                          bool to_pool, void *stream) {
     if (!src || !dst) return BDLM_E_NULL;

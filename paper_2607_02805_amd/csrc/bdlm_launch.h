@@ -92,8 +92,39 @@ int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream);
 
 // Forward scan over T tokens continuing the states in a.h_pool (via a.slots),
 // writing them back; a.y (optional) receives the forward outputs.
-// ws: prefill_workspace bytes.
-int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream);
+// ws: prefill_workspace bytes, or plan->total_bytes when a plan is given (nullptr: the
+// standard plan seq_plan(a.batch, a.nheads, a.dstate, T, 1)).
+int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream,
+                   const SeqPlan *plan = nullptr);
+
+// A prefill plan whose workspace fits in cap bytes: the standard plan if it fits, else
+// fewer and longer segments (the same computation with fewer workgroups).  False if
+// even one segment per row and head needs more than cap.
+inline bool prefill_plan_capped(int64_t batch, int64_t nheads, int64_t dstate, int64_t T,
+                                int64_t cap, SeqPlan *out) {
+    SeqPlan p = seq_plan(batch, nheads, dstate, T, 1);
+    if (p.total_bytes > cap) {
+        const int64_t units = batch * nheads;
+        const int64_t per_seg = units * int64_t(BDLM_HEADDIM) * dstate * 4;
+        int64_t nseg = (cap - (units * p.nseg * 4 + 255) / 256 * 256) / per_seg;
+        if (nseg < 1) return false;
+        int64_t S = (T + nseg - 1) / nseg;
+        S = (S + 63) / 64 * 64;
+        if (S < 256) S = 256;
+        p.seg_len = S;
+        p.nseg = (T + S - 1) / S;
+        p.state_bytes = units * p.nseg * int64_t(BDLM_HEADDIM) * dstate * 4;
+        p.total_bytes = p.state_bytes + (units * p.nseg * 4 + 255) / 256 * 256;
+        if (p.total_bytes > cap) return false;
+    }
+    *out = p;
+    return true;
+}
+
+// The library's own device scratch of the no-allocation prefill: BDLM_SCRATCH_BYTES,
+// 256-byte aligned, one array per device (its address on the current device, looked
+// up once per device).  BDLM_OK, or BDLM_E_LAUNCH if the runtime cannot resolve it.
+int scratch_pointer(void **out);
 
 // States entering every block of a clean sequence of nblocks blocks of a.L tokens:
 // s_out[(row * nblocks + k) * nheads + head] (pool layout) = the forward state after

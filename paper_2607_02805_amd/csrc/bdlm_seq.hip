@@ -1099,10 +1099,10 @@ int launch_full_window(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
     return BDLM_OK;
 }
 
-int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream) {
+int launch_prefill(const LaunchArgs &a, int64_t T, void *ws, void *stream, const SeqPlan *plan) {
     if (a.batch == 0 || T == 0) return BDLM_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const SeqPlan pl = seq_plan(a.batch, a.nheads, a.dstate, T, 1);
+    const SeqPlan pl = plan ? *plan : seq_plan(a.batch, a.nheads, a.dstate, T, 1);
     SeqArgs k = seq_args(a, T, pl, ws);
     const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads * pl.nseg);
     const bool f32 = !a.bf16;

@@ -563,3 +563,25 @@ def test_binding_rejects_slot_list_of_wrong_length(slots):
         bd.commit_boundary(*_args(v), pool, nc, nb, slot_idx=slots)
     with pytest.raises(ValueError, match="exactly 2 slot indices"):
         bd.prefill(*_args(v)[:6], pool, nc, nb, slot_idx=slots)
+
+
+def test_noalloc_prefill_host_refusals(L):
+    """bdlm_prefill_noalloc's checks run before it touches the device: argument errors and
+    a request its scratch cannot hold are refused without a GPU, bookkeeping untouched."""
+    i64 = ctypes.POINTER(ctypes.c_int64)
+    nc, nb = np.zeros(4, np.int64), np.zeros(4, np.int64)
+
+    def call(d, p, nslots=4, expect=-1):
+        return L.bdlm_prefill_noalloc(ctypes.byref(d), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                      p["D"], p["h"], nslots, None, nc.ctypes.data_as(i64),
+                                      nb.ctypes.data_as(i64), expect, 0, None, None)
+    assert call(desc(batch=2, L=300), ptrs(x=None)) == bd.E_NULL
+    assert call(desc(batch=2, L=300), ptrs(B=FAKE + 0x3008)) == bd.E_ALIGN
+    nb[:] = 1
+    assert call(desc(batch=2, L=300), ptrs(), expect=0) == bd.E_OFFSET
+    # 80 rows x 32 heads x 64 x 128 fp32 = 80 MiB of segment states even as one segment
+    big = desc(batch=80, H=32, N=128, L=256)
+    assert call(big, ptrs(), nslots=80) == bd.E_WORKSPACE
+    assert nb.tolist() == [1, 1, 1, 1] and nc.tolist() == [0] * 4
+    # nothing to do: succeeds without a device
+    assert call(desc(batch=0, L=300), ptrs(x=None, dt=None, B=None, C=None)) == bd.OK
