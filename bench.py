@@ -576,8 +576,34 @@ def run_variants(args) -> dict:
         "step_gbs": round(sb / t_step / 1e9, 1),
         "active_tokens_per_s": round(16 * 256 / t_step, 1)}
     del pools, y, yc
-    # separate reverse-direction inputs, L = 32
+    # commit of the clean block + the next block's first step in one launch (the state read
+    # once), against the commit launch followed by the step launch (350M layer, L 32)
     w = bi.WORKLOADS[3]
+    cl = to_dev(bi.commit_inputs(w), dev)
+    nx = to_dev(bi.block_inputs(w, 1), dev)
+    pools = [torch.randn(bd.pool_shape(16, 32, 128), device=dev) * 0.01 for _ in range(nl)]
+    y = torch.empty((16, 32, 32, 64), device=dev)
+    yc = torch.empty_like(y)
+    z = np.zeros(16, np.int64)
+    t_cs = _graph_time(lambda li: bd.commit_step(
+        (cl["x"], cl["dt"], cl["B"], cl["C"]), (nx["x"], nx["dt"], nx["B"], nx["C"]), cl["A"],
+        cl["D"], cl["D_rev"], pools[li], z.copy(), z.copy(), y_clean=yc, y_next=y), nl)
+
+    def two(li):
+        bd.commit_boundary(cl["x"], cl["dt"], cl["A"], cl["B"], cl["C"], cl["D"], cl["D_rev"],
+                           pools[li], z.copy(), z.copy(), y_clean=yc)
+        bd.scan_block_step(nx["x"], nx["dt"], nx["A"], nx["B"], nx["C"], nx["D"], nx["D_rev"],
+                           pools[li], y=y)
+    t_two = _graph_time(two, nl)
+    sb = step_bytes(16, 32, 64, 128, 1, 32)
+    cb = commit_bytes(16, 32, 64, 128, 1, 32)
+    fused_bytes = cb + sb - 16 * 32 * 64 * 128 * 4      # one state read fewer
+    out["commit_step_L32"] = {
+        "workload": "350m-mamba-layer-b16-L32-commit+next-step",
+        "fused_us": round(t_cs * 1e6, 2), "commit_then_step_us": round(t_two * 1e6, 2),
+        "fused_bytes": fused_bytes, "fused_gbs": round(fused_bytes / t_cs / 1e9, 1)}
+    del pools, y, yc
+    # separate reverse-direction inputs, L = 32
     f = to_dev(bi.block_inputs(w, 0), dev)
     r = to_dev(bi.block_inputs(w, 1), dev)
     pools = [torch.zeros(bd.pool_shape(16, 32, 128), device=dev) for _ in range(nl)]

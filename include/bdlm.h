@@ -170,6 +170,37 @@ int bdlm_commit_boundary(const bdlm_desc_t *desc, const void *x, const void *dt,
                          int64_t expected_block_index, float *y_clean, void *stream);
 
 /*
+ * Commit of the clean block followed by the first denoising step of the next block, in
+ * the order the sampler takes them, as one call: the same results as
+ * bdlm_commit_boundary(clean block) and then bdlm_scan_block_step(next block's noised
+ * inputs) on the same stream (Eq. boundary-state, then Eq. partial-reverse from the new
+ * state).  For bf16 blocks of at most 32 tokens it is one launch that reads each cached
+ * state once, updates it in registers, writes it and continues the next block's step
+ * from it, saving the step's read of the state; otherwise the two launches are enqueued.
+ * The paper runs the clean forward pass and the next block's steps as separate passes;
+ * this entry point is an alternative ordering of the same computation, not a change of
+ * its results.
+ *
+ * x, dt, B, C                      the clean block (as for bdlm_commit_boundary);
+ * x_next, dt_next, B_next, C_next  the next block's noised inputs at its first step,
+ *              with desc's shapes and strides (same block length, same slots);
+ * A, D, D_rev  shared by both (one layer).
+ * h_pool, nslots, slot_idx, n_committed, n_blocks, expected_block_index, y_clean
+ *              as for bdlm_commit_boundary (slots distinct, bookkeeping advanced by one
+ *              block on success).
+ * y_next       device fp32 [batch][block_len][nheads][64], 16-byte aligned, required:
+ *              the next block's step outputs, from the committed state.
+ * Blocks of at most BDLM_MAX_BLOCK_LEN tokens.
+ * Errors: as bdlm_commit_boundary, with the next block's inputs checked as a step's.
+ */
+int bdlm_commit_step(const bdlm_desc_t *desc, const void *x, const void *dt, const float *A,
+                     const void *B, const void *C, const float *D, const float *D_rev,
+                     const void *x_next, const void *dt_next, const void *B_next,
+                     const void *C_next, float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                     int64_t *n_committed, int64_t *n_blocks, int64_t expected_block_index,
+                     float *y_clean, float *y_next, void *stream);
+
+/*
  * The sequence entry points below split the sequence into segments, one
  * workgroup per (batch row, head, segment), and carry states between segments
  * through a device workspace that the caller allocates (the library allocates
@@ -429,6 +460,13 @@ int bdlm_check_conv_commit(const bdlm_desc_t *desc, const void *x, const void *d
                            const int32_t *slot_idx, const int64_t *n_committed,
                            const int64_t *n_blocks, int64_t expected_block_index,
                            const float *y_clean, const void *workspace, int64_t workspace_bytes);
+int bdlm_check_commit_step(const bdlm_desc_t *desc, const void *x, const void *dt,
+                           const float *A, const void *B, const void *C, const float *D,
+                           const float *D_rev, const void *x_next, const void *dt_next,
+                           const void *B_next, const void *C_next, const float *h_pool,
+                           int64_t nslots, const int32_t *slot_idx, const int64_t *n_committed,
+                           const int64_t *n_blocks, int64_t expected_block_index,
+                           const float *y_clean, const float *y_next);
 int bdlm_check_full_window(const bdlm_desc_t *desc, const void *x, const void *dt,
                            const float *A, const void *B, const void *C, const float *D,
                            const float *D_rev, const float *y, const void *workspace,

@@ -119,6 +119,10 @@ def lib() -> ctypes.CDLL:
                                          i64, i64, fp, vp, i64]
         L.bdlm_prefill.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p, i64,
                                    i64, fp, vp, i64, vp]
+        L.bdlm_commit_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, vp, vp, vp, vp, fp, i64,
+                                       i32p, i64p, i64p, i64, fp, fp, vp]
+        L.bdlm_check_commit_step.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, vp, vp, vp, vp, fp,
+                                             i64, i32p, i64p, i64p, i64, fp, fp]
         L.bdlm_prefill_noalloc.argtypes = [dp, vp, vp, fp, vp, vp, fp, fp, i64, i32p, i64p, i64p,
                                            i64, i64, fp, vp]
         f32 = ctypes.c_float
@@ -137,7 +141,7 @@ def lib() -> ctypes.CDLL:
                      "bdlm_scan_block_step_sep", "bdlm_conv_workspace",
                      "bdlm_check_conv_block_step", "bdlm_conv_block_step",
                      "bdlm_check_conv_commit", "bdlm_conv_commit_boundary",
-                     "bdlm_prefill_noalloc"):
+                     "bdlm_prefill_noalloc", "bdlm_commit_step", "bdlm_check_commit_step"):
             getattr(L, name).restype = ctypes.c_int
         if L.bdlm_abi_version() != 1:
             raise RuntimeError("libbdlm ABI version mismatch")
@@ -416,6 +420,45 @@ def commit_boundary(x, dt, A, B, C, D, D_rev, h_pool, n_committed, n_blocks,
     if rc != OK:
         raise BdlmError(rc, "bdlm_commit_boundary")
     return y_clean
+
+
+def commit_step(clean, nxt, A, D, D_rev, h_pool, n_committed, n_blocks, expected_block_index=-1,
+                slot_idx=None, y_clean=None, y_next=None, stream=None):
+    """Commit the clean block, then run the next block's first denoising step from the
+    committed state, in one call (``clean`` and ``nxt`` are (x, dt, B, C) tuples of the same
+    shapes and strides).  Same results as :func:`commit_boundary` followed by
+    :func:`scan_block_step`; for bf16 blocks of at most 32 tokens one launch reads each
+    state once.  Returns (y_next, y_clean)."""
+    x, dt, B, C = clean
+    xn, dtn, Bn, Cn = nxt
+    for a, b, what in ((x, xn, "x"), (dt, dtn, "dt"), (B, Bn, "B"), (C, Cn, "C")):
+        if tuple(a.shape) != tuple(b.shape) or a.dtype != b.dtype or a.stride() != b.stride():
+            raise ValueError(f"clean and next {what} must share shape, dtype and strides")
+    d = _desc(x, dt, B, C)
+    H, N = d.nheads, d.dstate
+    nslots = h_pool.shape[0]
+    for a in (n_committed, n_blocks):
+        if not isinstance(a, np.ndarray) or a.dtype != np.int64 or not a.flags.c_contiguous \
+                or a.shape != (nslots,):
+            raise ValueError(f"n_committed / n_blocks must be contiguous numpy int64 [{nslots}]")
+    shape = (d.batch, d.block_len, H, HEADDIM)
+    y_next = _out(y_next, shape, "y_next", x.device)
+    if y_clean is not None:
+        y_clean = _out(y_clean, shape, "y_clean", x.device)
+    keep, sp = _slots(slot_idx, d.batch)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    rc = lib().bdlm_commit_step(
+        ctypes.byref(d), _dev_ptr(x, "x"), _dev_ptr(dt, "dt"), _f32_vec(A, H, "A"),
+        _dev_ptr(B, "B"), _dev_ptr(C, "C"), _f32_vec(D, H, "D"), _f32_vec(D_rev, H, "D_rev"),
+        _dev_ptr(xn, "x_next"), _dev_ptr(dtn, "dt_next"), _dev_ptr(Bn, "B_next"),
+        _dev_ptr(Cn, "C_next"), _pool(h_pool, H, N), nslots, sp,
+        n_committed.ctypes.data_as(i64p), n_blocks.ctypes.data_as(i64p),
+        int(expected_block_index), None if y_clean is None else _dev_ptr(y_clean, "y_clean"),
+        _dev_ptr(y_next, "y_next"), _stream_handle(stream))
+    del keep
+    if rc != OK:
+        raise BdlmError(rc, "bdlm_commit_step")
+    return y_next, y_clean
 
 
 def _workspace_bytes(fn, d) -> int:

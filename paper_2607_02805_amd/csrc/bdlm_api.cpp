@@ -437,6 +437,51 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
     return BDLM_OK;
 }
 
+int bdlm_check_commit_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                           const void *B, const void *C, const float *D, const float *D_rev,
+                           const void *x_next, const void *dt_next, const void *B_next,
+                           const void *C_next, const float *h_pool, int64_t nslots,
+                           const int32_t *slot_idx, const int64_t *n_committed,
+                           const int64_t *n_blocks, int64_t expected_block_index,
+                           const float *y_clean, const float *y_next) {
+    int rc = check_common(d, x, dt, A, B, C, D, D_rev, h_pool, nslots, slot_idx);
+    if (rc != BDLM_OK) return rc;
+    rc = check_common(d, x_next, dt_next, A, B_next, C_next, D, D_rev, nullptr, 0, nullptr,
+                      BDLM_MAX_BLOCK_LEN, false);
+    if (rc != BDLM_OK) return rc;
+    if (!y_next && d->batch != 0 && d->block_len != 0) return BDLM_E_NULL;
+    if (!aligned(y_next, 16) || !aligned(y_clean, 16)) return BDLM_E_ALIGN;
+    return check_books(d, slot_idx, n_committed, n_blocks, expected_block_index);
+}
+
+int bdlm_commit_step(const bdlm_desc_t *d, const void *x, const void *dt, const float *A,
+                     const void *B, const void *C, const float *D, const float *D_rev,
+                     const void *x_next, const void *dt_next, const void *B_next,
+                     const void *C_next, float *h_pool, int64_t nslots, const int32_t *slot_idx,
+                     int64_t *n_committed, int64_t *n_blocks, int64_t expected_block_index,
+                     float *y_clean, float *y_next, void *stream) {
+    int rc = bdlm_check_commit_step(d, x, dt, A, B, C, D, D_rev, x_next, dt_next, B_next, C_next,
+                                    h_pool, nslots, slot_idx, n_committed, n_blocks,
+                                    expected_block_index, y_clean, y_next);
+    if (rc != BDLM_OK) return rc;
+    const bdlm::LaunchArgs a = make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
+    const bdlm::LaunchArgs n =
+        make_args(d, x_next, dt_next, A, B_next, C_next, D, D_rev, h_pool, slot_idx, y_next);
+    const int64_t yr = y_row_floats(d, d->block_len);
+    rc = by_row_chunks(a, yr, [&](const bdlm::LaunchArgs &ac) -> int {
+        const int64_t r0 = ac.slots ? ac.slots - a.slots : 0;
+        const bdlm::LaunchArgs nc = rows_of(n, r0, ac.batch, yr);
+        return bdlm::launch_commit_step(ac, nc, nc.y, stream);
+    });
+    if (rc != BDLM_OK) return rc;
+    for (int64_t b = 0; b < d->batch; ++b) {
+        const int64_t s = slot_idx ? slot_idx[b] : b;
+        n_committed[s] += d->block_len;
+        n_blocks[s] += 1;
+    }
+    return BDLM_OK;
+}
+
 int bdlm_conv_workspace(const bdlm_desc_t *d, int64_t *bytes) {
     if (!bytes) return BDLM_E_NULL;
     const int rc = check_desc(d, BDLM_MAX_SEQ_LEN);

@@ -25,6 +25,14 @@ struct LaunchArgs {
 // Arguments are already validated.  Returns BDLM_OK or BDLM_E_LAUNCH.
 int launch_block(const LaunchArgs &a, bool commit, void *stream);
 
+// Commit of the clean block (clean; clean.y: its outputs, or nullptr) followed by the first
+// denoising step of the next block (next's inputs, outputs into y_next) from the updated
+// state, for blocks of at most 64 tokens (next has clean's shapes, slots and parameters).
+// A bf16 block of at most 32 tokens is one launch that reads the state once; otherwise a
+// commit launch and a step launch.
+int launch_commit_step(const LaunchArgs &clean, const LaunchArgs &next, float *y_next,
+                       void *stream);
+
 // A step (or commit) of a block of at most 64 tokens whose reverse branch has inputs of
 // its own: the forward branch of `fwd` from the cached state (skip fwd.D) plus the
 // reverse branch of `rev` (skip rev.D_rev) into y; a commit updates the state from

@@ -62,7 +62,9 @@ struct KArgs {
     const float *A, *D, *D_rev;
     float *h_pool;
     float *y;
-    // kSep: the reverse branch's own inputs (same shapes and strides as the above)
+    float *y2;   // kCS: the next block's step outputs
+    // kSep: the reverse branch's own inputs (same shapes and strides as the above);
+    // kCS: the next block's noised inputs
     const void *x2, *dt2, *Bm2, *Cm2;
     const float *A2;
     int64_t xs_b, xs_t, xs_h;
@@ -86,6 +88,10 @@ struct KArgs {
 // DIR: kBoth computes both branches (one input set for both, Eq. partial-reverse);
 //     kFwd only the forward branch from the cached state (skip D) and stores y;
 //     kRev only the block-local reverse branch (skip D_rev) and adds it onto y;
+//     kCS  commit the clean block (x, dt, B, C; y: its outputs, optional) and then run
+//     the next block's first denoising step (x2, dt2, B2, C2, both branches; outputs
+//     into y2) from the updated state while it is still in registers: one state read,
+//     one state write, the same results as a commit followed by a step;
 //     kSep both branches, each from an input set of its own (x, dt, A, B, C for the
 //     forward branch, x2, dt2, A2, B2, C2 for the reverse one; bf16 storage, no
 //     commit): two Gram matrices, two intra products, one prefix term.  A step whose
@@ -114,7 +120,7 @@ struct KArgs {
 //      dstate quads of the state (the only step that waits for the state loads);
 //      the partial products are summed and y is stored; a commit then adds the
 //      block to each wave's quads of the state in place.
-constexpr int kBoth = 0, kFwd = 1, kRev = 2, kSep = 3;
+constexpr int kBoth = 0, kFwd = 1, kRev = 2, kSep = 3, kCS = 4;
 
 // c += a b over one quad of 16 contraction indices on fp32 MFMA: instruction r takes
 // value r of every lane, i.e. index 4 grp + r of the quad layout.
@@ -173,10 +179,13 @@ __device__ __forceinline__ uint4 gram_tile_bf16(const uint2 *iB, const uint2 *iC
 template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR, bool CV>
 __global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
-    static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep, "direction");
+    static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep || DIR == kCS,
+                  "direction");
+    static_assert(DIR != kCS || (!F32 && COMMIT && !CV), "commit + step: bf16 storage");
     static_assert(!CV || (F32 && (DIR == kFwd || DIR == kRev) && LT <= 32), "convolution staging");
     static_assert(!(COMMIT && DIR == kRev), "a commit updates the forward state");
     constexpr bool SEP = DIR == kSep;
+    constexpr bool TWO = SEP || DIR == kCS;   // a second input set is staged
     static_assert(!(SEP && (F32 || COMMIT)), "separate inputs: bf16 storage, step only");
     constexpr int NT = 256 * NPART;       // threads
     constexpr int NW = 4 * NPART;         // waves
@@ -199,11 +208,12 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) float sDt[64], sCs[64], sEx[64];   // dt, cs, ex per token
     __shared__ float sPar[4];                                          // A[h], D[h], D_rev[h]
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
-    // kSep: the reverse branch's images, x, decay sums and matrix
-    __shared__ __align__(16) uint2 sC2[SEP ? IMG : 1], sB2[SEP ? IMG : 1];
-    __shared__ __align__(16) AT sX2[SEP ? LT * XS : 1];
-    __shared__ __align__(16) float sDt2[SEP ? 64 : 1], sCs2[SEP ? 64 : 1], sEx2[SEP ? 64 : 1];
-    __shared__ __align__(16) uint4 sM2[SEP ? MT * MT * 64 : 1];
+    // the second input set's images, x, decay sums and matrix (kSep: the reverse branch;
+    // kCS: the next block)
+    __shared__ __align__(16) uint2 sC2[TWO ? IMG : 1], sB2[TWO ? IMG : 1];
+    __shared__ __align__(16) AT sX2[TWO ? LT * XS : 1];
+    __shared__ __align__(16) float sDt2[TWO ? 64 : 1], sCs2[TWO ? 64 : 1], sEx2[TWO ? 64 : 1];
+    __shared__ __align__(16) uint4 sM2[TWO ? MT * MT * 64 : 1];
     __shared__ __align__(16) f32x4 sRed[(NPART > 1 ? NPART - 1 : 1) * 4 * MT * 64];
 
     const int tid = threadIdx.x;
@@ -263,8 +273,8 @@ bdlm_block_kernel(const KArgs args) {
                                                       : gzero());
         }
     }
-    u32x4 cch2[SEP ? BC_PT : 1], bch2[SEP ? BC_PT : 1], xch2[SEP ? X_PT : 1];
-    if constexpr (SEP) {
+    u32x4 cch2[TWO ? BC_PT : 1], bch2[TWO ? BC_PT : 1], xch2[TWO ? X_PT : 1];
+    if constexpr (TWO) {
         const AT *Bg2 = static_cast<const AT *>(args.Bm2) + b * args.bcs_b + g * args.bcs_g;
         const AT *Cg2 = static_cast<const AT *>(args.Cm2) + b * args.bcs_b + g * args.bcs_g;
         const AT *xg2 = static_cast<const AT *>(args.x2) + b * args.xs_b + h * args.xs_h;
@@ -298,7 +308,7 @@ bdlm_block_kernel(const KArgs args) {
     const DT dtraw = *(lane < L ? (const g_dt *)(dtg + lane * args.dts_t)
                                 : (const g_dt *)(&kZeroChunk));
     AT dtraw2 = AT(0);
-    if constexpr (SEP) {
+    if constexpr (TWO) {
         const AT *dtg2 = static_cast<const AT *>(args.dt2) + b * args.dts_b + h;
         dtraw2 = *(lane < L ? (const g_at *)(dtg2 + lane * args.dts_t) : (const g_at *)(&kZeroChunk));
     }
@@ -431,7 +441,7 @@ bdlm_block_kernel(const KArgs args) {
         dst[0] = uint2{v.x, v.y};
         dst[1] = uint2{v.z, v.w};
     }
-    if constexpr (SEP) {
+    if constexpr (TWO) {
 #pragma unroll
         for (int k = 0; k < BC_PT; ++k) {
             if (!bc_owner) break;
@@ -454,7 +464,7 @@ bdlm_block_kernel(const KArgs args) {
             dst[0] = uint2{v.x, v.y};
             dst[1] = uint2{v.z, v.w};
         }
-        if (tid == 3) sPar[3] = parv;   // A of the reverse branch
+        if (SEP && tid == 3) sPar[3] = parv;   // A of the reverse branch
     }
     if (tid < 3) sPar[tid] = parv;
     if (wave == 0) {
@@ -468,10 +478,11 @@ bdlm_block_kernel(const KArgs args) {
         sDt[lane] = dtv;
         sCs[lane] = cs;
         sEx[lane] = lane == 0 ? 0.f : up;
-        if constexpr (SEP) {   // the reverse branch's decay sums (its own dt and A)
+        if constexpr (TWO) {   // the second set's decay sums (kSep: its own dt and A)
             const float dtv2 = Act<F32>::val(dtraw2);
             const float Ar2 =
-                __int_as_float(__builtin_amdgcn_readlane(__float_as_int(parv), 3)) * kLog2e;
+                __int_as_float(__builtin_amdgcn_readlane(__float_as_int(parv), SEP ? 3 : 0)) *
+                kLog2e;
             const float cs2 = wave_inclusive_sum(dtv2 * Ar2);
             const float up2 = __shfl_up(cs2, 1, 64);
             sDt2[lane] = dtv2;
@@ -485,7 +496,18 @@ bdlm_block_kernel(const KArgs args) {
 
     // ---- phase 2: Gram tiles (shared out)
 
-    if constexpr (SEP) {
+    if constexpr (DIR == kCS) {
+        // the clean block's tiles (only for its outputs), then the next block's
+        const int n1 = args.y != nullptr ? MT * MT : 0;
+        for (int tile = wave; tile < n1 + MT * MT; tile += NW) {
+            if (tile < n1)
+                sM[tile * 64 + lane] = gram_tile_bf16<QN, kBoth>(sB, sC, sCs, sEx, sDt, tile / MT,
+                                                                 tile % MT, grp, col);
+            else
+                sM2[(tile - n1) * 64 + lane] = gram_tile_bf16<QN, kBoth>(
+                    sB2, sC2, sCs2, sEx2, sDt2, (tile - n1) / MT, (tile - n1) % MT, grp, col);
+        }
+    } else if constexpr (SEP) {
         // forward tiles from the first input set, reverse tiles from the second
         for (int tile = wave; tile < 2 * MT * MT; tile += NW) {
             const int tt = tile < MT * MT ? tile : tile - MT * MT;
@@ -543,9 +565,9 @@ bdlm_block_kernel(const KArgs args) {
         }
     }
     auto xquad = [&](int jt) { return f32x4{xv[jt][0], xv[jt][1], xv[jt][2], xv[jt][3]}; };
-    float xv2[SEP ? MT : 1][4];
-    s16x4 xq2[SEP ? MT : 1];
-    if constexpr (SEP) {
+    float xv2[TWO ? MT : 1][4];
+    s16x4 xq2[TWO ? MT : 1];
+    if constexpr (TWO) {
 #pragma unroll
         for (int jt = 0; jt < MT; ++jt) {
 #pragma unroll
@@ -562,8 +584,8 @@ bdlm_block_kernel(const KArgs args) {
         // waiting for the state
         float pre[MT][4], es[MT][4];
         if (part == 0) {
-            const float skip =
-                DIR == kBoth ? sPar[1] + sPar[2] : (DIR == kFwd || SEP ? sPar[1] : sPar[2]);
+            const float skip = DIR == kBoth || DIR == kCS ? sPar[1] + sPar[2]
+                                                           : (DIR == kFwd || SEP ? sPar[1] : sPar[2]);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 f32x4 ai = {0.f, 0.f, 0.f, 0.f};
@@ -753,6 +775,88 @@ bdlm_block_kernel(const KArgs args) {
                 }
             }
             __builtin_nontemporal_store(acc, reinterpret_cast<f32x4 *>(hs + q * 16 * kP));
+            if constexpr (DIR == kCS) hq[k] = acc;   // the next block starts from it
+        }
+    }
+
+    if constexpr (DIR == kCS) {
+        // the next block's first step from the committed state, still in registers: the
+        // first group's intra product and skip, every wave's prefix partial product, the
+        // partials summed in LDS, y2 stored
+        float pre[MT][4], es[MT][4];
+        if (part == 0) {
+            const float skip = sPar[1] + sPar[2];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                s16x4 mh[MT], ml[MT];
+#pragma unroll
+                for (int jt = 0; jt < MT; ++jt) {
+                    const uint4 v = sM2[(mt * MT + jt) * 64 + lane];
+                    mh[jt] = as_s16x4(uint2{v.x, v.y});
+                    ml[jt] = as_s16x4(uint2{v.z, v.w});
+                }
+                f32x4 ai = {0.f, 0.f, 0.f, 0.f};
+                ai = mma_quads<MT>(mh, xq2, ai);
+                ai = mma_quads<MT>(ml, xq2, ai);
+                const f32x4 csq = *reinterpret_cast<const f32x4 *>(&sCs2[16 * mt + 4 * grp]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pre[mt][r] = ai[r] + skip * xv2[mt][r];
+                    es[mt][r] = exp2f(csq[r]);
+                }
+            }
+        }
+        f32x4 ap[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) ap[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < QW; k += 2) {
+            if (k + 1 < QW) {
+                s16x4 h0, l0, h1, l1;
+                split4(hq[k], h0, l0);
+                split4(hq[k + 1], h1, l1);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const s16x4 c0 = as_s16x4(sC2[img_idx<QN, false>(mt, q0 + k, grp, col)]);
+                    const s16x4 c1 = as_s16x4(sC2[img_idx<QN, false>(mt, q0 + k + 1, grp, col)]);
+                    ap[mt] = mma_k32(c0, c1, h0, h1, ap[mt]);
+                    ap[mt] = mma_k32(c0, c1, l0, l1, ap[mt]);
+                }
+            } else {
+                s16x4 h0, l0;
+                split4(hq[k], h0, l0);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const s16x4 c0 = as_s16x4(sC2[img_idx<QN, false>(mt, q0 + k, grp, col)]);
+                    ap[mt] = mma_k16(c0, h0, ap[mt]);
+                    ap[mt] = mma_k16(c0, l0, ap[mt]);
+                }
+            }
+        }
+        if constexpr (NPART > 1) {
+            __syncthreads();   // the clean block's partials (if any) have been read
+            if (part > 0)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    sRed[(((part - 1) * 4 + pblk) * MT + mt) * 64 + lane] = ap[mt];
+            __syncthreads();
+            if (part == 0)
+#pragma unroll
+                for (int pt = 1; pt < NPART; ++pt)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+                        ap[mt] += sRed[(((pt - 1) * 4 + pblk) * MT + mt) * 64 + lane];
+        }
+        if (part == 0) {
+            float *yrow = args.y2 + ((static_cast<int64_t>(b) * L + 4 * grp) * args.nheads + h) * kP + p;
+            const int ytok = args.nheads * kP;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (L == LT || 16 * mt + 4 * grp + r < L)
+                        __builtin_nontemporal_store(es[mt][r] * ap[mt][r] + pre[mt][r],
+                                                    yrow + (16 * mt + r) * ytok);
         }
     }
 }
@@ -841,6 +945,7 @@ KArgs kargs(const LaunchArgs &a) {
     k.D_rev = a.D_rev;
     k.h_pool = a.h_pool;
     k.y = a.y;
+    k.y2 = nullptr;
     k.x2 = k.dt2 = k.Bm2 = k.Cm2 = nullptr;
     k.A2 = nullptr;
     k.conv_w = k.conv_b = k.conv_pool = nullptr;
@@ -919,6 +1024,35 @@ int launch_block_pair(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit,
     int rc = launch_dir(f, kFwd, commit, stream);
     if (rc != BDLM_OK || !want_y) return rc;
     return launch_dir(rev, kRev, false, stream);
+}
+
+int launch_commit_step(const LaunchArgs &clean, const LaunchArgs &next, float *y_next,
+                       void *stream) {
+    if (clean.batch == 0) return BDLM_OK;
+    if (clean.L == 0) {   // nothing to commit: the next block's step alone
+        LaunchArgs n = next;
+        n.y = y_next;
+        return launch_block(n, false, stream);
+    }
+    if (clean.bf16 && clean.L <= 32) {
+        KArgs k = kargs(clean);
+        k.x2 = next.x;
+        k.dt2 = next.dt;
+        k.Bm2 = next.Bm;
+        k.Cm2 = next.Cm;
+        k.y2 = y_next;
+        const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(clean.batch) * clean.nheads);
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        const hipError_t e = clean.L <= 16 ? by_ns<16, false, true, kCS>(clean.dstate, k, grid, s)
+                                           : by_ns<32, false, true, kCS>(clean.dstate, k, grid, s);
+        return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+    }
+    // otherwise the commit, then the step, as two launches on the stream
+    int rc = launch_block(clean, true, stream);
+    if (rc != BDLM_OK) return rc;
+    LaunchArgs n = next;
+    n.y = y_next;
+    return launch_block(n, false, stream);
 }
 
 template <int LT, bool COMMIT, int DIR>

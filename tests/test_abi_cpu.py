@@ -585,3 +585,29 @@ def test_noalloc_prefill_host_refusals(L):
     assert nb.tolist() == [1, 1, 1, 1] and nc.tolist() == [0] * 4
     # nothing to do: succeeds without a device
     assert call(desc(batch=0, L=300), ptrs(x=None, dt=None, B=None, C=None)) == bd.OK
+
+
+def test_commit_step_checks(L):
+    d = desc(batch=2, L=32)
+    p = ptrs()
+    q = dict(x=FAKE + 0x40000, dt=FAKE + 0x41000, B=FAKE + 0x42000, C=FAKE + 0x43000)
+    yn = FAKE + 0x50000
+
+    def chk(p=p, q=q, yn=yn, yc=None, slots=None, nb=None, expect=-1, dd=d):
+        nc = np.zeros(4, np.int64)
+        nb = np.zeros(4, np.int64) if nb is None else nb
+        return L.bdlm_check_commit_step(ctypes.byref(dd), p["x"], p["dt"], p["A"], p["B"], p["C"],
+                                        p["D"], p["Drev"], q["x"], q["dt"], q["B"], q["C"], p["h"],
+                                        4, i32p(slots), i64p(nc), i64p(nb), expect, yc, yn)
+    assert chk() == bd.OK
+    assert chk(yc=FAKE + 0x60000) == bd.OK
+    for f in ("x", "dt", "B", "C"):
+        assert chk(q=dict(q, **{f: None})) == bd.E_NULL, f
+    assert chk(yn=None) == bd.E_NULL
+    assert chk(yn=FAKE + 0x50008) == bd.E_ALIGN
+    assert chk(yc=FAKE + 0x60004) == bd.E_ALIGN
+    assert chk(q=dict(q, B=FAKE + 0x42008)) == bd.E_ALIGN
+    assert chk(slots=np.array([1, 1], np.int32)) == bd.E_SLOT          # a commit: distinct
+    assert chk(nb=np.array([3, 3, 0, 0], np.int64), expect=3) == bd.OK
+    assert chk(nb=np.array([3, 2, 0, 0], np.int64), expect=3) == bd.E_OFFSET
+    assert chk(dd=desc(batch=2, L=65)) == bd.E_SHAPE                   # up to 64 tokens
