@@ -588,6 +588,13 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 #pragma unroll
         for (int q = 0; q < QN; ++q) S[q] = *reinterpret_cast<const f32x4 *>(src + quad_off(q, grp, p));
     }
+    // The state loads complete here, before the chunk loop.  Otherwise the compiler's wait
+    // analysis carries the pending loads into the loop: the first use of each quad in
+    // every chunk then waits on the vector-memory counter, which from the second chunk on
+    // means waiting for the next chunk's prefetched inputs (their full latency, every
+    // chunk).
+#pragma unroll
+    for (int q = 0; q < QN; ++q) asm volatile("" : "+v"(S[q]));
     // states entering the segment's chunks (blocks), forward only
     float *emit_base = nullptr;
     int64_t emit_first = 0;
