@@ -40,8 +40,8 @@ CSRC = os.path.join(ROOT, "paper_2607_02805_amd", "csrc")
 # the sources each profiled kernel family is compiled from (a summary under profiles/
 # records their hash; a figure is read back only while the hash still matches)
 SOURCE_SETS = {
-    "block": ("bdlm_scan.hip", "bdlm_device.h", "bdlm_launch.h"),
-    "seq": ("bdlm_seq.hip", "bdlm_device.h", "bdlm_launch.h"),
+    "block": ("bdlm_scan.hip", "bdlm_device.h"),
+    "seq": ("bdlm_seq.hip", "bdlm_device.h"),
     "all": ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_conv.hip", "bdlm_norm.hip", "bdlm_device.h",
             "bdlm_launch.h"),
 }
@@ -1037,6 +1037,131 @@ def summarize_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv,
     return res
 
 
+def _step_dispatches(trace_csv: str, kernel: str, grid_threads: int):
+    """(start, end) ns of the dispatches of one kernel at one launch shape."""
+    out = []
+    for r in _csv_rows(trace_csv):
+        name = r["Kernel_Name"].replace("bdlm::(anonymous namespace)::", "")
+        if kernel in name and int(r["Grid_Size_X"]) == grid_threads:
+            out.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    return sorted(out)
+
+
+def span_per_node(disp, run_len: int) -> float | None:
+    """Median over graph replays of (last end - first start) / nodes for runs of exactly
+    ``run_len`` back-to-back dispatches (one replay of the ring's steps): the trace's
+    counterpart of the HIP-event time per step node."""
+    import statistics as st
+    runs, cur = [], [disp[0]] if disp else []
+    for d in disp[1:]:
+        if d[0] - cur[-1][1] < 20_000:      # within 20 us of the previous dispatch's end
+            cur.append(d)
+        else:
+            runs.append(cur)
+            cur = [d]
+    if cur:
+        runs.append(cur)
+    spans = [(r[-1][1] - r[0][0]) / 1e3 / len(r) for r in runs if len(r) == run_len]
+    return st.median(spans) if spans else None
+
+
+def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> None:
+    """Write the three block-step summaries under ``out_dir`` from a rocprofv3 output
+    directory ``src`` holding trace_kernel_stats.csv / trace_kernel_trace.csv (kernel
+    trace), fetch/write/copyfetch/copywrite_counter_collection.csv (HBM traffic) and
+    mfma_counter_collection.csv (MfmaUtil), taken with the commands listed in them."""
+    import statistics as st
+    sha = kernel_source_sha("block")
+    hdr = f"- kernel_source_sha256_16: `{sha}`\n"
+    R = "python3 $R/bench.py --steps 20 --warmup 5 --no-extras --no-cpu-baseline"
+    pre = "cd /tmp && export TMPDIR=/tmp && "
+    cmd_trace = (f"{pre}rocprofv3 --kernel-trace --stats --output-format csv -d $OUT -o trace -- {R}")
+    # trace
+    stats = os.path.join(src, "trace_kernel_stats.csv")
+    trace = os.path.join(src, "trace_kernel_trace.csv")
+    disp = _step_dispatches(trace, STEP_KERNEL, 512 * 512)
+    durs = [(e - b) / 1e3 for b, e in disp]
+    cdisp = _step_dispatches(trace, COMMIT_KERNEL, 512 * 512)
+    cdur = [(e - b) / 1e3 for b, e in cdisp]
+    span = span_per_node(disp, nl * p)
+    # the bench's own HIP-event figure in the traced run (stdout saved as trace.log)
+    ev = None
+    log = os.path.join(src, "trace.log")
+    if os.path.exists(log):
+        for ln in open(log):
+            if ln.startswith("{") and '"roofline"' in ln:
+                ev = json.loads(ln)["config"]["step_us"]
+    text = (f"# Block step kernel trace: 350M layer shape, batch 16, L 32, 262K prefix\n\n"
+            f"The headline workload of `bench.py` (8 denoising steps + commit per block cycle, "
+            f"ring of {nl} layers, graph replay), under the kernel tracer.\n\n{hdr}"
+            f"- step_kernel: `{STEP_KERNEL}` (512 workgroups x 512 threads)\n"
+            f"- step_kernel_dispatches: {len(durs)}\n"
+            f"- step_kernel_mean_us: {st.fmean(durs):.3f}\n"
+            f"- step_kernel_median_us: {st.median(durs):.3f}\n"
+            f"- step_span_per_node_us: {'' if span is None else f'{span:.3f}'}\n"
+            f"- commit_kernel_mean_us: {st.fmean(cdur):.3f}\n"
+            f"- bench_events_step_us_under_tracer: {'' if ev is None else ev}\n\n"
+            "`step_kernel_mean_us` is the mean dispatch duration the tracer records (start to end "
+            "of each dispatch); `step_span_per_node_us` is, for each replay of the ring's "
+            f"{nl * p} step nodes, the time from the first node's start to the last node's end "
+            "divided by the node count, the quantity the bench's HIP events measure "
+            "(`bench_events_step_us_under_tracer`, the bench's own figure in this traced run).  "
+            "The tracer serialises dispatches: under it a node no longer starts while its "
+            "predecessor drains, so the traced span per node exceeds the untraced HIP-event "
+            "figure the bench reports, and each dispatch runs its ramp-up and drain alone.  The "
+            "traced dispatch duration is therefore an upper bound on the pipelined per-node time "
+            "the roofline fraction uses, not an equal of it.  The commit kernel's mean covers the "
+            "prefix commits (no clean-block outputs) and the cycle commits (with them).\n\n"
+            f"Command (R = repository root, OUT = an output directory; MI355X, ROCm 7.2):\n\n"
+            f"    {cmd_trace}\n    python3 bench.py --write-block-profiles $OUT profiles\n\n"
+            "## Kernel statistics (whole run)\n\n" + summarize_trace(stats) + "\n")
+    open(os.path.join(out_dir, "block_step_350m_b16_L32_kernel_trace.md"), "w").write(text)
+    # traffic
+    f = [os.path.join(src, f"{k}_counter_collection.csv") for k in ("fetch", "write", "copyfetch", "copywrite")]
+    t = summarize_traffic(*f)
+    sb, cb = step_bytes(16, 32, 64, 128, 1, 32), commit_bytes(16, 32, 64, 128, 1, 32)
+    step_hbm = t["step"]["fetch_bytes"] + t["step"]["write_bytes"]
+    commit_hbm = t["commit"]["fetch_bytes"] + t["commit"]["write_bytes"]
+    cmds = "\n".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {a}"
+                     for c, o, a in (("FETCH_SIZE", "fetch", R), ("WRITE_SIZE", "write", R),
+                                     ("FETCH_SIZE", "copyfetch", "python3 $R/bench.py --copy-calibration"),
+                                     ("WRITE_SIZE", "copywrite", "python3 $R/bench.py --copy-calibration")))
+    text = (f"# HBM traffic of the block step and the commit: 350M layer shape, batch 16, L 32\n\n"
+            f"{hdr}- step_hbm_bytes_per_launch: {step_hbm}\n- step_alg_bytes: {sb}\n"
+            f"- step_traffic_over_alg: {step_hbm / sb:.4f}\n"
+            f"- commit_hbm_bytes_per_launch: {commit_hbm}\n- commit_alg_bytes: {cb}\n"
+            f"- fetch_scale: {t['fetch_scale']:.4f}\n- write_scale: {t['write_scale']:.4f}\n\n"
+            "FETCH_SIZE and WRITE_SIZE (KiB per dispatch, median over dispatches) scaled by what "
+            "the same counter reads for a plain 256 MiB device copy (bytes = KiB x 1024 x scale).\n\n"
+            f"Commands (R = repository root, OUT = an output directory):\n\n{cmds}\n"
+            f"    python3 bench.py --write-block-profiles $OUT profiles\n\n"
+            f"| kernel | dispatches | fetch bytes | write bytes |\n|---|---|---|---|\n"
+            f"| step `{STEP_KERNEL}` | {t['step']['dispatches']} | {t['step']['fetch_bytes']:,} | "
+            f"{t['step']['write_bytes']:,} |\n"
+            f"| commit `{COMMIT_KERNEL}` | {t['commit']['dispatches']} | {t['commit']['fetch_bytes']:,} | "
+            f"{t['commit']['write_bytes']:,} |\n")
+    open(os.path.join(out_dir, "hbm_traffic_block_step_350m_b16_L32.md"), "w").write(text)
+    # MFMA utilisation
+    mf = os.path.join(src, "mfma_counter_collection.csv")
+    vals = {}
+    for r in _csv_rows(mf):
+        name = r["Kernel_Name"]
+        if STEP_KERNEL in name.replace("bdlm::(anonymous namespace)::", "") \
+                and int(r["Grid_Size"]) == 512 * 512:
+            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    util = st.median(vals["MfmaUtil"])
+    text = (f"# MFMA utilisation of the block step: 350M layer shape, batch 16, L 32\n\n{hdr}"
+            f"- step_mfma_busy_pct: {util:.2f}\n- step_dispatches: {len(vals['MfmaUtil'])}\n\n"
+            "rocprofv3's derived counter MfmaUtil = 100 x SQ_VALU_MFMA_BUSY_CYCLES (summed over "
+            "SIMDs) / (GRBM_GUI_ACTIVE x SIMD count), median over the step dispatches: the share "
+            "of the launch's active cycles in which a SIMD's matrix unit is busy.  The step is "
+            "bound by HBM, so this is evidence of where the Gram and split-bf16 products sit, "
+            "not a roof.\n\nCommand (R = repository root, OUT = an output directory):\n\n"
+            f"    {pre}rocprofv3 --pmc MfmaUtil --output-format csv -d $OUT -o mfma -- {R}\n"
+            f"    python3 bench.py --write-block-profiles $OUT profiles\n")
+    open(os.path.join(out_dir, "sq_counters_block_step_350m_b16_L32.md"), "w").write(text)
+
+
 def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
     """A plain device-to-device copy of known size, for scaling HBM counters (FETCH_SIZE,
     WRITE_SIZE) of profiled kernels to bytes."""
@@ -1086,7 +1211,18 @@ def main():
                     help="print per-launch HBM bytes from rocprofv3 counter CSVs and exit")
     ap.add_argument("--traffic-kernels", metavar="TAG=NAME,...",
                     help="with --summarize-traffic: kernels to report (name substrings)")
+    ap.add_argument("--write-block-profiles", nargs=2, metavar=("ROCPROF_DIR", "OUT_DIR"),
+                    help="write the block-step profile summaries from a rocprofv3 output "
+                         "directory and exit")
+    ap.add_argument("--source-sha", choices=sorted(SOURCE_SETS),
+                    help="print the hash of a kernel family's sources and exit")
     args = ap.parse_args()
+    if args.source_sha:
+        print(kernel_source_sha(args.source_sha))
+        return
+    if args.write_block_profiles:
+        write_block_profiles(*args.write_block_profiles)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
@@ -1210,6 +1346,15 @@ def main():
     }
     if ceiling is not None:
         line["stream_ceiling"] = ceiling
+    cs = extras.get("variants", {}).get("commit_step_L32")
+    if cs is not None and args.block_len == 32:
+        # the same block cycle with the commit fused into the next block's first step (one
+        # state read fewer per cycle; same results): p - 1 steps + the fused launch
+        t = (args.denoise - 1) * r["avg_step_us"] + cs["fused_us"]
+        line["fused_order"] = {
+            "cycle_us_per_layer": round(t, 3),
+            "value": round(args.denoise * s["batch"] * s["block_len"] / (t * 1e-6), 1),
+            "note": "p - 1 steps + one commit+next-step launch per block cycle (bdlm_commit_step)"}
     if "copy_reference" in extras:
         cr = extras["copy_reference"]
         line["roofline"]["copy_same_bytes_gbs"] = cr["gbs"]
