@@ -1162,6 +1162,77 @@ def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> No
     open(os.path.join(out_dir, "sq_counters_block_step_350m_b16_L32.md"), "w").write(text)
 
 
+SEQ_WORKLOADS = """All workloads of `bench.py --sequence-only` (350M layer shape: 32 heads x 64, or the
+paper's 26, dstate 128, one group, bf16 activations unless stated):
+
+* full window: batch 4, 65,536 tokens, forward + reverse from zero; 16 segments of
+  4,096 tokens per row and head -- `seg_state` (both directions' local states, 2048
+  workgroups), `seg_combine` (1024 workgroups), `seg_out` forward and reverse (2048);
+* prefill: batch 16, 16,384 tokens -- `seg_state` (2048), `seg_combine` (2048);
+* all-block forward: batch 8, 8,192-token window, L = 32 (256 blocks; segments of 16
+  blocks) -- `seg_state` (4096), `seg_combine` (4096), `seg_out` with SUB = 32 carrying
+  the state block by block and writing the block states and the clean outputs (4096),
+  then the block step over 2,048 rows (65536 x 512);
+* paper geometry: batch 16, 26 heads, L = 256 -- `seg_out` forward and reverse, one
+  segment per row and head (416 workgroups);
+* separate reverse inputs: batch 16, L = 32 -- one block-kernel launch with both input
+  sets (direction 3), 512 x 512;
+* convolution state: batch 16, L = 32 -- the fp32 block kernel with the convolution in
+  its staging (last template flag true), forward (direction 1; the commit instantiation
+  on commits) then reverse (direction 2), and `bdlm_conv_keep_kernel` on commits;
+* gated RMS normalisation: 512 tokens x 2,048 channels -- `bdlm_gated_rmsnorm_kernel`
+  alone and after the block step;
+* fused commit + next step: batch 16, L = 32 -- the block kernel's direction 4.
+"""
+
+
+def write_seq_profiles(src: str, out_dir: str) -> None:
+    """Write the sequence/all-block/variant summaries under ``out_dir`` from a rocprofv3
+    output directory ``src`` holding trace_kernel_trace.csv, fetch/write/copyfetch/
+    copywrite_counter_collection.csv and p1/p2/mfma_counter_collection.csv, taken with the
+    commands listed in them."""
+    hdr = f"- kernel_source_sha256_16: `{kernel_source_sha('all')}`\n"
+    pre = "cd /tmp && export TMPDIR=/tmp && "
+    R = "python3 $R/bench.py --sequence-only"
+    cal = "python3 $R/bench.py --copy-calibration"
+    tail = "    python3 bench.py --write-seq-profiles $OUT profiles\n"
+    f = [os.path.join(src, f"{k}_counter_collection.csv") for k in ("fetch", "write", "copyfetch", "copywrite")]
+    cmds = (f"    {pre}rocprofv3 --kernel-trace --stats --output-format csv -d $OUT -o trace -- {R} --contrast-reps 5\n"
+            + "".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {a}\n"
+                      for c, o, a in (("FETCH_SIZE", "fetch", R + " --contrast-reps 1"),
+                                      ("WRITE_SIZE", "write", R + " --contrast-reps 1"),
+                                      ("FETCH_SIZE", "copyfetch", cal), ("WRITE_SIZE", "copywrite", cal)))
+            + tail)
+    text = ("# Sequence kernels, all-block forward and block variants: kernel trace and HBM traffic\n\n"
+            + hdr + "\n" + SEQ_WORKLOADS
+            + "\nCommands (R = repository root, OUT = an output directory; MI355X, ROCm 7.2):\n\n"
+            + cmds + "\n## Kernel trace\n\nPer kernel and launch shape (traced durations of the "
+            "short launches include the dispatch start-up that untraced graph replay overlaps with "
+            "the previous node):\n\n"
+            + summarize_dispatches(os.path.join(src, "trace_kernel_trace.csv"))
+            + "\n\n## HBM traffic per dispatch\n\nFETCH_SIZE / WRITE_SIZE medians per dispatch, "
+            "each scaled by the same counter's reading for a 256 MiB device copy.\n\n"
+            + summarize_traffic_shapes(*f) + "\n")
+    open(os.path.join(out_dir, "sequence_allblock_variants_350m_trace_and_traffic.md"), "w").write(text)
+    passes = [("p1", "SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS "
+                     "SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS SQ_LDS_BANK_CONFLICT"),
+              ("p2", "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_LDS "
+                     "SQ_LDS_IDX_ACTIVE SQ_ACTIVE_INST_VMEM SQ_WAIT_ANY"),
+              ("mfma", "MfmaUtil")]
+    cmds = "".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {R} --contrast-reps 1\n"
+                   for o, c in passes) + tail
+    text = ("# SQ counters per dispatch (median): sequence kernels and block variants, 350M layer shape\n\n"
+            + hdr + "\nThe workloads of the sequence trace summary, one timed repetition of the "
+            "contrast; one pass per counter set (at most 8 SQ counters each).  MfmaUtil is "
+            "rocprofv3's derived 100 x SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMD count): "
+            "the share of active cycles in which a SIMD's matrix unit is busy.\n\n"
+            "Commands (R = repository root, OUT = an output directory; MI355X, ROCm 7.2):\n\n"
+            + cmds
+            + "".join(f"\n## Pass {o}\n\n" + summarize_counters(os.path.join(src, f"{o}_counter_collection.csv")) + "\n"
+                      for o, _ in passes))
+    open(os.path.join(out_dir, "sq_counters_sequence_kernels_350m.md"), "w").write(text)
+
+
 def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
     """A plain device-to-device copy of known size, for scaling HBM counters (FETCH_SIZE,
     WRITE_SIZE) of profiled kernels to bytes."""
@@ -1214,6 +1285,9 @@ def main():
     ap.add_argument("--write-block-profiles", nargs=2, metavar=("ROCPROF_DIR", "OUT_DIR"),
                     help="write the block-step profile summaries from a rocprofv3 output "
                          "directory and exit")
+    ap.add_argument("--write-seq-profiles", nargs=2, metavar=("ROCPROF_DIR", "OUT_DIR"),
+                    help="write the sequence/variant profile summaries from a rocprofv3 output "
+                         "directory and exit")
     ap.add_argument("--source-sha", choices=sorted(SOURCE_SETS),
                     help="print the hash of a kernel family's sources and exit")
     args = ap.parse_args()
@@ -1222,6 +1296,9 @@ def main():
         return
     if args.write_block_profiles:
         write_block_profiles(*args.write_block_profiles)
+        return
+    if args.write_seq_profiles:
+        write_seq_profiles(*args.write_seq_profiles)
         return
     if args.copy_calibration:
         copy_calibration()
