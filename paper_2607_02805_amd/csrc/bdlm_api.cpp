@@ -368,7 +368,7 @@ int bdlm_scan_block_step(const bdlm_desc_t *d, const void *x, const void *dt, co
     const bdlm::LaunchArgs a =
         make_args(d, x, dt, A, B, C, D, D_rev, const_cast<float *>(h_pool), slot_idx, y);
     return by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
-        return d->block_len > BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_long(c, c, false, true, stream)
+        return d->block_len > BDLM_MAX_BLOCK_LEN ? bdlm::launch_block_long_shared(c, false, true, stream)
                                                  : bdlm::launch_block(c, false, stream);
     });
 }
@@ -425,7 +425,7 @@ int bdlm_commit_boundary(const bdlm_desc_t *d, const void *x, const void *dt, co
         make_args(d, x, dt, A, B, C, D, D_rev, h_pool, slot_idx, y_clean);
     rc = by_row_chunks(a, y_row_floats(d, d->block_len), [&](const bdlm::LaunchArgs &c) {
         return d->block_len > BDLM_MAX_BLOCK_LEN
-                   ? bdlm::launch_block_long(c, c, true, y_clean != nullptr, stream)
+                   ? bdlm::launch_block_long_shared(c, true, y_clean != nullptr, stream)
                    : bdlm::launch_block(c, true, stream);
     });
     if (rc != BDLM_OK) return rc;

@@ -176,6 +176,14 @@ inline int64_t boundary_workspace(int64_t batch, int64_t nheads, int64_t dstate,
 int launch_block_long(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit, bool want_y,
                       void *stream);
 
+// Blocks of 65 to 256 tokens with bf16 activations and one input set for both branches:
+// one launch with the block's 64-token chunks side by side (bdlm_long.hip).
+bool long_chunked_fits(const LaunchArgs &a);
+int launch_long_chunked(const LaunchArgs &a, bool commit, bool want_y, void *stream);
+// A long block's step or commit with one input set: launch_long_chunked where it fits,
+// else launch_block_long.
+int launch_block_long_shared(const LaunchArgs &a, bool commit, bool want_y, void *stream);
+
 // The convolution part of the boundary state, then the block step (commit: the
 // commit) on the convolved inputs: a.x / a.Bm / a.Cm are the pre-convolution inputs,
 // conv_pool [nslots][3][channels] the cached input rows (a commit replaces them).

@@ -73,6 +73,64 @@ def test_long_block_commit(H, N, L, want_y):
         assert rel_err(out, y_ref) <= REL_TOL
 
 
+@pytest.mark.parametrize("H,N,L,G", [(4, 16, 256, 1), (4, 32, 129, 2), (6, 64, 191, 1),
+                                   (2, 128, 200, 2), (5, 128, 255, 1), (3, 64, 66, 1),
+                                   (8, 32, 192, 4), (3, 16, 130, 1)])
+def test_long_block_chunked_shapes(H, N, L, G):
+    """Blocks of 65 to 256 tokens with bf16 inputs run as one launch over 64-token chunks
+    side by side (two, three or four chunks; ragged last chunks from 1 to 63 tokens;
+    every dstate; several groups): the step and then the commit with its clean-block
+    outputs, against the oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 3, H, 64, N, G, L, 0, True, 1, 10200 + H + N + L)
+    d, c = bi.block_inputs(w, 0), bi.commit_inputs(w)
+    d["D_rev"] = (d["D"] * 0.5).astype(np.float32)
+    c["D_rev"] = d["D_rev"]
+    pool = bi.random_state(w, 4, 9, 0.5).astype(np.float64)
+    slots = [3, 0, 2]
+    h = pool_dev(pool)
+    v = to_dev(d)
+    say("chunked long step", dict(H=H, N=N, L=L, G=G))
+    y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], h,
+                           slot_idx=slots)
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.block_step(d, pool, slot_idx=slots))
+    say("  step rel err", e)
+    assert e <= REL_TOL
+    nb = np.array([2, 5, 2, 2], np.int64)
+    nc = nb * L
+    ref_pool, ref_nc, ref_nb = pool.copy(), nc.copy(), nb.copy()
+    rc, y_ref = oracle.commit(c, ref_pool, ref_nc, ref_nb, slot_idx=slots, expected_block_index=2,
+                              want_y=True)
+    assert rc == 0
+    vc = to_dev(c)
+    out = bd.commit_boundary(vc["x"], vc["dt"], vc["A"], vc["B"], vc["C"], vc["D"], vc["D_rev"], h,
+                             nc, nb, 2, slot_idx=slots, y_clean=True)
+    torch.cuda.synchronize()
+    got = from_pool(h)
+    eh, ey = rel_err(got[slots], ref_pool[slots]), rel_err(out, y_ref)
+    say("  commit state rel err", eh, "y_clean rel err", ey)
+    assert eh <= REL_TOL and ey <= REL_TOL
+    assert nc.tolist() == ref_nc.tolist() and nb.tolist() == ref_nb.tolist()
+    np.testing.assert_array_equal(got[1], pool[1].astype(np.float32))     # untouched slot
+
+
+def test_long_block_fp32_sequence_path():
+    """fp32 activations in blocks longer than 64 tokens keep the sequence kernels' path."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, 3, 64, 64, 1, 256, 0, False, 1, 10300)
+    d = bi.block_inputs(w, 0)
+    pool = bi.random_state(w, 2, 4, 0.5).astype(np.float64)
+    v = to_dev(d)
+    say("fp32 long step", w)
+    y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"],
+                           pool_dev(pool))
+    torch.cuda.synchronize()
+    e = rel_err(y, oracle.block_step(d, pool))
+    say("  rel err", e)
+    assert e <= REL_TOL
+
+
 def test_paper_geometry_full_size():
     """The paper's 350M geometry at the size the bench times it (batch 16, 26 heads,
     dstate 128, 256-token blocks, identity slots: 416 workgroups per launch): the step,

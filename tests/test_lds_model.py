@@ -66,6 +66,9 @@ class Model:
 
     def __init__(self, arrays: dict):
         self.arrays = arrays                  # name -> size in bytes
+        # a wave may rewrite bytes it wrote before in the same interval (with later
+        # instructions: a wave's LDS instructions are served in order)
+        self.same_wave_rewrites = False
         self.interval = 0
         self.acc = collections.defaultdict(list)
         self.oob = []
@@ -107,7 +110,11 @@ class Model:
                 wthreads = {t for t, _ in writers}
                 readers = {t for t, k, _ in lst if k == "R"}
                 if len(wthreads) > 1:
-                    problems.append(("two writers in one interval", iv, key, sorted(wthreads)[:4]))
+                    per_instr = collections.Counter(i for _, i in writers)
+                    ok = (self.same_wave_rewrites and len({t // 64 for t in wthreads}) == 1 and
+                          max(per_instr.values()) == 1)
+                    if not ok:
+                        problems.append(("two writers in one interval", iv, key, sorted(wthreads)[:4]))
                 wwaves = {t // 64 for t in wthreads}
                 rwaves = {t // 64 for t in readers}
                 if wwaves and (rwaves - wwaves or len(wwaves) > 1):
@@ -431,6 +438,144 @@ def block_model(LT, NS, commit, npart, want_y=True):
     return m
 
 
+# ------------------------------------------------------------- long-block kernel
+def long_model(NS, NCH, commit, want_y=True):
+    """bdlm_long_block_kernel (bdlm_long.hip): wave c owns chunk c and its LDS region, which
+    holds the chunk's C row image, then its B row image, then the local states it publishes;
+    one barrier, after which every wave reads the other chunks' published states."""
+    QN, RS = NS // 16, NS + 4
+    REG = 64 * RS * 2
+    PR, RPI = NS // 8, 64 // (NS // 8)
+    names = ["Cs", "Ex", "Dt", "Ec", "Er", "Wf", "Wr", "La", "Lb", "Ua", "Ub"]
+    arrays = {"reg": NCH * REG, "tot": 4 * NCH}
+    arrays.update({n: NCH * 64 * 4 for n in names})
+    m = new_model(arrays)
+    m.same_wave_rewrites = True
+
+    class Lockstep:
+        """A wave's lanes issue each instruction together: accesses are collected per lane
+        and replayed instruction by instruction."""
+        def __init__(self):
+            self.ops = []
+
+        def access(self, tid, kind, instr, array, off, nbytes, tag=None):
+            self.ops.append((instr, len(self.ops), tid, kind, array, off, nbytes, tag))
+
+        def flush(self):
+            for instr, _, tid, kind, array, off, nbytes, tag in sorted(self.ops, key=lambda o: o[:2]):
+                outer.access(tid, kind, instr, array, off, nbytes, tag)
+            self.ops = []
+    outer = m
+    for c in range(NCH):
+        m = Lockstep()
+        need_f, need_r = commit or c + 1 < NCH, want_y and c > 0
+        base = c * REG
+        for l in range(64):
+            t, col, grp = 64 * c + l, l % 16, l // 16
+            ins = 0
+
+            def nxt():
+                nonlocal ins
+                ins += 1
+                return ins
+            for n in names:                       # per-token factors (lane = token)
+                m.access(t, "W", nxt(), n, (c * 64 + l) * 4, 4, tag=(n, c, l))
+            if l == 0:
+                m.access(t, "W", nxt(), "tot", 4 * c, 4, tag=("tot", c))
+            else:
+                nxt()
+
+            def stage(what):
+                rl, pc = l // PR, l % PR
+                for i in range(PR):
+                    row = RPI * i + rl
+                    for h in range(2):
+                        off = base + ((row * RS + pc * 8 + 4 * h) * 2)
+                        i0 = nxt()
+                        for e in range(4):
+                            m.access(t, "W", i0, "reg", off + 2 * e, 2, tag=(what, row, pc * 8 + 4 * h + e))
+
+            def quad(what, row, n0):
+                i0 = nxt()
+                for e in range(4):
+                    m.access(t, "R", i0, "reg", base + (row * RS + n0 + e) * 2, 2, tag=(what, row, n0 + e))
+            if want_y:
+                stage("C")
+                for mt in range(4):
+                    for q in range(QN):
+                        quad("C", 16 * mt + col, 16 * q + 4 * grp)
+            stage("B")
+            if want_y:
+                for mt in range(4):
+                    for n in ("Cs", "Ex", "La", "Ua"):
+                        m.access(t, "R", nxt(), n, (c * 64 + 16 * mt + col) * 4, 4, tag=(n, c, 16 * mt + col))
+                for jt in (0, 2):
+                    for d in range(2):
+                        for q in range(QN):
+                            quad("B", 16 * (jt + d) + col, 16 * q + 4 * grp)
+                    for d in range(2):
+                        jj = jt + d
+                        for n in ("Lb", "Ub", "Cs", "Ex", "Dt"):
+                            i0 = nxt()
+                            for r in range(4):
+                                j = 16 * jj + 4 * grp + r
+                                m.access(t, "R", i0, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
+            for jt in range(4):
+                for n in ("Wf", "Wr"):
+                    i0 = nxt()
+                    for r in range(4):
+                        j = 16 * jt + 4 * grp + r
+                        m.access(t, "R", i0, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
+            for q in range(QN):                   # B read transposed
+                for jt in range(4):
+                    for r in range(4):
+                        j = 16 * jt + 4 * grp + r
+                        m.access(t, "R", nxt(), "reg", base + (j * RS + 16 * q + col) * 2, 2,
+                                 tag=("B", j, 16 * q + col))
+            for q in range(QN):                   # publish
+                if need_f:
+                    m.access(t, "W", nxt(), "reg", base + ((4 * q + grp) * 16 + col) * 16, 16,
+                             tag=("F", c, q, grp, col))
+                if need_r:
+                    m.access(t, "W", nxt(), "reg", base + (QN * 64 + (4 * q + grp) * 16 + col) * 16, 16,
+                             tag=("R", c, q, grp, col))
+        m.flush()
+    m = outer
+    m.barrier()
+    for c in range(NCH):
+        for l in range(64):
+            t, col, grp = 64 * c + l, l % 16, l // 16
+            ins = 1000
+
+            def rd(k, q, which):
+                nonlocal ins
+                ins += 1
+                off = k * REG + ((QN * 64 if which == "R" else 0) + (4 * q + grp) * 16 + col) * 16
+                m.access(t, "R", ins, "reg", off, 16, tag=(which, k, q, grp, col))
+            for k in range(c):
+                ins += 1
+                m.access(t, "R", ins, "tot", 4 * k, 4, tag=("tot", k))
+                for q in range(QN):
+                    rd(k, q, "F")
+            if commit and c == NCH - 1:
+                for q in range(QN):
+                    rd(c, q, "F")
+            if want_y:
+                for n, lo, hi in (("Ec", 0, 0), ("Er", 0, 0)):
+                    for mt in range(4):
+                        ins += 1
+                        for r in range(4):
+                            j = 16 * mt + 4 * grp + r
+                            m.access(t, "R", ins, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
+                for k in range(NCH - 1, c, -1):
+                    ins += 1
+                    m.access(t, "R", ins, "tot", 4 * k, 4, tag=("tot", k))
+                    for q in range(QN):
+                        rd(k, q, "R")
+    m.barrier()
+    return m
+
+
 # ---------------------------------------------------------------------- tests
 @pytest.mark.parametrize("NS", [16, 32, 64, 128])
 @pytest.mark.parametrize("both", [False, True])
@@ -458,6 +603,39 @@ def test_block_kernel_lds(LT, NS, commit):
     assert block_model(LT, NS, commit, npart).check() == []
     if commit:
         assert block_model(LT, NS, True, npart, want_y=False).check() == []
+
+
+@pytest.mark.parametrize("NS", [16, 32, 64, 128])
+@pytest.mark.parametrize("NCH", [2, 3, 4])
+@pytest.mark.parametrize("commit", [False, True])
+def test_long_block_kernel_lds(NS, NCH, commit):
+    assert long_model(NS, NCH, commit).check() == []
+    if commit:
+        assert long_model(NS, NCH, True, want_y=False).check() == []
+
+
+def test_long_block_model_catches_a_cross_wave_rewrite():
+    """Rewrites are allowed within a wave only: the same byte written by two waves in one
+    interval, or by two lanes of one instruction, is still flagged."""
+    w = new_model({"a": 256})
+    w.same_wave_rewrites = True
+    w.access(0, "W", 1, "a", 0, 4)
+    w.access(1, "W", 2, "a", 0, 4)      # another lane of wave 0, a later instruction: fine
+    assert w.check() == []
+    w.access(64, "W", 3, "a", 0, 4)     # wave 1
+    assert any(p[0] == "two writers in one interval" for p in w.check())
+    v = new_model({"a": 256})
+    v.same_wave_rewrites = True
+    v.access(0, "W", 1, "a", 0, 4)
+    v.access(1, "W", 1, "a", 0, 4)      # two lanes, one instruction
+    assert any(p[0] == "two writers in one interval" for p in v.check())
+    # the long-block kernel without its barrier: waves read states other waves publish
+    m = long_model(32, 3, False)
+    merged = new_model(m.arrays)
+    merged.same_wave_rewrites = True
+    for (iv, arr, b), lst in m.acc.items():
+        merged.acc[(0, arr, b)].extend(lst)
+    assert any(p[0] == "cross-wave access to a written byte" for p in merged.check())
 
 
 def test_the_model_catches_planted_hazards():
