@@ -282,9 +282,21 @@ def run_gpu(args):
                       parity=not args.no_cpu_baseline)
 
 
-def config_line(r: dict, name: str) -> dict:
-    """A benched configuration in the headline's format (no roofline extras)."""
+def step_unit_bytes(r: dict):
+    """Per-unit byte shape of a benched step for the streaming probe: ((row, head) units,
+    (state, inputs, output) bytes per unit, the inputs rounded down to 64 bytes)."""
     s = r["shape"]
+    st, out = s["headdim"] * s["dstate"] * 4, s["block_len"] * s["headdim"] * 4
+    units = s["batch"] * s["nheads"]
+    return units, (st, (r["step_bytes"] - units * (st + out)) // units // 64 * 64, out)
+
+
+def config_line(r: dict, name: str) -> dict:
+    """A benched configuration in the headline's format, with the streaming probe at its
+    step's byte shape beside it."""
+    s = r["shape"]
+    units, unit = step_unit_bytes(r)
+    ceiling = run_stream_ceiling(unit, units)
     return {
         "workload": name,
         "value": round(r["value"], 1), "unit": "tokens/s",
@@ -297,6 +309,9 @@ def config_line(r: dict, name: str) -> dict:
         "step_bytes": r["step_bytes"], "step_gbs": round(r["achieved_gbs"], 1),
         "frac": round(r["achieved_gbs"] / HBM_PEAK_GBS, 4),
         "commit_gbs": round(r["commit_gbs"], 1),
+        "stream_ceiling_gbs": None if ceiling is None else ceiling["gbs"],
+        "frac_of_stream_ceiling": None if ceiling is None
+        else round(r["achieved_gbs"] / ceiling["gbs"], 4),
     }
 
 
@@ -1344,9 +1359,7 @@ def main():
     r = run_gpu(args)
     extras = {}
     s = r["shape"]
-    unit = (s["headdim"] * s["dstate"] * 4, 0, s["block_len"] * s["headdim"] * 4)
-    units = s["batch"] * s["nheads"]
-    unit = (unit[0], (r["step_bytes"] - units * (unit[0] + unit[2])) // units // 64 * 64, unit[2])
+    units, unit = step_unit_bytes(r)
     ceiling = run_stream_ceiling(unit, units)
     if not args.no_extras:
         extras["configs"] = run_other_configs(args)
