@@ -120,7 +120,10 @@ template <int NS, int NCH, bool COMMIT>
 __global__ void __launch_bounds__(64 * NCH) __attribute__((amdgpu_waves_per_eu(2)))
 bdlm_long_block_kernel(const LongArgs a) {
     constexpr int QN = NS / 16;        // dstate quads
-    constexpr int RS = NS + 4;         // row stride (elements) of a wave's row images
+    // row stride (elements) of a wave's row images: NS + 8 puts consecutive rows 4 banks
+    // apart (of 64), so the operand-quad reads (16 rows x 4 lane groups), the transposed
+    // two-byte reads and the 16-byte row writes each touch distinct banks
+    constexpr int RS = NS + 8;
     constexpr int REG = kCh * RS * 2;  // bytes of a wave's LDS region
     constexpr int PR = NS / 8;         // 16-byte pieces per B / C row
     constexpr int RPI = 64 / PR;       // rows per load instruction (a row per PR lanes)
@@ -190,11 +193,8 @@ bdlm_long_block_kernel(const LongArgs a) {
     auto stage_rows = [&](const u32x4 (&v)[PR]) {
         const int rl = lane / PR, pc = lane % PR;
 #pragma unroll
-        for (int i = 0; i < PR; ++i) {
-            uint2 *dst = reinterpret_cast<uint2 *>(&img[(RPI * i + rl) * RS + pc * 8]);
-            dst[0] = uint2{v[i][0], v[i][1]};
-            dst[1] = uint2{v[i][2], v[i][3]};
-        }
+        for (int i = 0; i < PR; ++i)
+            *reinterpret_cast<u32x4 *>(&img[(RPI * i + rl) * RS + pc * 8]) = v[i];
     };
     uint2 xq[4];
 #pragma unroll

@@ -443,7 +443,7 @@ def long_model(NS, NCH, commit, want_y=True):
     """bdlm_long_block_kernel (bdlm_long.hip): wave c owns chunk c and its LDS region, which
     holds the chunk's C row image, then its B row image, then the local states it publishes;
     one barrier, after which every wave reads the other chunks' published states."""
-    QN, RS = NS // 16, NS + 4
+    QN, RS = NS // 16, NS + 8
     REG = 64 * RS * 2
     PR, RPI = NS // 8, 64 // (NS // 8)
     names = ["Cs", "Ex", "Dt", "Ec", "Er", "Wf", "Wr", "La", "Lb", "Ua", "Ub"]
@@ -489,11 +489,10 @@ def long_model(NS, NCH, commit, want_y=True):
                 rl, pc = l // PR, l % PR
                 for i in range(PR):
                     row = RPI * i + rl
-                    for h in range(2):
-                        off = base + ((row * RS + pc * 8 + 4 * h) * 2)
-                        i0 = nxt()
-                        for e in range(4):
-                            m.access(t, "W", i0, "reg", off + 2 * e, 2, tag=(what, row, pc * 8 + 4 * h + e))
+                    off = base + (row * RS + pc * 8) * 2
+                    i0 = nxt()
+                    for e in range(8):
+                        m.access(t, "W", i0, "reg", off + 2 * e, 2, tag=(what, row, pc * 8 + e))
 
             def quad(what, row, n0):
                 i0 = nxt()
