@@ -1080,13 +1080,28 @@ def span_per_node(disp, run_len: int) -> float | None:
     return st.median(spans) if spans else None
 
 
+def profiled_sha(src: str, which: str) -> str:
+    """The kernel-source hash recorded next to a rocprofv3 output directory when it was
+    taken (source_sha_<which>.txt, written by the profiling commands), so a summary is
+    stamped with the sources that produced its numbers; refuses to stamp a directory
+    taken on other sources than the current ones."""
+    f = os.path.join(src, f"source_sha_{which}.txt")
+    if not os.path.exists(f):
+        raise SystemExit(f"{f} missing: record `bench.py --source-sha {which}` with the profile")
+    sha = open(f).read().strip()
+    if sha != kernel_source_sha(which):
+        raise SystemExit(f"{src} was profiled on sources {sha}, the tree holds "
+                         f"{kernel_source_sha(which)}: profile again")
+    return sha
+
+
 def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> None:
     """Write the three block-step summaries under ``out_dir`` from a rocprofv3 output
     directory ``src`` holding trace_kernel_stats.csv / trace_kernel_trace.csv (kernel
     trace), fetch/write/copyfetch/copywrite_counter_collection.csv (HBM traffic) and
     mfma_counter_collection.csv (MfmaUtil), taken with the commands listed in them."""
     import statistics as st
-    sha = kernel_source_sha("block")
+    sha = profiled_sha(src, "block")
     hdr = f"- kernel_source_sha256_16: `{sha}`\n"
     R = "python3 $R/bench.py --steps 20 --warmup 5 --no-extras --no-cpu-baseline"
     pre = "cd /tmp && export TMPDIR=/tmp && "
@@ -1128,6 +1143,7 @@ def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> No
             "the roofline fraction uses, not an equal of it.  The commit kernel's mean covers the "
             "prefix commits (no clean-block outputs) and the cycle commits (with them).\n\n"
             f"Command (R = repository root, OUT = an output directory; MI355X, ROCm 7.2):\n\n"
+            f"    python3 $R/bench.py --source-sha block > $OUT/source_sha_block.txt\n"
             f"    {cmd_trace}\n    python3 bench.py --write-block-profiles $OUT profiles\n\n"
             "## Kernel statistics (whole run)\n\n" + summarize_trace(stats) + "\n")
     open(os.path.join(out_dir, "block_step_350m_b16_L32_kernel_trace.md"), "w").write(text)
@@ -1148,7 +1164,8 @@ def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> No
             f"- fetch_scale: {t['fetch_scale']:.4f}\n- write_scale: {t['write_scale']:.4f}\n\n"
             "FETCH_SIZE and WRITE_SIZE (KiB per dispatch, median over dispatches) scaled by what "
             "the same counter reads for a plain 256 MiB device copy (bytes = KiB x 1024 x scale).\n\n"
-            f"Commands (R = repository root, OUT = an output directory):\n\n{cmds}\n"
+            f"Commands (R = repository root, OUT = an output directory):\n\n"
+            f"    python3 $R/bench.py --source-sha block > $OUT/source_sha_block.txt\n{cmds}\n"
             f"    python3 bench.py --write-block-profiles $OUT profiles\n\n"
             f"| kernel | dispatches | fetch bytes | write bytes |\n|---|---|---|---|\n"
             f"| step `{STEP_KERNEL}` | {t['step']['dispatches']} | {t['step']['fetch_bytes']:,} | "
@@ -1172,6 +1189,7 @@ def write_block_profiles(src: str, out_dir: str, nl: int = 32, p: int = 8) -> No
             "of the launch's active cycles in which a SIMD's matrix unit is busy.  The step is "
             "bound by HBM, so this is evidence of where the Gram and split-bf16 products sit, "
             "not a roof.\n\nCommand (R = repository root, OUT = an output directory):\n\n"
+            "    python3 $R/bench.py --source-sha block > $OUT/source_sha_block.txt\n"
             f"    {pre}rocprofv3 --pmc MfmaUtil --output-format csv -d $OUT -o mfma -- {R}\n"
             f"    python3 bench.py --write-block-profiles $OUT profiles\n")
     open(os.path.join(out_dir, "sq_counters_block_step_350m_b16_L32.md"), "w").write(text)
@@ -1207,13 +1225,14 @@ def write_seq_profiles(src: str, out_dir: str) -> None:
     output directory ``src`` holding trace_kernel_trace.csv, fetch/write/copyfetch/
     copywrite_counter_collection.csv and p1/p2/mfma_counter_collection.csv, taken with the
     commands listed in them."""
-    hdr = f"- kernel_source_sha256_16: `{kernel_source_sha('all')}`\n"
+    hdr = f"- kernel_source_sha256_16: `{profiled_sha(src, 'all')}`\n"
     pre = "cd /tmp && export TMPDIR=/tmp && "
     R = "python3 $R/bench.py --sequence-only"
     cal = "python3 $R/bench.py --copy-calibration"
     tail = "    python3 bench.py --write-seq-profiles $OUT profiles\n"
     f = [os.path.join(src, f"{k}_counter_collection.csv") for k in ("fetch", "write", "copyfetch", "copywrite")]
-    cmds = (f"    {pre}rocprofv3 --kernel-trace --stats --output-format csv -d $OUT -o trace -- {R} --contrast-reps 5\n"
+    cmds = ("    python3 $R/bench.py --source-sha all > $OUT/source_sha_all.txt\n"
+            f"    {pre}rocprofv3 --kernel-trace --stats --output-format csv -d $OUT -o trace -- {R} --contrast-reps 5\n"
             + "".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {a}\n"
                       for c, o, a in (("FETCH_SIZE", "fetch", R + " --contrast-reps 1"),
                                       ("WRITE_SIZE", "write", R + " --contrast-reps 1"),
@@ -1235,8 +1254,9 @@ def write_seq_profiles(src: str, out_dir: str) -> None:
               ("p2", "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_LDS "
                      "SQ_LDS_IDX_ACTIVE SQ_ACTIVE_INST_VMEM SQ_WAIT_ANY"),
               ("mfma", "MfmaUtil")]
-    cmds = "".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {R} --contrast-reps 1\n"
-                   for o, c in passes) + tail
+    cmds = ("    python3 $R/bench.py --source-sha all > $OUT/source_sha_all.txt\n" +
+            "".join(f"    {pre}rocprofv3 --pmc {c} --output-format csv -d $OUT -o {o} -- {R} --contrast-reps 1\n"
+                    for o, c in passes) + tail)
     text = ("# SQ counters per dispatch (median): sequence kernels and block variants, 350M layer shape\n\n"
             + hdr + "\nThe workloads of the sequence trace summary, one timed repetition of the "
             "contrast; one pass per counter set (at most 8 SQ counters each).  MfmaUtil is "
