@@ -115,6 +115,49 @@ def test_long_block_chunked_shapes(H, N, L, G):
     np.testing.assert_array_equal(got[1], pool[1].astype(np.float32))     # untouched slot
 
 
+def _decay_regime(d, regime):
+    """Inputs with extreme decays: "fast" (dt x 300: a token's decay reaches 2^-60, and
+    most products of decay factors underflow to zero) or "slow" (A x 1e-4: decays within
+    1e-3 of one, so whole blocks add up undamped)."""
+    if regime == "fast":
+        dt = bi.bf16_bits_to_f32(d["dt"]) * np.float32(300.0)
+        d["dt"] = bi.to_bf16_bits(dt)
+    else:
+        d["A"] = (d["A"] * np.float32(1e-4)).astype(np.float32)
+    return d
+
+
+@pytest.mark.parametrize("regime", ["fast", "slow"])
+@pytest.mark.parametrize("L", [32, 256, 150])
+def test_extreme_decays(regime, L):
+    """The block kernel (L 32) and the long-block kernel (L 150, 256) under extreme decays:
+    no overflow, NaN or lost precision in the decay factors; step and commit against the
+    oracle."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 2, 4, 64, 128, 1, L, 0, True, 1, 10400 + L + (regime == "fast"))
+    d = _decay_regime(bi.block_inputs(w, 0), regime)
+    c = _decay_regime(bi.commit_inputs(w), regime)
+    pool = bi.random_state(w, 2, 11, 0.5).astype(np.float64)
+    h = pool_dev(pool)
+    v = to_dev(d)
+    say("extreme decays", regime, "L", L)
+    y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], h)
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all()
+    e = rel_err(y, oracle.block_step(d, pool))
+    nc, nb = np.zeros(2, np.int64), np.zeros(2, np.int64)
+    ref_pool = pool.copy()
+    rc, y_ref = oracle.commit(c, ref_pool, nc.copy(), nb.copy(), expected_block_index=0, want_y=True)
+    assert rc == 0
+    vc = to_dev(c)
+    out = bd.commit_boundary(vc["x"], vc["dt"], vc["A"], vc["B"], vc["C"], vc["D"], vc["D_rev"], h,
+                             nc, nb, 0, y_clean=True)
+    torch.cuda.synchronize()
+    eh, ey = rel_err(from_pool(h), ref_pool), rel_err(out, y_ref)
+    say("  rel err step", e, "state", eh, "clean y", ey)
+    assert max(e, eh, ey) <= REL_TOL
+
+
 def test_long_block_fp32_sequence_path():
     """fp32 activations in blocks longer than 64 tokens keep the sequence kernels' path."""
     import paper_2607_02805_amd as bd
