@@ -262,6 +262,8 @@ def run_config(w, p: int, nl: int, prefix: int, steps: int, warmup: int,
         "avg_step_us": avg_step_s * 1e6,
         "median_step_us": float(np.median(t["step_us"])),
         "min_step_us": float(t["step_us"].min()),
+        "step_us_per_replay": [float(v) for v in t["step_us"]],
+        "commit_us_per_replay": [float(v) for v in t["commit_us"]],
         "avg_commit_us": avg_commit_s * 1e6,
         "step_bytes": sb,
         "commit_bytes": cb,
@@ -1269,6 +1271,39 @@ def write_seq_profiles(src: str, out_dir: str) -> None:
     open(os.path.join(out_dir, "sq_counters_sequence_kernels_350m.md"), "w").write(text)
 
 
+def write_timing_profile(path: str, r: dict, roof: dict, argv: list) -> None:
+    """The HIP-event timing behind roofline.frac, written by the run that measured it: per
+    timed replay of the ring's step graph, the time per step node, and the figures
+    derived from them (the rocprofv3 trace of the same command serialises dispatches, so
+    its durations are reported beside these, not in their place)."""
+    sb = r["step_bytes"]
+    st = r["step_us_per_replay"]
+    lines = [
+        "# Block step timing by HIP events: 350M layer shape, batch 16, L 32, 262K prefix", "",
+        f"- kernel_source_sha256_16: `{kernel_source_sha('block')}`",
+        f"- step_nodes_per_replay: {r['layers'] * r['denoise_steps']}",
+        f"- timed_replays: {len(st)}",
+        f"- step_us_mean: {np.mean(st):.4f}",
+        f"- step_us_median: {np.median(st):.4f}",
+        f"- step_bytes_per_launch: {sb}",
+        f"- achieved_gbs: {sb / np.mean(st) / 1e3:.1f}",
+        f"- frac_of_8tbs: {sb / np.mean(st) / 1e3 / HBM_PEAK_GBS:.4f}",
+        f"- commit_us_mean: {np.mean(r['commit_us_per_replay']):.4f}",
+        f"- stream_ceiling_gbs: {roof.get('stream_ceiling_gbs')}",
+        "",
+        "Each timed replay runs the ring's step graph (every layer's denoising steps, one "
+        "launch per node) between two HIP events on the replay stream; the time per node is "
+        "the events' interval divided by the node count.  `achieved_gbs` = algorithmic bytes "
+        "per launch / `step_us_mean`, the figure `roofline.frac` is computed from.", "",
+        f"Command (R = repository root; MI355X, ROCm 7.2):", "",
+        f"    python3 $R/bench.py {' '.join(argv)}", "",
+        "| replay | step us per node | commit us per node |", "|---|---|---|"]
+    lines += [f"| {i} | {a:.4f} | {b:.4f} |" for i, (a, b) in
+              enumerate(zip(st, r["commit_us_per_replay"]))]
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def copy_calibration(nbytes: int = 256 << 20, reps: int = 5):
     """A plain device-to-device copy of known size, for scaling HBM counters (FETCH_SIZE,
     WRITE_SIZE) of profiled kernels to bytes."""
@@ -1324,6 +1359,8 @@ def main():
     ap.add_argument("--write-seq-profiles", nargs=2, metavar=("ROCPROF_DIR", "OUT_DIR"),
                     help="write the sequence/variant profile summaries from a rocprofv3 output "
                          "directory and exit")
+    ap.add_argument("--timing-profile", metavar="PATH",
+                    help="also write the HIP-event timing behind roofline.frac to PATH")
     ap.add_argument("--source-sha", choices=sorted(SOURCE_SETS),
                     help="print the hash of a kernel family's sources and exit")
     args = ap.parse_args()
@@ -1471,6 +1508,8 @@ def main():
         line["roofline"]["copy_same_bytes_gbs"] = cr["gbs"]
         line["roofline"]["frac_of_copy"] = round(r["achieved_gbs"] / cr["gbs"], 4)
     line.update(extras)
+    if args.timing_profile:
+        write_timing_profile(args.timing_profile, r, line["roofline"], sys.argv[1:])
     print(json.dumps(line), flush=True)
 
 

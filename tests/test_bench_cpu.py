@@ -73,3 +73,19 @@ def test_source_sets_name_existing_files():
         for f in files:
             assert os.path.exists(os.path.join(bench.CSRC, f)), (which, f)
         assert len(bench.kernel_source_sha(which)) == 16
+
+
+def test_timing_profile_recomputes_the_fraction(tmp_path):
+    """The timing summary the bench writes holds what roofline.frac is computed from: the
+    mean time per step node over the timed replays and the algorithmic bytes."""
+    sb = bench.step_bytes(16, 32, 64, 128, 1, 32)
+    r = {"step_bytes": sb, "step_us_per_replay": [6.2, 6.3, 6.25],
+         "commit_us_per_replay": [9.1, 9.2, 9.3], "layers": 32, "denoise_steps": 8}
+    p = tmp_path / "timing.md"
+    bench.write_timing_profile(str(p), r, {"stream_ceiling_gbs": 4000.0}, ["--steps", "3"])
+    kv = bench.profile_fields(str(p))
+    mean = bench._num(kv, "step_us_mean")
+    assert abs(mean - 6.25) < 1e-9
+    frac = sb / (mean * 1e3) / bench.HBM_PEAK_GBS
+    assert abs(bench._num(kv, "frac_of_8tbs") - frac) < 1e-4
+    assert bench._num(kv, "timed_replays", int) == 3
