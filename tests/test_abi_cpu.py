@@ -611,3 +611,13 @@ def test_commit_step_checks(L):
     assert chk(nb=np.array([3, 3, 0, 0], np.int64), expect=3) == bd.OK
     assert chk(nb=np.array([3, 2, 0, 0], np.int64), expect=3) == bd.E_OFFSET
     assert chk(dd=desc(batch=2, L=65)) == bd.E_SHAPE                   # up to 64 tokens
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    """With the HIP library absent the binding raises instead of computing anything (there
+    is no CPU path)."""
+    import paper_2607_02805_amd as bd
+    monkeypatch.setattr(bd, "_lib", None)
+    monkeypatch.setattr(bd, "LIB_PATH", str(tmp_path / "libbdlm.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        bd.lib()
