@@ -23,12 +23,16 @@
 // Work split: one workgroup per (batch row, head, 16 head-dim columns), so a state
 // slice (16 x N) fits one wave's registers and the grid holds four workgroups per
 // (row, head).  Every wave computes its chunk's full decay-weighted Gram matrix C.B^T
-// (the four column slices of a head each recompute it) on bf16 MFMA from B and C quads
-// loaded straight into operand registers; the contractions over tokens (local states)
-// read B transposed from a row image the wave writes into its own LDS region, which
-// later holds the local states it publishes.  Products with an fp32 operand split it
-// into bf16 terms (two; three for the local forward states of a commit, whose sum
-// becomes a cached state).  bf16 activations only.
+// (the four column slices of a head each recompute it) on bf16 MFMA.  B and C are
+// loaded as whole rows (every 16 lanes read 256 contiguous bytes) and rearranged into
+// operand quads through a row image in the wave's own LDS region: C's quads are kept in
+// registers for the Gram tiles and the prefix terms, B's are read back for the Gram
+// tiles and, transposed, for the contractions over tokens (local states); the region
+// then holds the local states the wave publishes.  Decay weights come from per-token
+// factors relative to 16-token tile boundaries (one exponential per token and factor,
+// one per tile pair), each at most 1.  Products with an fp32 operand split it into bf16
+// terms (two; three for the local forward states of a commit, whose sum becomes a
+// cached state).  bf16 activations only.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -121,8 +125,9 @@ __global__ void __launch_bounds__(64 * NCH) __attribute__((amdgpu_waves_per_eu(2
 bdlm_long_block_kernel(const LongArgs a) {
     constexpr int QN = NS / 16;        // dstate quads
     // row stride (elements) of a wave's row images: NS + 8 puts consecutive rows 4 banks
-    // apart (of 64), so the operand-quad reads (16 rows x 4 lane groups), the transposed
-    // two-byte reads and the 16-byte row writes each touch distinct banks
+    // apart, so the operand-quad reads (16 rows x 4 lane groups), the transposed two-byte
+    // reads and the 16-byte row writes spread over the banks (measured: no conflicts left
+    // but those of the two-byte reads themselves)
     constexpr int RS = NS + 8;
     constexpr int REG = kCh * RS * 2;  // bytes of a wave's LDS region
     constexpr int PR = NS / 8;         // 16-byte pieces per B / C row
@@ -162,10 +167,10 @@ bdlm_long_block_kernel(const LongArgs a) {
     const bool want_y = a.y != nullptr;
     uint16_t *img = reinterpret_cast<uint16_t *>(sReg[c]);
 
-    // ---- loads: dt (lane = token), x quads (tokens 16jt + 4grp .. +3 at column p), B and
-    // C operand quads (row 16mt + col, dstate 16q + 4grp .. +3); rows past the block read 0
-    // (resource bases are uniform across the wave: a per-lane base would make the compiler
-    // loop over the lanes' distinct values for every access)
+    // ---- loads: dt (lane = token), B and C rows, x quads (tokens 16jt + 4grp .. +3 at
+    // column p); rows past the block read 0 (resource bases are uniform across the wave: a
+    // per-lane base would make the compiler loop over the lanes' distinct values for every
+    // access)
     const char *xb = static_cast<const char *>(a.x) + (b * a.xs_b + t0 * a.xs_t + h * a.xs_h + p0) * 2;
     const char *db = static_cast<const char *>(a.dt) + (b * a.dts_b + t0 * a.dts_t + h) * 2;
     const int64_t bco = (b * a.bcs_b + t0 * a.bcs_t + g * a.bcs_g) * 2;
