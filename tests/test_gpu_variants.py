@@ -75,7 +75,7 @@ def test_long_block_commit(H, N, L, want_y):
 
 @pytest.mark.parametrize("H,N,L,G", [(4, 16, 256, 1), (4, 32, 129, 2), (6, 64, 191, 1),
                                    (2, 128, 200, 2), (5, 128, 255, 1), (3, 64, 66, 1),
-                                   (8, 32, 192, 4), (3, 16, 130, 1)])
+                                   (8, 32, 192, 4), (3, 16, 130, 1), (1, 64, 193, 1)])
 def test_long_block_chunked_shapes(H, N, L, G):
     """Blocks of 65 to 256 tokens with bf16 inputs run as one launch over 64-token chunks
     side by side (two, three or four chunks; ragged last chunks from 1 to 63 tokens;
