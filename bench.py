@@ -42,7 +42,7 @@ CSRC = os.path.join(ROOT, "paper_2607_02805_amd", "csrc")
 SOURCE_SETS = {
     "block": ("bdlm_scan.hip", "bdlm_device.h"),
     "seq": ("bdlm_seq.hip", "bdlm_device.h"),
-    "all": ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_long.hip", "bdlm_conv.hip", "bdlm_norm.hip",
+    "all": ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_mask.hip", "bdlm_conv.hip", "bdlm_norm.hip",
             "bdlm_device.h", "bdlm_launch.h"),
 }
 KERNEL_SRCS = [os.path.join(CSRC, f) for f in SOURCE_SETS["block"]]
@@ -564,7 +564,7 @@ def _graph_time(fn, nlayers, reps=10):
 def run_variants(args) -> dict:
     """Block-step variants, each over a ring of 24 layers' states (cold reads):
     the paper's 350M geometry (d_inner 1664: 26 heads of 64, dstate 128) with its block
-    length 256 at batch 16 (step and commit, on the chunked long-block kernel), and the step with
+    length 256 at batch 16 (step and commit, on the masked long-block kernel), and the step with
     separate reverse-direction inputs at the 350M layer shape (32 heads, L 32)."""
     import torch
 
@@ -1208,9 +1208,9 @@ paper's 26, dstate 128, one group, bf16 activations unless stated):
   blocks) -- `seg_state` (4096), `seg_combine` (4096), `seg_out` with SUB = 32 carrying
   the state block by block and writing the block states and the clean outputs (4096),
   then the block step over 2,048 rows (65536 x 512);
-* paper geometry: batch 16, 26 heads, L = 256 -- `bdlm_long_block_kernel`, one
-  workgroup per (row, head, 16 head-dim columns), a wave per 64-token chunk (1,664
-  workgroups of 256 threads);
+* paper geometry: batch 16, 26 heads, L = 256 -- `bdlm_mask_block_kernel`, the block in
+  masked-matrix form, one workgroup of eight waves per (row, head), each wave owning 32
+  output tokens (416 workgroups of 512 threads);
 * separate reverse inputs: batch 16, L = 32 -- one block-kernel launch with both input
   sets (direction 3), 512 x 512;
 * convolution state: batch 16, L = 32 -- the fp32 block kernel with the convolution in

@@ -38,7 +38,7 @@ def _run(cmd: list[str]) -> None:
             sys.stderr.write(line + "\n")
 
 
-HIP_SRCS = ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_long.hip", "bdlm_conv.hip", "bdlm_norm.hip",
+HIP_SRCS = ("bdlm_scan.hip", "bdlm_seq.hip", "bdlm_mask.hip", "bdlm_conv.hip", "bdlm_norm.hip",
             "bdlm_scratch.hip")
 
 

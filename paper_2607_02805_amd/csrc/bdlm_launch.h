@@ -177,10 +177,10 @@ int launch_block_long(const LaunchArgs &fwd, const LaunchArgs &rev, bool commit,
                       void *stream);
 
 // Blocks of 65 to 256 tokens with bf16 activations and one input set for both branches:
-// one launch with the block's 64-token chunks side by side (bdlm_long.hip).
-bool long_chunked_fits(const LaunchArgs &a);
-int launch_long_chunked(const LaunchArgs &a, bool commit, bool want_y, void *stream);
-// A long block's step or commit with one input set: launch_long_chunked where it fits,
+// one launch in masked-matrix form, one workgroup per (row, head) (bdlm_mask.hip).
+bool long_masked_fits(const LaunchArgs &a);
+int launch_long_masked(const LaunchArgs &a, bool commit, bool want_y, void *stream);
+// A long block's step or commit with one input set: launch_long_masked where it fits,
 // else launch_block_long.
 int launch_block_long_shared(const LaunchArgs &a, bool commit, bool want_y, void *stream);
 

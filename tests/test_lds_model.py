@@ -4,7 +4,8 @@ interval, per wave and per lane (no GPU).
 Each kernel's LDS accesses are written out here from its source: for every thread, the
 array, the byte range and the direction of every LDS read and write between two
 workgroup barriers (the kernels' __syncthreads calls), for one 64-token chunk (sequence
-kernels) or one block (block kernel), at every dstate the kernels are built for.  The
+kernels) or one block (block kernel, masked long-block kernel), at every dstate the
+kernels are built for.  The
 checks, per interval:
 
 * no byte is written by one wave and read or written by another (with no barrier in
@@ -438,144 +439,178 @@ def block_model(LT, NS, commit, npart, want_y=True):
     return m
 
 
-# ------------------------------------------------------------- long-block kernel
-def long_model(NS, NCH, commit, want_y=True):
-    """bdlm_long_block_kernel (bdlm_long.hip): wave c owns chunk c and its LDS region, which
-    holds the chunk's C row image, then its B row image, then the local states it publishes;
-    one barrier, after which every wave reads the other chunks' published states."""
-    QN, RS = NS // 16, NS + 8
-    REG = 64 * RS * 2
-    PR, RPI = NS // 8, 64 // (NS // 8)
-    names = ["Cs", "Ex", "Dt", "Ec", "Er", "Wf", "Wr", "La", "Lb", "Ua", "Ub"]
-    arrays = {"reg": NCH * REG, "tot": 4 * NCH}
-    arrays.update({n: NCH * 64 * 4 for n in names})
+# ------------------------------------------------------------- masked long-block kernel
+def pair_idx(QP, mt, qp, grp, col):
+    """16-byte entry of the quad pair (2qp, 2qp + 1) of lane (col, grp) of token tile mt in
+    the masked long-block kernel's B and C images (bdlm_mask.hip, pair_idx)."""
+    return (mt * QP + qp) * 64 + grp * 16 + (col ^ ((2 * qp + (grp >> 1)) & 15))
+
+
+def mask_model(NS, MT, commit, want_y=True):
+    """bdlm_mask_block_kernel (bdlm_mask.hip): eight waves, wave w owning the output rows of
+    token tiles TPW w ..; the B image, the region that holds the C image and then the
+    transposed x and the split state images, and the per-token decay arrays.  Elements are
+    tagged, so every operand read is checked against the element the staging wrote there."""
+    QN = NS // 16
+    QP = (QN + 1) // 2
+    NW, NT = 8, 512
+    TPW = MT // NW
+    NTOK = 16 * MT
+    TPL = NTOK // 64
+    LPT = 16 // TPL
+    IMG, XTQ, SQP = MT * QP * 64, MT * 4 * 64, QP * 4 * 64
+    REGION = max(IMG * 16, XTQ * 8 + SQP * 32)
+    names = ["Dt", "Cs", "Ex", "Ec", "La", "Lb", "Ua", "Ub"] + (["Wc"] if commit else [])
+    arrays = {"sB": IMG * 16, "sU": REGION, "sE": 4 * MT}
+    arrays.update({n: NTOK * 4 for n in names})
     m = new_model(arrays)
-    m.same_wave_rewrites = True
-
-    class Lockstep:
-        """A wave's lanes issue each instruction together: accesses are collected per lane
-        and replayed instruction by instruction."""
-        def __init__(self):
-            self.ops = []
-
-        def access(self, tid, kind, instr, array, off, nbytes, tag=None):
-            self.ops.append((instr, len(self.ops), tid, kind, array, off, nbytes, tag))
-
-        def flush(self):
-            for instr, _, tid, kind, array, off, nbytes, tag in sorted(self.ops, key=lambda o: o[:2]):
-                outer.access(tid, kind, instr, array, off, nbytes, tag)
-            self.ops = []
-    outer = m
-    for c in range(NCH):
-        m = Lockstep()
-        need_f, need_r = commit or c + 1 < NCH, want_y and c > 0
-        base = c * REG
-        for l in range(64):
-            t, col, grp = 64 * c + l, l % 16, l // 16
-            ins = 0
-
-            def nxt():
-                nonlocal ins
-                ins += 1
-                return ins
-            for n in names:                       # per-token factors (lane = token)
-                m.access(t, "W", nxt(), n, (c * 64 + l) * 4, 4, tag=(n, c, l))
-            if l == 0:
-                m.access(t, "W", nxt(), "tot", 4 * c, 4, tag=("tot", c))
-            else:
-                nxt()
-
-            def stage(what):
-                rl, pc = l // PR, l % PR
-                for i in range(PR):
-                    row = RPI * i + rl
-                    off = base + (row * RS + pc * 8) * 2
-                    i0 = nxt()
-                    for e in range(8):
-                        m.access(t, "W", i0, "reg", off + 2 * e, 2, tag=(what, row, pc * 8 + e))
-
-            def quad(what, row, n0):
-                i0 = nxt()
-                for e in range(4):
-                    m.access(t, "R", i0, "reg", base + (row * RS + n0 + e) * 2, 2, tag=(what, row, n0 + e))
-            if want_y:
-                stage("C")
-                for mt in range(4):
-                    for q in range(QN):
-                        quad("C", 16 * mt + col, 16 * q + 4 * grp)
-            stage("B")
-            if want_y:
-                for mt in range(4):
-                    for n in ("Cs", "Ex", "La", "Ua"):
-                        m.access(t, "R", nxt(), n, (c * 64 + 16 * mt + col) * 4, 4, tag=(n, c, 16 * mt + col))
-                for jt in (0, 2):
-                    for d in range(2):
-                        for q in range(QN):
-                            quad("B", 16 * (jt + d) + col, 16 * q + 4 * grp)
-                    for d in range(2):
-                        jj = jt + d
-                        for n in ("Lb", "Ub", "Cs", "Ex", "Dt"):
-                            i0 = nxt()
-                            for r in range(4):
-                                j = 16 * jj + 4 * grp + r
-                                m.access(t, "R", i0, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
-            for jt in range(4):
-                for n in ("Wf", "Wr"):
-                    i0 = nxt()
-                    for r in range(4):
-                        j = 16 * jt + 4 * grp + r
-                        m.access(t, "R", i0, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
-            for q in range(QN):                   # B read transposed
-                for jt in range(4):
-                    for r in range(4):
-                        j = 16 * jt + 4 * grp + r
-                        m.access(t, "R", nxt(), "reg", base + (j * RS + 16 * q + col) * 2, 2,
-                                 tag=("B", j, 16 * q + col))
-            for q in range(QN):                   # publish
-                if need_f:
-                    m.access(t, "W", nxt(), "reg", base + ((4 * q + grp) * 16 + col) * 16, 16,
-                             tag=("F", c, q, grp, col))
-                if need_r:
-                    m.access(t, "W", nxt(), "reg", base + (QN * 64 + (4 * q + grp) * 16 + col) * 16, 16,
-                             tag=("R", c, q, grp, col))
-        m.flush()
-    m = outer
+    CPR = NS // 8
+    BCN = NTOK * CPR
+    BCK = BCN // NT if BCN >= NT else 1
+    XN = 4 * MT * 8
+    XK = XN // NT if XN >= NT else 1
+    SN = 16 * NS
+    SK = SN // NT if SN >= NT else 1
+    S_OFF = XTQ * 8                     # state hi image in the region; lo follows
+    # ---- interval 0: B and C images, the decay arrays (wave 0)
+    for tid in range(NT):
+        if tid >= BCN:
+            continue
+        for k in range(BCK):
+            i = tid + NT * k
+            t, c = i // CPR, i % CPR
+            q, gr = c >> 1, 2 * (c & 1)
+            at = 2 * pair_idx(QP, t >> 4, q >> 1, gr, t & 15) + (q & 1)
+            at1 = 2 * pair_idx(QP, t >> 4, q >> 1, gr + 1, t & 15) + (q & 1)
+            for arr, ok in (("sB", True), ("sU", want_y)):
+                if not ok:
+                    continue
+                name = arr if arr == "sB" else "C"
+                m.access(tid, "W", 1, arr, at * 8, 8, tag=(name, t, 16 * q + 4 * gr))
+                m.access(tid, "W", 2, arr, at1 * 8, 8, tag=(name, t, 16 * q + 4 * gr + 4))
+                if QN % 2 == 1 and q == QN - 1:
+                    m.access(tid, "W", 3, arr, (at + 1) * 8, 8, tag=("Z",))
+                    m.access(tid, "W", 4, arr, (at1 + 1) * 8, 8, tag=("Z",))
+    for lane in range(64):
+        for i in range(TPL):
+            t = TPL * lane + i
+            for n in names:
+                m.access(lane, "W", 10, n, 4 * t, 4)
+        if (lane & (LPT - 1)) == LPT - 1:
+            m.access(lane, "W", 11, "sE", 4 * ((TPL * lane) >> 4), 4)
     m.barrier()
-    for c in range(NCH):
-        for l in range(64):
-            t, col, grp = 64 * c + l, l % 16, l // 16
-            ins = 1000
+    # ---- interval 1: every wave's C quad pairs (then a barrier before the region is reused)
+    if want_y:
+        for tid in range(NT):
+            w, lane = tid // 64, tid % 64
+            col, grp = lane & 15, lane >> 4
+            for mm in range(TPW):
+                mt = TPW * w + mm
+                for qp in range(QP):
+                    e = pair_idx(QP, mt, qp, grp, col)
+                    hi = ("Z",) if 2 * qp + 1 >= QN else ("C", 16 * mt + col, 32 * qp + 16 + 4 * grp)
+                    m.access(tid, "R", 20, "sU", e * 16, 8, tag=("C", 16 * mt + col, 32 * qp + 4 * grp))
+                    m.access(tid, "R", 20, "sU", e * 16 + 8, 8, tag=hi)
+        m.barrier()
+    # ---- interval 2: transposed x, the state's hi / lo images
+    for tid in range(NT):
+        if tid < XN:
+            for k in range(XK):
+                task = tid + NT * k
+                tq, pc = task >> 3, task & 7
+                for d in range(4):
+                    for h in range(2):
+                        pcol = pc * 8 + 2 * d + h
+                        m.access(tid, "W", 30 + h, "sU", (tq * 64 + pcol) * 8, 8, tag=("X", tq, pcol))
+        if want_y and tid < SN:
+            for k in range(SK):
+                i = tid + NT * k
+                q, gp = i >> 8, i & 255
+                at = 2 * ((q >> 1) * 256 + gp) + (q & 1)
+                for img, off in (("SH", S_OFF), ("SL", S_OFF + SQP * 16)):
+                    m.access(tid, "W", 32, "sU", off + at * 8, 8, tag=(img, q, gp))
+                    if QN % 2 == 1 and q == QN - 1:
+                        m.access(tid, "W", 33, "sU", off + (at + 1) * 8, 8, tag=("Z",))
+    m.barrier()
+    # ---- interval 3: the masked product, the diagonal tiles, the prefix term and stores,
+    # the commit (reads only)
+    for tid in range(NT):
+        w, lane = tid // 64, tid % 64
+        col, grp = lane & 15, lane >> 4
+        mt0 = TPW * w
 
-            def rd(k, q, which):
-                nonlocal ins
-                ins += 1
-                off = k * REG + ((QN * 64 if which == "R" else 0) + (4 * q + grp) * 16 + col) * 16
-                m.access(t, "R", ins, "reg", off, 16, tag=(which, k, q, grp, col))
-            for k in range(c):
-                ins += 1
-                m.access(t, "R", ins, "tot", 4 * k, 4, tag=("tot", k))
-                for q in range(QN):
-                    rd(k, q, "F")
-            if commit and c == NCH - 1:
-                for q in range(QN):
-                    rd(c, q, "F")
-            if want_y:
-                for n, lo, hi in (("Ec", 0, 0), ("Er", 0, 0)):
-                    for mt in range(4):
-                        ins += 1
-                        for r in range(4):
-                            j = 16 * mt + 4 * grp + r
-                            m.access(t, "R", ins, n, (c * 64 + j) * 4, 4, tag=(n, c, j))
-                for k in range(NCH - 1, c, -1):
-                    ins += 1
-                    m.access(t, "R", ins, "tot", 4 * k, 4, tag=("tot", k))
-                    for q in range(QN):
-                        rd(k, q, "R")
+        def rd(instr, arr, off, n, tag=None):
+            m.access(tid, "R", instr, arr, off, n, tag=tag)
+
+        def xt(instr, tq, pcol):
+            rd(instr, "sU", (tq * 64 + pcol) * 8, 8, tag=("X", tq, pcol))
+
+        def b_pair(instr, jt, qp):
+            e = pair_idx(QP, jt, qp, grp, col)
+            rd(instr, "sB", e * 16, 8, tag=("sB", 16 * jt + col, 32 * qp + 4 * grp))
+            hi = ("Z",) if 2 * qp + 1 >= QN else ("sB", 16 * jt + col, 32 * qp + 16 + 4 * grp)
+            rd(instr, "sB", e * 16 + 8, 8, tag=hi)
+        if want_y:
+            for mm in range(TPW):
+                t = 16 * (mt0 + mm) + col
+                rd(40, "La", 4 * t, 4)
+                rd(41, "Ua", 4 * t, 4)
+            mm, jt = lane // MT, lane % MT
+            mt = mt0 + (mm if mm < TPW else 0)
+            for e in (mt - 1 if mt > 0 else 0, jt, jt - 1 if jt > 0 else 0, mt):
+                rd(42, "sE", 4 * e, 4)
+            for j0 in range(0, MT, 2):
+                for d in range(2):
+                    for qp in range(QP):
+                        b_pair(43, j0 + d, qp)
+                for mm in range(TPW):
+                    mt = mt0 + mm
+                    for d in range(2):
+                        jt = j0 + d
+                        rd(44, "Lb" if jt < mt else "Ub", 4 * (16 * jt + 4 * grp), 16)
+                for pt in range(4):
+                    xt(45, 4 * j0 + grp, 16 * pt + col)
+                    xt(46, 4 * (j0 + 1) + grp, 16 * pt + col)
+            for mm in range(TPW):
+                mt = mt0 + mm
+                for qp in range(QP):
+                    b_pair(47, mt, qp)
+                rd(48, "Cs", 4 * (16 * mt + col), 4)
+                rd(48, "Ex", 4 * (16 * mt + col), 4)
+                for n in ("Cs", "Ex", "Dt"):
+                    rd(49, n, 4 * (16 * mt + 4 * grp), 16)
+                for pt in range(4):
+                    xt(50, 4 * mt + grp, 16 * pt + col)
+                rd(51, "Ec", 4 * (16 * mt + 4 * grp), 16)
+            for pt in range(4):
+                for qp in range(QP):
+                    e = (qp * 4 + grp) * 64 + 16 * pt + col
+                    gp = grp * 64 + 16 * pt + col
+                    for img, off in (("SH", S_OFF), ("SL", S_OFF + SQP * 16)):
+                        hi = ("Z",) if 2 * qp + 1 >= QN else (img, 2 * qp + 1, gp)
+                        rd(52, "sU", off + e * 16, 8, tag=(img, 2 * qp, gp))
+                        rd(52, "sU", off + e * 16 + 8, 8, tag=hi)
+                for mm in range(TPW):
+                    xt(53, 4 * (mt0 + mm) + grp, 16 * pt + col)
+        if commit:
+            rd(60, "sE", 4 * (MT - 1), 4)
+            pt = w & 3
+            for jt in range(MT):
+                rd(61, "Wc", 4 * (16 * jt + 4 * grp), 16)
+                xt(62, 4 * jt + grp, 16 * pt + col)
+            for i in range((4 * QN + NW - 1) // NW):
+                kk = w + NW * i
+                if kk >= 4 * QN:
+                    break
+                q = kk >> 2
+                nb = (q & 1) * 4 + (col & 3)
+                for jt in range(MT):
+                    for r in range(4):
+                        e = pair_idx(QP, jt, q >> 1, col >> 2, 4 * grp + r) * 8 + nb
+                        rd(63, "sB", e * 2, 2, tag=("sB", 16 * jt + 4 * grp + r, 16 * q + 4 * (col >> 2)))
     m.barrier()
     return m
 
-
-# ---------------------------------------------------------------------- tests
 @pytest.mark.parametrize("NS", [16, 32, 64, 128])
 @pytest.mark.parametrize("both", [False, True])
 @pytest.mark.parametrize("swz", [False, True])
@@ -605,15 +640,15 @@ def test_block_kernel_lds(LT, NS, commit):
 
 
 @pytest.mark.parametrize("NS", [16, 32, 64, 128])
-@pytest.mark.parametrize("NCH", [2, 3, 4])
+@pytest.mark.parametrize("MT", [8, 16])
 @pytest.mark.parametrize("commit", [False, True])
-def test_long_block_kernel_lds(NS, NCH, commit):
-    assert long_model(NS, NCH, commit).check() == []
+def test_mask_block_kernel_lds(NS, MT, commit):
+    assert mask_model(NS, MT, commit).check() == []
     if commit:
-        assert long_model(NS, NCH, True, want_y=False).check() == []
+        assert mask_model(NS, MT, True, want_y=False).check() == []
 
 
-def test_long_block_model_catches_a_cross_wave_rewrite():
+def test_the_model_catches_cross_wave_rewrites():
     """Rewrites are allowed within a wave only: the same byte written by two waves in one
     interval, or by two lanes of one instruction, is still flagged."""
     w = new_model({"a": 256})
@@ -628,10 +663,9 @@ def test_long_block_model_catches_a_cross_wave_rewrite():
     v.access(0, "W", 1, "a", 0, 4)
     v.access(1, "W", 1, "a", 0, 4)      # two lanes, one instruction
     assert any(p[0] == "two writers in one interval" for p in v.check())
-    # the long-block kernel without its barrier: waves read states other waves publish
-    m = long_model(32, 3, False)
+    # the masked long-block kernel without its barriers: waves read images other waves write
+    m = mask_model(32, 8, False)
     merged = new_model(m.arrays)
-    merged.same_wave_rewrites = True
     for (iv, arr, b), lst in m.acc.items():
         merged.acc[(0, arr, b)].extend(lst)
     assert any(p[0] == "cross-wave access to a written byte" for p in merged.check())
