@@ -173,20 +173,51 @@ __device__ __forceinline__ uint4 gram_tile_bf16(const uint2 *iB, const uint2 *iC
     return uint4{a.x, a.y, c2.x, c2.y};
 }
 
+// The same tile from fp32 operand images on fp32 MFMA, unsplit (fp32 storage).
+template <int QN, int WDIR>
+__device__ __forceinline__ uint4 gram_tile_f32(const f32x4 *iB, const f32x4 *iC, const float *dCs,
+                                               const float *dEx, const float *dDt, int mt, int jt,
+                                               int grp, int col) {
+    f32x4 gacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < QN; ++q)
+        gacc = mma_q32(iB[img_idx<QN, true>(jt, q, grp, col)], iC[img_idx<QN, true>(mt, q, grp, col)], gacc);
+    const int t = 16 * mt + col;
+    const float cst = dCs[t], ext = dEx[t];
+    const f32x4 csj = *reinterpret_cast<const f32x4 *>(&dCs[16 * jt + 4 * grp]);
+    const f32x4 exj = *reinterpret_cast<const f32x4 *>(&dEx[16 * jt + 4 * grp]);
+    const f32x4 dtj = *reinterpret_cast<const f32x4 *>(&dDt[16 * jt + 4 * grp]);
+    f32x4 m;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int j = 16 * jt + 4 * grp + r;
+        const float e = exp2f(j < t ? cst - csj[r] : exj[r] - ext);
+        const float w = j == t ? (WDIR == kBoth ? 2.f : 1.f)
+                               : (j < t ? (WDIR == kRev ? 0.f : e) : (WDIR == kFwd ? 0.f : e));
+        m[r] = gacc[r] * w * dtj[r];
+    }
+    return __builtin_bit_cast(uint4, m);
+}
+
 // CV: the block's x, B and C are convolved while they are staged (bf16 inputs before
 // the mixer's convolution, fp32 operands after it; forward: the convolution continues
 // from the cached rows, reverse: zero past the block's end).
 template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR, bool CV>
-__global__ void __launch_bounds__(256 * NPART) __attribute__((amdgpu_waves_per_eu(2 * NPART)))
+__global__ void __launch_bounds__(256 * NPART)
+__attribute__((amdgpu_waves_per_eu(CV && DIR == kSep ? NPART : 2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
     static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep || DIR == kCS,
                   "direction");
     static_assert(DIR != kCS || (!F32 && COMMIT && !CV), "commit + step: bf16 storage");
-    static_assert(!CV || (F32 && (DIR == kFwd || DIR == kRev) && LT <= 32), "convolution staging");
+    static_assert(!CV || (F32 && (DIR == kFwd || DIR == kRev || DIR == kSep) && LT <= 32),
+                  "convolution staging");
     static_assert(!(COMMIT && DIR == kRev), "a commit updates the forward state");
     constexpr bool SEP = DIR == kSep;
     constexpr bool TWO = SEP || DIR == kCS;   // a second input set is staged
-    static_assert(!(SEP && (F32 || COMMIT)), "separate inputs: bf16 storage, step only");
+    // separate input sets: bf16 storage and steps only, except under convolution staging,
+    // where the two sets are the block's forward and reverse convolutions (fp32, and a
+    // commit updates the state from the forward set)
+    static_assert(!(SEP && !CV && (F32 || COMMIT)), "separate inputs: bf16 storage, step only");
     constexpr int NT = 256 * NPART;       // threads
     constexpr int NW = 4 * NPART;         // waves
     constexpr int MT = LT / 16;           // token tiles = quads along the block
@@ -210,7 +241,8 @@ bdlm_block_kernel(const KArgs args) {
     __shared__ __align__(16) uint4 sM[MT * MT * 64];                  // M: hi (xy), lo (zw)
     // the second input set's images, x, decay sums and matrix (kSep: the reverse branch;
     // kCS: the next block)
-    __shared__ __align__(16) uint2 sC2[TWO ? IMG : 1], sB2[TWO ? IMG : 1];
+    __shared__ __align__(16) uint2 sC2[TWO && !F32 ? IMG : 1], sB2[TWO && !F32 ? IMG : 1];
+    __shared__ __align__(16) f32x4 sCf2[TWO && F32 ? IMG : 1], sBf2[TWO && F32 ? IMG : 1];
     __shared__ __align__(16) AT sX2[TWO ? LT * XS : 1];
     __shared__ __align__(16) float sDt2[TWO ? 64 : 1], sCs2[TWO ? 64 : 1], sEx2[TWO ? 64 : 1];
     __shared__ __align__(16) uint4 sM2[TWO ? MT * MT * 64 : 1];
@@ -274,7 +306,7 @@ bdlm_block_kernel(const KArgs args) {
         }
     }
     u32x4 cch2[TWO ? BC_PT : 1], bch2[TWO ? BC_PT : 1], xch2[TWO ? X_PT : 1];
-    if constexpr (TWO) {
+    if constexpr (TWO && !CV) {
         const AT *Bg2 = static_cast<const AT *>(args.Bm2) + b * args.bcs_b + g * args.bcs_g;
         const AT *Cg2 = static_cast<const AT *>(args.Cm2) + b * args.bcs_b + g * args.bcs_g;
         const AT *xg2 = static_cast<const AT *>(args.x2) + b * args.xs_b + h * args.xs_h;
@@ -307,10 +339,10 @@ bdlm_block_kernel(const KArgs args) {
     typedef __attribute__((address_space(1))) const DT g_dt;
     const DT dtraw = *(lane < L ? (const g_dt *)(dtg + lane * args.dts_t)
                                 : (const g_dt *)(&kZeroChunk));
-    AT dtraw2 = AT(0);
+    DT dtraw2 = DT(0);
     if constexpr (TWO) {
-        const AT *dtg2 = static_cast<const AT *>(args.dt2) + b * args.dts_b + h;
-        dtraw2 = *(lane < L ? (const g_at *)(dtg2 + lane * args.dts_t) : (const g_at *)(&kZeroChunk));
+        const DT *dtg2 = static_cast<const DT *>(args.dt2) + b * args.dts_b + h;
+        dtraw2 = *(lane < L ? (const g_dt *)(dtg2 + lane * args.dts_t) : (const g_dt *)(&kZeroChunk));
     }
     // per-head parameters as vector loads in this first batch: a scalar load issued
     // later would queue behind the state loads of every workgroup
@@ -321,14 +353,18 @@ bdlm_block_kernel(const KArgs args) {
                                     : (tid == 1 ? args.D : (SEP && tid == 3 ? args.A2 : args.D_rev));
         parv = *(const g_f *)(par + h);
     }
-    // Convolution staging: task (matrix, channel quad, 8-token group) loads the 11 input
-    // rows its 8 outputs need (each row the sum of a cached-row load and an input-row
-    // load, the one that does not apply reading a zero chunk), the 4 channels' weights
-    // and biases.
+    // Convolution staging: task (matrix, channel quad, 8-token group) loads the input rows
+    // its 8 outputs need (each row the sum of a cached-row load and an input-row load, the
+    // one that does not apply reading a zero chunk), the 4 channels' weights and biases:
+    // rows t0-3 .. t0+7 for the forward convolution (before the block: the cache), t0 ..
+    // t0+10 for the reverse one (zero past the block's end), t0-3 .. t0+10 for both (kSep:
+    // the first input set is the forward convolution, the second the reverse one).
     constexpr int CQX = kP / 4, CQB = NS / 4, TG = LT / 8;
     constexpr int CV_TASKS = (CQX + 2 * CQB) * TG;
     static_assert(!CV || CV_TASKS <= NT, "one convolution task per thread");
-    f32x4 cu[CV ? 11 : 1], cw[CV ? 4 : 1], cb = {0.f, 0.f, 0.f, 0.f};
+    constexpr int CV_ROWS = DIR == kSep ? 14 : 11;
+    constexpr int CV_BASE = DIR == kRev ? 0 : 3;   // row i of the task is token t0 - CV_BASE + i
+    f32x4 cu[CV ? CV_ROWS : 1], cw[CV ? 4 : 1], cb = {0.f, 0.f, 0.f, 0.f};
     int cv_m = 0, cv_q = 0, cv_t0 = 0;   // matrix (0 x, 1 B, 2 C), channel quad, first token
     if constexpr (CV) {
         typedef unsigned v2u __attribute__((ext_vector_type(2)));
@@ -348,14 +384,13 @@ bdlm_block_kernel(const KArgs args) {
         const int64_t rs = cv_m == 0 ? args.xs_t : args.bcs_t;
         const float *crow = args.conv_pool + slot * 3 * static_cast<int64_t>(args.conv_ch) + c;
 #pragma unroll
-        for (int i = 0; i < 11; ++i) {
-            // forward rows t0-3 .. t0+7 (before the block: the cache), reverse t0 .. t0+10
-            const int rr = DIR == kFwd ? cv_t0 - 3 + i : cv_t0 + i;
+        for (int i = 0; i < CV_ROWS; ++i) {
+            const int rr = cv_t0 - CV_BASE + i;
             const bool in_blk = rr >= 0 && rr < L;
             const v2u u = *(in_blk ? (const g_u2 *)(src + rr * rs) : (const g_u2 *)(&kZeroChunk));
             f32x4 v = f32x4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
                             __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
-            if constexpr (DIR == kFwd)
+            if constexpr (DIR != kRev)
                 v += *(rr < 0 ? (const g_f4 *)(crow + (rr < 0 ? rr + 3 : 0) * args.conv_ch)
                               : (const g_f4 *)(&kZeroChunk));
             cu[i] = v;
@@ -383,17 +418,19 @@ bdlm_block_kernel(const KArgs args) {
 
     // ---- phase 1: LDS images
     if constexpr (CV) {
-        if (tid < CV_TASKS) {
+        // one direction's 8 outputs of the task, convolved and through SiLU, into (dX, dB,
+        // dC): forward w0 u[t-3] + ... + w3 u[t], reverse w0 u[t+3] + ... + w3 u[t]
+        auto conv_emit = [&](bool rev, AT *dX, f32x4 *dB, f32x4 *dC) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int t = cv_t0 + i;
                 f32x4 o;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    // forward: w0 u[t-3] + ... + w3 u[t]; reverse: w0 u[t+3] + ... + w3 u[t]
                     float a = cb[e];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) a += cw[e][k] * cu[DIR == kFwd ? i + k : i + 3 - k][e];
+                    for (int k = 0; k < 4; ++k)
+                        a += cw[e][k] * cu[rev ? i + 3 + CV_BASE - k : i + k + CV_BASE - 3][e];
                     // SiLU a / (1 + e^-a) on the hardware exp2 and reciprocal (each within
                     // a few ulp; the B and C channels are convolved by every head's
                     // workgroup, so this runs 5x more often than one pass over the
@@ -402,12 +439,20 @@ bdlm_block_kernel(const KArgs args) {
                     o[e] = t < L ? a * sg : 0.f;
                 }
                 if (cv_m == 0) {
-                    *reinterpret_cast<f32x4 *>(&sX[t * XS + 4 * cv_q]) = o;
+                    *reinterpret_cast<f32x4 *>(&dX[t * XS + 4 * cv_q]) = o;
                 } else {
                     const int at = img_idx<QN, true>(t >> 4, cv_q >> 2, cv_q & 3, t & 15);
-                    if (cv_m == 1) sBf[at] = o;
-                    else sCf[at] = o;
+                    if (cv_m == 1) dB[at] = o;
+                    else dC[at] = o;
                 }
+            }
+        };
+        if (tid < CV_TASKS) {
+            if constexpr (DIR == kSep) {
+                conv_emit(false, sX, sBf, sCf);
+                conv_emit(true, sX2, sBf2, sCf2);
+            } else {
+                conv_emit(DIR == kRev, sX, sBf, sCf);
             }
         }
     }
@@ -444,7 +489,7 @@ bdlm_block_kernel(const KArgs args) {
     if constexpr (TWO) {
 #pragma unroll
         for (int k = 0; k < BC_PT; ++k) {
-            if (!bc_owner) break;
+            if (CV || !bc_owner) break;
             const int i = tid + NT * k;
             const int t = i / CPR, c = i % CPR;
             const u32x4 cz = cch2[k], bz = bch2[k];
@@ -456,7 +501,7 @@ bdlm_block_kernel(const KArgs args) {
         }
 #pragma unroll
         for (int k = 0; k < X_PT; ++k) {
-            if (!x_owner) break;
+            if (CV || !x_owner) break;
             const int i = tid + NT * k;
             const int j = i / (kP / E), c = i % (kP / E);
             const u32x4 v = xch2[k];
@@ -479,7 +524,7 @@ bdlm_block_kernel(const KArgs args) {
         sCs[lane] = cs;
         sEx[lane] = lane == 0 ? 0.f : up;
         if constexpr (TWO) {   // the second set's decay sums (kSep: its own dt and A)
-            const float dtv2 = Act<F32>::val(dtraw2);
+            const float dtv2 = Act<F32 && !CV>::val(dtraw2);
             const float Ar2 =
                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(parv), SEP ? 3 : 0)) *
                 kLog2e;
@@ -512,10 +557,17 @@ bdlm_block_kernel(const KArgs args) {
         for (int tile = wave; tile < 2 * MT * MT; tile += NW) {
             const int tt = tile < MT * MT ? tile : tile - MT * MT;
             const int mt = tt / MT, jt = tt % MT;
-            if (tile < MT * MT)
-                sM[tt * 64 + lane] = gram_tile_bf16<QN, kFwd>(sB, sC, sCs, sEx, sDt, mt, jt, grp, col);
-            else
-                sM2[tt * 64 + lane] = gram_tile_bf16<QN, kRev>(sB2, sC2, sCs2, sEx2, sDt2, mt, jt, grp, col);
+            if constexpr (F32) {   // the block's two convolutions, fp32 operands
+                if (tile < MT * MT)
+                    sM[tt * 64 + lane] = gram_tile_f32<QN, kFwd>(sBf, sCf, sCs, sEx, sDt, mt, jt, grp, col);
+                else
+                    sM2[tt * 64 + lane] = gram_tile_f32<QN, kRev>(sBf2, sCf2, sCs2, sEx2, sDt2, mt, jt, grp, col);
+            } else {
+                if (tile < MT * MT)
+                    sM[tt * 64 + lane] = gram_tile_bf16<QN, kFwd>(sB, sC, sCs, sEx, sDt, mt, jt, grp, col);
+                else
+                    sM2[tt * 64 + lane] = gram_tile_bf16<QN, kRev>(sB2, sC2, sCs2, sEx2, sDt2, mt, jt, grp, col);
+            }
         }
     } else if constexpr (!F32) {
         for (int tile = wave; tile < MT * MT; tile += NW)
@@ -594,6 +646,14 @@ bdlm_block_kernel(const KArgs args) {
                     for (int jt = 0; jt < MT; ++jt)
                         ai = mma_q32(__builtin_bit_cast(f32x4, sM[(mt * MT + jt) * 64 + lane]),
                                      xquad(jt), ai);
+                    if constexpr (SEP) {   // + the reverse convolution's intra product and skip
+#pragma unroll
+                        for (int jt = 0; jt < MT; ++jt)
+                            ai = mma_q32(__builtin_bit_cast(f32x4, sM2[(mt * MT + jt) * 64 + lane]),
+                                         f32x4{xv2[jt][0], xv2[jt][1], xv2[jt][2], xv2[jt][3]}, ai);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) ai[r] += sPar[2] * xv2[mt][r];
+                    }
                 } else {
                     s16x4 mh[MT], ml[MT];
 #pragma unroll
@@ -1084,16 +1144,23 @@ int launch_conv_fused(const LaunchArgs &a, const float *w, const float *bias, co
     k.conv_ch = a.nheads * kP + 2 * a.ngroups * a.dstate;
     const unsigned grid = static_cast<unsigned>(static_cast<int64_t>(a.batch) * a.nheads);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    KArgs f = k;
-    if (!want_y) f.y = nullptr;
     hipError_t e;
-    if (a.L <= 16)
-        e = commit ? conv_by_ns<16, true, kFwd>(a.dstate, f, grid, s) : conv_by_ns<16, false, kFwd>(a.dstate, f, grid, s);
-    else
-        e = commit ? conv_by_ns<32, true, kFwd>(a.dstate, f, grid, s) : conv_by_ns<32, false, kFwd>(a.dstate, f, grid, s);
-    if (e != hipSuccess) return BDLM_E_LAUNCH;
-    if (!want_y) return BDLM_OK;
-    e = a.L <= 16 ? conv_by_ns<16, false, kRev>(a.dstate, k, grid, s) : conv_by_ns<32, false, kRev>(a.dstate, k, grid, s);
+    if (want_y) {
+        // one launch: both convolutions staged side by side (the forward one as the first
+        // input set, the reverse one as the second, same dt and A), both branches' intra
+        // products, the prefix term, a commit's state update from the forward set
+        k.dt2 = a.dt;
+        k.A2 = a.A;
+        if (a.L <= 16)
+            e = commit ? conv_by_ns<16, true, kSep>(a.dstate, k, grid, s) : conv_by_ns<16, false, kSep>(a.dstate, k, grid, s);
+        else
+            e = commit ? conv_by_ns<32, true, kSep>(a.dstate, k, grid, s) : conv_by_ns<32, false, kSep>(a.dstate, k, grid, s);
+        return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
+    }
+    // a commit without outputs: the forward convolution and the state update alone
+    KArgs f = k;
+    f.y = nullptr;
+    e = a.L <= 16 ? conv_by_ns<16, true, kFwd>(a.dstate, f, grid, s) : conv_by_ns<32, true, kFwd>(a.dstate, f, grid, s);
     return e == hipSuccess ? BDLM_OK : BDLM_E_LAUNCH;
 }
 
