@@ -15,7 +15,8 @@
 //                and for a prefill writes the final state 2^{T_{K-1}} Sin_{K-1} + F_{K-1}
 //                back to the cache;
 //   seg_out      the outputs of each segment in 64-token chunks from its entering state
-//                (the reverse pass adds its outputs to the forward pass's).
+//                (the reverse pass reads the forward pass's outputs a chunk at a time
+//                and stores the sums: one reader and writer per element, no atomics).
 // The reverse direction is the forward scan of the time-reversed sequence (every
 // token keeps its own x, dt, B, C), so seg_out loads each chunk flipped and walks
 // the segment's chunks backwards with the forward arithmetic.
@@ -619,6 +620,25 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             decay_sums<false>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, nullptr);
         __syncthreads();
         if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
+        // the reverse pass adds onto the forward pass's outputs: this lane's 16 of them are
+        // requested now, before the chunk's products, and stored back with the sums (one
+        // reader and writer per element, so the sum is exact fp32 and deterministic)
+        float yv[REV ? 16 : 1];
+        if constexpr (REV) {
+            if (a.y) {
+                const __amdgpu_buffer_rsrc_t rYl = rsrc(ybase + st.window(c) * (ytokB / 4));
+                const int lim = st.valid(c);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = 16 * mt + r;
+                        const uint32_t o = 16 * mt + 4 * grp + r < lim
+                                               ? oy - static_cast<uint32_t>(i * ytokB) : kOOB;
+                        yv[4 * mt + r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rYl, o, 0, 0));
+                    }
+            }
+        }
 
         // decay-weighted Gram tiles M[t][j] = 2^{cs_t - cs_j} dt_j (C_t . B_j), j <= t,
         // held as the transposed product (lane (grp, col): j = 16jt + 4grp + r, t = 16mt + col)
@@ -776,12 +796,9 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     const uint32_t o = 16 * mt + 4 * grp + r < lim
                                            ? oy + static_cast<uint32_t>((REV ? -i : i) * ytokB)
                                            : kOOB;
-                    // the reverse pass adds onto the forward pass's outputs in L2 (one
-                    // addend per element: the sum is exact fp32 and deterministic)
-                    if constexpr (REV)
-                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(out[r], rY, o, 0, 0);
-                    else
-                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(out[r]), rY, o, 0, kNT);
+                    float v = out[r];
+                    if constexpr (REV) v += yv[4 * mt + r];
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rY, o, 0, kNT);
                 }
             }
         }
