@@ -35,8 +35,8 @@
  *     <= 2^22 (within the 32-bit grid of a launch).  A block step or commit with
  *     L <= BDLM_MAX_BLOCK_LEN is one fused launch; longer blocks need per-token
  *     strides (and nheads * 64 * 4) of at most 16 MiB and run, with bf16 activations
- *     and L <= 256 (the paper's block length), as one launch over the block's 64-token
- *     chunks side by side, else on the sequence kernels as a forward launch from the
+ *     and L <= 256 (the paper's block length), as one launch computing the whole block
+ *     in masked-matrix form, else on the sequence kernels as a forward launch from the
  *     cached state and a reverse launch adding into y.
  *   - Activation storage (x, dt, B, C) is fp32 or bf16 (desc.in_dtype).  All
  *     arithmetic, states and outputs are fp32.

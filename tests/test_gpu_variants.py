@@ -77,10 +77,10 @@ def test_long_block_commit(H, N, L, want_y):
                                    (2, 128, 200, 2), (5, 128, 255, 1), (3, 64, 66, 1),
                                    (8, 32, 192, 4), (3, 16, 130, 1), (1, 64, 193, 1)])
 def test_long_block_chunked_shapes(H, N, L, G):
-    """Blocks of 65 to 256 tokens with bf16 inputs run as one launch over 64-token chunks
-    side by side (two, three or four chunks; ragged last chunks from 1 to 63 tokens;
-    every dstate; several groups): the step and then the commit with its clean-block
-    outputs, against the oracle."""
+    """Blocks of 65 to 256 tokens with bf16 inputs run as one masked-matrix launch (8 or
+    16 token tiles; ragged last tiles from 1 to 15 tokens; every dstate, the lone quad
+    of dstate 16 paired with zeros; several groups): the step and then the commit with
+    its clean-block outputs, against the oracle."""
     import paper_2607_02805_amd as bd
     w = bi.Workload("t", 3, H, 64, N, G, L, 0, True, 1, 10200 + H + N + L)
     d, c = bi.block_inputs(w, 0), bi.commit_inputs(w)
@@ -90,7 +90,7 @@ def test_long_block_chunked_shapes(H, N, L, G):
     slots = [3, 0, 2]
     h = pool_dev(pool)
     v = to_dev(d)
-    say("chunked long step", dict(H=H, N=N, L=L, G=G))
+    say("long step", dict(H=H, N=N, L=L, G=G))
     y = bd.scan_block_step(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], h,
                            slot_idx=slots)
     torch.cuda.synchronize()
