@@ -70,8 +70,9 @@ def test_step_and_commit_batch_1024_over_2048_slots():
 
 
 def test_long_block_and_separate_inputs_over_256_rows():
-    """Batch 300 slot-mapped: an 80-token block (the sequence kernels) step and commit,
-    and a separate-reverse-input step of 32 tokens (one fused launch per 256 rows)."""
+    """Batch 300 slot-mapped: an 80-token bf16 block (the masked long-block kernel, one
+    launch per 256 rows) step and commit, and a separate-reverse-input step of 32 tokens
+    (one fused launch per 256 rows)."""
     import paper_2607_02805_amd as bd
     B, S = 300, 400
     rng = np.random.default_rng(15200)
