@@ -50,6 +50,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "bdlm.h"
 #include "bdlm_device.h"
 #include "bdlm_launch.h"
@@ -204,7 +206,7 @@ __device__ __forceinline__ uint4 gram_tile_f32(const f32x4 *iB, const f32x4 *iC,
 // from the cached rows, reverse: zero past the block's end).
 template <int LT, int NS, bool F32, bool COMMIT, int NPART, int DIR, bool CV>
 __global__ void __launch_bounds__(256 * NPART)
-__attribute__((amdgpu_waves_per_eu(CV && DIR == kSep ? NPART : 2 * NPART)))
+__attribute__((amdgpu_waves_per_eu(2 * NPART)))
 bdlm_block_kernel(const KArgs args) {
     static_assert(DIR == kBoth || DIR == kFwd || DIR == kRev || DIR == kSep || DIR == kCS,
                   "direction");
@@ -242,9 +244,11 @@ bdlm_block_kernel(const KArgs args) {
     // the second input set's images, x, decay sums and matrix (kSep: the reverse branch;
     // kCS: the next block)
     __shared__ __align__(16) uint2 sC2[TWO && !F32 ? IMG : 1], sB2[TWO && !F32 ? IMG : 1];
-    __shared__ __align__(16) f32x4 sCf2[TWO && F32 ? IMG : 1], sBf2[TWO && F32 ? IMG : 1];
+    // (the block's reverse convolution, CV, passes through sBf / sCf before the forward one)
+    __shared__ __align__(16) f32x4 sCf2[TWO && F32 && !CV ? IMG : 1], sBf2[TWO && F32 && !CV ? IMG : 1];
     __shared__ __align__(16) AT sX2[TWO ? LT * XS : 1];
-    __shared__ __align__(16) float sDt2[TWO ? 64 : 1], sCs2[TWO ? 64 : 1], sEx2[TWO ? 64 : 1];
+    __shared__ __align__(16) float sDt2[TWO && !CV ? 64 : 1], sCs2[TWO && !CV ? 64 : 1],
+        sEx2[TWO && !CV ? 64 : 1];
     __shared__ __align__(16) uint4 sM2[TWO ? MT * MT * 64 : 1];
     __shared__ __align__(16) f32x4 sRed[(NPART > 1 ? NPART - 1 : 1) * 4 * MT * 64];
 
@@ -417,43 +421,43 @@ bdlm_block_kernel(const KArgs args) {
     for (int k = 0; k < QE; ++k) load_state(k);
 
     // ---- phase 1: LDS images
-    if constexpr (CV) {
-        // one direction's 8 outputs of the task, convolved and through SiLU, into (dX, dB,
-        // dC): forward w0 u[t-3] + ... + w3 u[t], reverse w0 u[t+3] + ... + w3 u[t]
-        auto conv_emit = [&](bool rev, AT *dX, f32x4 *dB, f32x4 *dC) {
+    // one direction's 8 outputs of the task, convolved and through SiLU, into (dX, dB,
+    // dC): forward w0 u[t-3] + ... + w3 u[t], reverse w0 u[t+3] + ... + w3 u[t]
+    auto conv_emit = [&](auto rev_tag, AT *dX, f32x4 *dB, f32x4 *dC) {
+        constexpr bool rev = decltype(rev_tag)::value;   // a template: instantiated only under CV
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int t = cv_t0 + i;
-                f32x4 o;
+        for (int i = 0; i < 8; ++i) {
+            const int t = cv_t0 + i;
+            f32x4 o;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float a = cb[e];
+            for (int e = 0; e < 4; ++e) {
+                float a = cb[e];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        a += cw[e][k] * cu[rev ? i + 3 + CV_BASE - k : i + k + CV_BASE - 3][e];
-                    // SiLU a / (1 + e^-a) on the hardware exp2 and reciprocal (each within
-                    // a few ulp; the B and C channels are convolved by every head's
-                    // workgroup, so this runs 5x more often than one pass over the
-                    // channels); padded rows stay zero
-                    const float sg = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-a * kLog2e));
-                    o[e] = t < L ? a * sg : 0.f;
-                }
-                if (cv_m == 0) {
-                    *reinterpret_cast<f32x4 *>(&dX[t * XS + 4 * cv_q]) = o;
-                } else {
-                    const int at = img_idx<QN, true>(t >> 4, cv_q >> 2, cv_q & 3, t & 15);
-                    if (cv_m == 1) dB[at] = o;
-                    else dC[at] = o;
-                }
+                for (int k = 0; k < 4; ++k)
+                    a += cw[e][k] * cu[rev ? i + 3 + CV_BASE - k : i + k + CV_BASE - 3][e];
+                // SiLU a / (1 + e^-a) on the hardware exp2 and reciprocal (each within
+                // a few ulp; the B and C channels are convolved by every head's
+                // workgroup, so this runs 5x more often than one pass over the
+                // channels); padded rows stay zero
+                const float sg = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-a * kLog2e));
+                o[e] = t < L ? a * sg : 0.f;
             }
-        };
-        if (tid < CV_TASKS) {
-            if constexpr (DIR == kSep) {
-                conv_emit(false, sX, sBf, sCf);
-                conv_emit(true, sX2, sBf2, sCf2);
+            if (cv_m == 0) {
+                *reinterpret_cast<f32x4 *>(&dX[t * XS + 4 * cv_q]) = o;
             } else {
-                conv_emit(DIR == kRev, sX, sBf, sCf);
+                const int at = img_idx<QN, true>(t >> 4, cv_q >> 2, cv_q & 3, t & 15);
+                if (cv_m == 1) dB[at] = o;
+                else dC[at] = o;
             }
+        }
+    };
+    if constexpr (CV) {
+        // both directions (kSep): the reverse convolution first, through the same images
+        // as the forward one; its Gram tiles are formed and kept (below) before the forward
+        // convolution overwrites them, so two fp32 image sets fit in the LDS of one
+        if (tid < CV_TASKS) {
+            if constexpr (DIR == kSep) conv_emit(std::true_type{}, sX2, sBf, sCf);
+            else conv_emit(std::integral_constant<bool, DIR == kRev>{}, sX, sBf, sCf);
         }
     }
 #pragma unroll
@@ -523,7 +527,7 @@ bdlm_block_kernel(const KArgs args) {
         sDt[lane] = dtv;
         sCs[lane] = cs;
         sEx[lane] = lane == 0 ? 0.f : up;
-        if constexpr (TWO) {   // the second set's decay sums (kSep: its own dt and A)
+        if constexpr (TWO && !CV) {   // the second set's decay sums (kSep: its own dt and A)
             const float dtv2 = Act<F32 && !CV>::val(dtraw2);
             const float Ar2 =
                 __int_as_float(__builtin_amdgcn_readlane(__float_as_int(parv), SEP ? 3 : 0)) *
@@ -534,6 +538,14 @@ bdlm_block_kernel(const KArgs args) {
             sCs2[lane] = cs2;
             sEx2[lane] = lane == 0 ? 0.f : up2;
         }
+    }
+    if constexpr (CV && SEP) {
+        __syncthreads();   // the reverse convolution's images and the decay sums
+        for (int tile = wave; tile < MT * MT; tile += NW)
+            sM2[tile * 64 + lane] =
+                gram_tile_f32<QN, kRev>(sBf, sCf, sCs, sEx, sDt, tile / MT, tile % MT, grp, col);
+        __syncthreads();   // its tiles are formed: the images are overwritten next
+        if (tid < CV_TASKS) conv_emit(std::false_type{}, sX, sBf, sCf);
     }
     __syncthreads();
 #pragma unroll
@@ -557,11 +569,9 @@ bdlm_block_kernel(const KArgs args) {
         for (int tile = wave; tile < 2 * MT * MT; tile += NW) {
             const int tt = tile < MT * MT ? tile : tile - MT * MT;
             const int mt = tt / MT, jt = tt % MT;
-            if constexpr (F32) {   // the block's two convolutions, fp32 operands
-                if (tile < MT * MT)
+            if constexpr (F32) {   // the block's two convolutions: the reverse tiles are formed
+                if (tile < MT * MT)  // while staging, only the forward ones here
                     sM[tt * 64 + lane] = gram_tile_f32<QN, kFwd>(sBf, sCf, sCs, sEx, sDt, mt, jt, grp, col);
-                else
-                    sM2[tt * 64 + lane] = gram_tile_f32<QN, kRev>(sBf2, sCf2, sCs2, sEx2, sDt2, mt, jt, grp, col);
             } else {
                 if (tile < MT * MT)
                     sM[tt * 64 + lane] = gram_tile_bf16<QN, kFwd>(sB, sC, sCs, sEx, sDt, mt, jt, grp, col);
