@@ -87,12 +87,21 @@ __device__ __forceinline__ f32x4 mma_k32(s16x4 a0, s16x4 a1, s16x4 b0, s16x4 b1,
 __device__ __forceinline__ f32x4 mma_k16(s16x4 a, s16x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
-// c += sum over Q quads of A_q B_q (16 contraction indices per quad).
+// c += sum over Q quads of A_q B_q (16 contraction indices per quad).  An accumulator is
+// never handed from one MFMA shape to another: a dependent 16-deep MFMA issued right after
+// the 32-deep one that produced its accumulator input has read part of that input before
+// it was written (two of the four rows, measured).  So an odd last quad after pairs runs
+// as a 32-deep MFMA with a zero upper half.
 template <int Q>
 __device__ __forceinline__ f32x4 mma_quads(const s16x4 (&a)[Q], const s16x4 (&b)[Q], f32x4 c) {
 #pragma unroll
     for (int q = 0; q + 1 < Q; q += 2) c = mma_k32(a[q], a[q + 1], b[q], b[q + 1], c);
-    if constexpr (Q & 1) c = mma_k16(a[Q - 1], b[Q - 1], c);
+    if constexpr (Q == 1) {
+        c = mma_k16(a[0], b[0], c);
+    } else if constexpr (Q & 1) {
+        constexpr s16x4 z = {0, 0, 0, 0};
+        c = mma_k32(a[Q - 1], z, b[Q - 1], z, c);
+    }
     return c;
 }
 

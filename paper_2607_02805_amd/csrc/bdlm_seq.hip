@@ -145,13 +145,22 @@ __device__ __forceinline__ Unit decode(const SeqArgs &a) {
 }
 
 // Buffer resources: chunks are addressed from a per-chunk base (uniform, in scalar
-// registers) plus a fixed per-thread byte offset.  Rows outside the segment get an
-// offset past the resource's range: their loads return zeros and their stores are
+// registers) plus a fixed per-thread byte offset.  Rows outside the segment lie past the
+// resource's range (forward: the resource ends after the chunk's valid rows; reverse:
+// they get an out-of-range offset): their loads return zeros and their stores are
 // dropped, with no branch.
 constexpr uint32_t kOOB = 0x80000000u;
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
                                              0x7fffffff, 0x00020000);
+}
+// The same over the first `bytes` bytes only: an access whose per-lane offset lies past
+// them loads zeros and a store there is dropped (the range check of a buffer resource with
+// stride 0 covers the per-lane and immediate offsets, not the scalar offset, so accesses
+// through such a resource pass their whole offset per lane).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_n(const void *base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
+                                             bytes, 0x00020000);
 }
 constexpr int kNT = 2;   // buffer cache policy: nontemporal
 
@@ -235,9 +244,15 @@ struct Stager {
     __device__ __forceinline__ void issue(int c, int tid, int wave, int lane) {
         const int64_t w = window(c);
         const int lim = valid(c);
-        const __amdgpu_buffer_rsrc_t rB = rsrc(Bg + w * bcrow);
-        const __amdgpu_buffer_rsrc_t rC = rsrc(Cg + w * bcrow);
-        const __amdgpu_buffer_rsrc_t rX = rsrc(xg + w * xrow);
+        // Forward, the chunk's rows past the segment are its last ones: the resources end
+        // after the valid rows, so those rows load as zeros with no per-row test.  In
+        // reverse they are the first rows of the window and get an out-of-range offset.
+        const __amdgpu_buffer_rsrc_t rB =
+            REV ? rsrc(Bg + w * bcrow) : rsrc_n(Bg + w * bcrow, static_cast<int>(lim * bcrow));
+        const __amdgpu_buffer_rsrc_t rC =
+            REV ? rsrc(Cg + w * bcrow) : rsrc_n(Cg + w * bcrow, static_cast<int>(lim * bcrow));
+        const __amdgpu_buffer_rsrc_t rX =
+            REV ? rsrc(xg + w * xrow) : rsrc_n(xg + w * xrow, static_cast<int>(lim * xrow));
 #pragma unroll
         for (int k = 0; k < G::BPT; ++k) {
             const int task = tid + kThreads * k;
@@ -245,7 +260,7 @@ struct Stager {
                 const int g = task / G::BCPR;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const uint32_t o = 4 * g + r < lim ? ob[k][r] : kOOB;
+                    const uint32_t o = !REV || 4 * g + r < lim ? ob[k][r] : kOOB;
                     rb[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rB, o, 0, 0);
                     if constexpr (LOADC) rc[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rC, o, 0, 0);
                 }
@@ -258,14 +273,15 @@ struct Stager {
                 const int g = task / G::XCPR;
 #pragma unroll
                 for (int r = 0; r < G::XROWS; ++r) {
-                    const uint32_t o = G::XROWS * g + r < lim ? ox[k][r] : kOOB;
+                    const uint32_t o = !REV || G::XROWS * g + r < lim ? ox[k][r] : kOOB;
                     rx[k][r] = __builtin_amdgcn_raw_buffer_load_b128(rX, o, 0, 0);
                 }
             }
         }
         if (wave == 0) {
-            const __amdgpu_buffer_rsrc_t rD = rsrc(dtg + w * dtrow);
-            const uint32_t o = lane < lim ? odt : kOOB;
+            const __amdgpu_buffer_rsrc_t rD =
+                REV ? rsrc(dtg + w * dtrow) : rsrc_n(dtg + w * dtrow, static_cast<int>(lim * dtrow));
+            const uint32_t o = !REV || lane < lim ? odt : kOOB;
             if constexpr (F32) dtraw = __builtin_amdgcn_raw_buffer_load_b32(rD, o, 0, 0);
             else dtraw = __builtin_amdgcn_raw_buffer_load_b16(rD, o, 0, 0);
         }
@@ -612,6 +628,12 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
     const float *ybase = a.y + (static_cast<int64_t>(un.b) * a.T * a.nheads + un.h) * kP;
     const int64_t ytokB = static_cast<int64_t>(a.nheads) * kP * 4;
     const uint32_t oy = static_cast<uint32_t>(Stager<NS, F32, REV, true>::row(4 * grp) * ytokB + p * 4);
+    // Full chunks (every local token inside the segment) address y as this lane's fixed
+    // offset oyf plus a wave-uniform offset per (mt, r) in a scalar register, with no
+    // per-access range test: local token 4grp + i sits at oyf + ysoff(i).  Partial chunks
+    // keep a tested per-lane offset: the buffer range check does not see scalar offsets.
+    const uint32_t oyf = REV ? oy - static_cast<uint32_t>(51 * ytokB) : oy;
+    auto ysoff = [&](int i) { return static_cast<int>((REV ? 51 - i : i) * ytokB); };
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
@@ -628,15 +650,23 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             if (a.y) {
                 const __amdgpu_buffer_rsrc_t rYl = rsrc(ybase + st.window(c) * (ytokB / 4));
                 const int lim = st.valid(c);
+                if (lim == kC) {
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt)
+                    for (int i = 0; i < 16; ++i)
+                        yv[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                            rYl, oyf, ysoff(16 * (i >> 2) + (i & 3)), 0));
+                } else {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int i = 16 * mt + r;
-                        const uint32_t o = 16 * mt + 4 * grp + r < lim
-                                               ? oy - static_cast<uint32_t>(i * ytokB) : kOOB;
-                        yv[4 * mt + r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rYl, o, 0, 0));
-                    }
+                    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int i = 16 * mt + r;
+                            const uint32_t o = 16 * mt + 4 * grp + r < lim
+                                                   ? oy - static_cast<uint32_t>(i * ytokB) : kOOB;
+                            yv[4 * mt + r] =
+                                __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rYl, o, 0, 0));
+                        }
+                }
             }
         }
 
@@ -775,9 +805,15 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     const s16x4 h1 = as_s16x4(uint2{v1.x, v1.y}), l1 = as_s16x4(uint2{v1.z, v1.w});
                     Y[mt] = mma_k32(h0, h1, xh[jt], xh[jt + 1], Y[mt]);
                     Y[mt] = mma_k32(l0, l1, xh[jt], xh[jt + 1], Y[mt]);
-                } else {
+                } else if (jt == 0) {
                     Y[mt] = mma_k16(h0, xh[jt], Y[mt]);
                     Y[mt] = mma_k16(l0, xh[jt], Y[mt]);
+                } else {
+                    // the accumulator comes from 32-deep MFMAs: stay on that shape (zero
+                    // upper half) rather than hand it to a 16-deep MFMA
+                    constexpr s16x4 z = {0, 0, 0, 0};
+                    Y[mt] = mma_k32(h0, z, xh[jt], z, Y[mt]);
+                    Y[mt] = mma_k32(l0, z, xh[jt], z, Y[mt]);
                 }
             }
             }
@@ -785,21 +821,37 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
 
         // skip term and store (lane (grp, col): token 16mt + 4grp + r, column p)
         {
-            const __amdgpu_buffer_rsrc_t rY = rsrc(ybase + st.window(c) * (ytokB / 4));
             const int lim = st.valid(c);
+            const __amdgpu_buffer_rsrc_t rY = rsrc(ybase + st.window(c) * (ytokB / 4));
+            float v[16];
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
                 const f32x4 out = Y[mt] + skip * xv(mt);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int i = 16 * mt + r;   // + 4grp: this lane's local token
-                    const uint32_t o = 16 * mt + 4 * grp + r < lim
-                                           ? oy + static_cast<uint32_t>((REV ? -i : i) * ytokB)
-                                           : kOOB;
-                    float v = out[r];
-                    if constexpr (REV) v += yv[4 * mt + r];
-                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rY, o, 0, kNT);
+                    v[4 * mt + r] = out[r];
+                    if constexpr (REV) v[4 * mt + r] += yv[4 * mt + r];
                 }
+            }
+            // full chunks store at the lane's fixed offset plus a scalar offset with no per-row
+            // test (the buffer range check does not cover the scalar offset, so a partial
+            // chunk takes the tested path)
+            if (lim == kC) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), rY, oyf,
+                                                          ysoff(16 * (i >> 2) + (i & 3)), kNT);
+            } else {
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = 16 * mt + r;   // + 4grp: this lane's local token
+                        const uint32_t o = 16 * mt + 4 * grp + r < lim
+                                               ? oy + static_cast<uint32_t>((REV ? -i : i) * ytokB)
+                                               : kOOB;
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[4 * mt + r]), rY, o, 0, kNT);
+                    }
             }
         }
         }
