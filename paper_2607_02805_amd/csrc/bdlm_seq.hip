@@ -28,8 +28,9 @@
 // changes nothing.
 //
 // Work split: 4 waves, wave w owns head-dim columns 16w .. 16w+15 of the state and
-// of y.  A chunk is staged once in LDS: B and C as row images (MFMA operands over
-// dstate), B and x transposed (operands over tokens), dt and its decay sums.  The
+// of y.  A chunk is staged once in LDS: B, C and x as row images (MFMA operands over
+// dstate; in bf16 storage B and x are also read transposed, as operands over tokens,
+// with the LDS transpose read), dt and its decay sums.  The
 // decay-weighted Gram tiles C.B^T (10 lower-triangle 16x16 tiles) are shared out
 // over the waves and published in LDS; each wave then forms its columns' y and
 // updates its state rows on MFMA: bf16 storage on bf16 MFMA (fp32 operands such as
@@ -102,17 +103,12 @@ struct Geo {
     static_assert(XT % kThreads == 0 || XT < kThreads, "x tasks");
 };
 
-// x transposed in LDS: per (token quad g, column p) the four tokens' values.
+// x in LDS: a bf16 row image (quads of four columns), or fp32 quads of four tokens'
+// values per (token quad g, column p).
 template <bool F32> struct XQuad;
 template <> struct XQuad<false> { using T = uint2; };
 template <> struct XQuad<true> { using T = f32x4; };
 
-__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) {   // a.lo16, b.lo16
-    return (a & 0xffffu) | (b << 16);
-}
-__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {   // a.hi16, b.hi16
-    return (a >> 16) | (b & 0xffff0000u);
-}
 __device__ __forceinline__ float ex2(float v) { return __builtin_amdgcn_exp2f(v); }
 
 // c += a b over one quad on fp32 MFMA: instruction r contracts lane group g's value
@@ -164,33 +160,46 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_n(const void *base, int b
 }
 constexpr int kNT = 2;   // buffer cache policy: nontemporal
 
+// Row images of B and C in bf16 storage: quad (local token t, dstate quad Q = n / 4) at
+// row_slot<QN>(t, Q).  Blocks of 64 quads per (16-token tile, 16-wide dstate tile); in a
+// block, quad a = Q % 4 of the tile fills a row of 16 slots, the token within the tile
+// XOR-permuted with 4a and the dstate tile.  Three access patterns each touch 16 distinct
+// 8-byte bank pairs per 16 lanes for dstate 64 and 128 (checked on the CPU): the staging
+// writes (one token, 16 consecutive 16-byte pieces of its row), the operand reads over
+// dstate (16 tokens, one quad) and the transposed reads (4 tokens x 4 quads).
+template <int QN>
+__device__ __forceinline__ int row_slot(int t, int Q) {
+    const int q = Q >> 2, a = Q & 3;
+    return ((t >> 4) * QN + q) * 64 + a * 16 + ((t & 15) ^ (4 * a) ^ (q & 7));
+}
+// Row image of x in bf16 storage: quad (local token t, column quad PQ = p / 4) at
+// x_slot(t, PQ), the same scheme over column tiles w = PQ / 4 (16 columns, one wave's).
+__device__ __forceinline__ int x_slot(int t, int PQ) {
+    const int w = PQ >> 2, a = PQ & 3;
+    return ((t >> 4) * 4 + w) * 64 + a * 16 + ((t & 15) ^ (4 * a) ^ ((w & 1) | ((w & 2) << 1)));
+}
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+// LDS transpose read (gfx950): every lane reads four bf16 at its own 8-byte-aligned
+// address, and within each group of 16 lanes, lane 4a + b receives element b of the words
+// read by lanes a, a + 4, a + 8 and a + 12 of its group, in that order.  So when lane s
+// of group kg reads the quad (token 4kg + s / 4, columns c0 + 4 (s % 4) .. +3) of a
+// token-major image, lane (kg, col) receives column c0 + col of tokens 4kg .. 4kg + 3:
+// the operand over tokens of an MFMA that contracts along the chunk.
+__device__ __forceinline__ s16x4 ds_read_tr(const uint2 *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(const_cast<uint2 *>(p)));
+}
+// The quad lane `lane` reads for the transposed operand of 16-token tile jt: token
+// 16jt + tr_tok(lane), column quad 4 c + tr_quad(lane) of column tile c.
+__device__ __forceinline__ int tr_tok(int lane) { return 4 * (lane >> 4) + ((lane & 15) >> 2); }
+__device__ __forceinline__ int tr_quad(int lane) { return lane & 3; }
+
 // One chunk's global loads into registers and their staging into LDS.  Local token
 // i of chunk c is the segment's token 64c + i (reverse: its 64c + i-th token from
-// the end); row(i) is its position in the chunk's memory window.
-// Slots of the bf16 transposed images as seg_state lays them out: element (token
-// quad tq, column n) of the transposed B image at bt_slot<NS>(tq, n), of the
-// transposed x image at xt_slot(tq, p).  The column is XOR-permuted within its row so
-// that the staging writes (a task writes 8 consecutive columns of one token quad,
-// tasks ordered column piece fastest) and the operand reads (16 columns x 2 token
-// quads per half-wave) each touch every LDS bank once (checked on the CPU for every
-// dstate).  seg_out keeps the plain layout (tq * stride + column).
-template <int NS>
-__device__ __forceinline__ int bt_slot(int tq, int n) {
-    int t;
-    if constexpr (NS == 16) t = (tq >> 1) & 7;
-    else if constexpr (NS == 32) t = (tq & 7) | ((tq & 1) << 4);
-    else if constexpr (NS == 64)
-        t = ((tq & 1) << 4) | (((n >> 4) & 1) << 2) | (((tq >> 1) & 1) << 1) | ((n >> 5) & 1);
-    else t = ((tq & 1) << 4) | ((n >> 4) & 1) | (((n >> 5) & 3) << 1);
-    return tq * NS + (n ^ t);
-}
-__device__ __forceinline__ int xt_slot(int tq, int p) {
-    const int t = ((tq & 1) << 4) | ((p >> 4) & 1) | (((tq >> 1) & 1) << 1) | (((p >> 5) & 1) << 2);
-    return tq * kP + (p ^ t);
-}
-
-// SWZ: the permuted transposed layouts above (bf16 storage only).
-template <int NS, bool F32, bool REV, bool LOADC, bool SWZ = false>
+// the end); row(i) is its position in the chunk's memory window.  bf16 storage stages
+// row images only (B, C when loaded, x), read transposed where the contraction runs
+// over tokens; fp32 storage stages row images of B and C and transposed images of B
+// and x (quads of four tokens' fp32 values).
+template <int NS, bool F32, bool REV, bool LOADC>
 struct Stager {
     using G = Geo<NS, F32>;
     static constexpr int ES = F32 ? 4 : 2;
@@ -301,33 +310,15 @@ struct Stager {
                 const int at = img_idx<G::QN, true>(j >> 4, pc >> 2, pc & 3, j & 15);
                 reinterpret_cast<f32x4 *>(hi)[at] = __builtin_bit_cast(f32x4, v[r]);
             } else {
-                const int q0 = 2 * pc, q1 = 2 * pc + 1;
-                hi[img_idx<G::QN, false>(j >> 4, q0 >> 2, q0 & 3, j & 15)] = uint2{v[r].x, v[r].y};
-                hi[img_idx<G::QN, false>(j >> 4, q1 >> 2, q1 & 3, j & 15)] = uint2{v[r].z, v[r].w};
+                hi[row_slot<G::QN>(j, 2 * pc)] = uint2{v[r].x, v[r].y};
+                hi[row_slot<G::QN>(j, 2 * pc + 1)] = uint2{v[r].z, v[r].w};
             }
         }
     }
 
-    // Transposed quads: out[g * stride + col] holds the four tokens 4g .. 4g+3 of
-    // column col = piece * E + e.
-    __device__ __forceinline__ static void transpose_bf16(const u32x4 (&v)[4], int g, int pc,
-                                                          uint2 *out) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-            const uint2 lo = uint2{lo_pair(v[0][d], v[1][d]), lo_pair(v[2][d], v[3][d])};
-            const uint2 hi = uint2{hi_pair(v[0][d], v[1][d]), hi_pair(v[2][d], v[3][d])};
-            if constexpr (SWZ) {
-                out[bt_slot<NS>(g, pc * 8 + 2 * d)] = lo;
-                out[bt_slot<NS>(g, pc * 8 + 2 * d + 1)] = hi;
-            } else {
-                out[g * NS + pc * 8 + 2 * d] = lo;
-                out[g * NS + pc * 8 + 2 * d + 1] = hi;
-            }
-        }
-    }
-
-    // Write the registers of the current chunk into LDS.  bt: transposed B, sb and sc:
-    // row images, xt: transposed x.
+    // Write the registers of the current chunk into LDS.  sb, sc: row images of B and
+    // C (B always for bf16 storage, both only when C is loaded for fp32); bt: the
+    // transposed B image (fp32 only); xt: x, a row image (bf16) or transposed (fp32).
     __device__ __forceinline__ void stage(int tid, uint2 *sb, uint2 *sc, uint2 *bt,
                                           typename XQuad<F32>::T *xt) const {
 #pragma unroll
@@ -335,18 +326,14 @@ struct Stager {
             const int task = tid + kThreads * k;
             if (task < G::BT) {
                 const int g = task / G::BCPR, pc = task % G::BCPR;
-                if constexpr (LOADC) {
-                    row_image(rb[k], g, pc, sb);
-                    row_image(rc[k], g, pc, sc);
-                }
+                if constexpr (LOADC || !F32) row_image(rb[k], g, pc, sb);
+                if constexpr (LOADC) row_image(rc[k], g, pc, sc);
                 if constexpr (F32) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         reinterpret_cast<f32x4 *>(bt)[g * NS + pc * 4 + e] =
                             f32x4{__uint_as_float(rb[k][0][e]), __uint_as_float(rb[k][1][e]),
                                   __uint_as_float(rb[k][2][e]), __uint_as_float(rb[k][3][e])};
-                } else {
-                    transpose_bf16(rb[k], g, pc, bt);
                 }
             }
         }
@@ -362,20 +349,11 @@ struct Stager {
                             f32x4{__uint_as_float(rx[k][0][e]), __uint_as_float(rx[k][1][e]),
                                   __uint_as_float(rx[k][2][e]), __uint_as_float(rx[k][3][e])};
                 } else {
-                    // token pair g: half (g & 1) of the quads of token quad g / 2
-                    uint32_t *x32 = reinterpret_cast<uint32_t *>(xt);
 #pragma unroll
-                    for (int d = 0; d < 4; ++d) {
-                        if constexpr (SWZ) {
-                            x32[xt_slot(g >> 1, pc * 8 + 2 * d) * 2 + (g & 1)] =
-                                lo_pair(rx[k][0][d], rx[k][1][d]);
-                            x32[xt_slot(g >> 1, pc * 8 + 2 * d + 1) * 2 + (g & 1)] =
-                                hi_pair(rx[k][0][d], rx[k][1][d]);
-                        } else {
-                            const int at = ((g >> 1) * kP + pc * 8 + 2 * d) * 2 + (g & 1);
-                            x32[at] = lo_pair(rx[k][0][d], rx[k][1][d]);
-                            x32[at + 2] = hi_pair(rx[k][0][d], rx[k][1][d]);
-                        }
+                    for (int r = 0; r < G::XROWS; ++r) {
+                        const int t = G::XROWS * g + r;
+                        xt[x_slot(t, 2 * pc)] = uint2{rx[k][r].x, rx[k][r].y};
+                        xt[x_slot(t, 2 * pc + 1)] = uint2{rx[k][r].z, rx[k][r].w};
                     }
                 }
             }
@@ -399,17 +377,17 @@ __device__ __forceinline__ void decay_sums(float dtv, float A2, int lane, float 
     if constexpr (WITH_WR) sWr[lane] = ex2(cs - l2) * dtv;
 }
 
-// Operand quad of x for lane (grp, col): tokens 16jt + 4grp .. +3, column p.
+// Operand quad of x for lane (grp, col) of wave w: tokens 16jt + 4grp .. +3 of column
+// p = 16w + col, as bf16 (bf16 storage, read transposed from the row image) and as fp32.
 template <bool F32>
-__device__ __forceinline__ void x_operand(const typename XQuad<F32>::T &v, s16x4 &hi, s16x4 &lo,
-                                          f32x4 &val) {
+__device__ __forceinline__ void x_operand(const typename XQuad<F32>::T *xt, int jt, int wave,
+                                          int lane, s16x4 &hi, f32x4 &val) {
     if constexpr (F32) {
-        val = v;
-        hi = lo = s16x4{0, 0, 0, 0};
+        val = xt[(4 * jt + (lane >> 4)) * kP + 16 * wave + (lane & 15)];
+        hi = s16x4{0, 0, 0, 0};
     } else {
-        hi = as_s16x4(v);
+        hi = ds_read_tr(xt + x_slot(16 * jt + tr_tok(lane), 4 * wave + tr_quad(lane)));
         val = f32x4{bf16_to_f32(hi[0]), bf16_to_f32(hi[1]), bf16_to_f32(hi[2]), bf16_to_f32(hi[3])};
-        lo = s16x4{0, 0, 0, 0};
     }
 }
 
@@ -432,13 +410,13 @@ __device__ __forceinline__ void w_set(WOps<F32, T3> &o, int jt, f32x4 v) {
     else if constexpr (T3) split4x3(v, o.h[jt], o.m[jt], o.l[jt]);
     else split4(v, o.h[jt], o.l[jt]);
 }
-template <int NS, bool F32, bool SWZ = false>
-__device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, int q, int grp, int col) {
+// bt: the B row image (bf16, read transposed) or the transposed fp32 B image.
+template <int NS, bool F32>
+__device__ __forceinline__ void bt_read(BtOps<F32> &o, const uint2 *bt, int q, int lane) {
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
-        if constexpr (F32) o.f[jt] = f32q(bt, (4 * jt + grp) * NS + 16 * q + col);
-        else if constexpr (SWZ) o.h[jt] = as_s16x4(bt[bt_slot<NS>(4 * jt + grp, 16 * q + col)]);
-        else o.h[jt] = as_s16x4(bt[(4 * jt + grp) * NS + 16 * q + col]);
+        if constexpr (F32) o.f[jt] = f32q(bt, (4 * jt + (lane >> 4)) * NS + 16 * q + (lane & 15));
+        else o.h[jt] = ds_read_tr(bt + row_slot<NS / 16>(16 * jt + tr_tok(lane), 4 * q + tr_quad(lane)));
     }
 }
 template <bool F32, bool T3>
@@ -486,7 +464,8 @@ template <int NS, bool F32, bool BOTH>
 __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(const SeqArgs a) {
     using G = Geo<NS, F32>;
     constexpr int QN = G::QN;
-    __shared__ __align__(16) uint2 sBt[(F32 ? 2 : 1) * 16 * NS];
+    // B: bf16 row image (read transposed) or fp32 transposed image; x likewise
+    __shared__ __align__(16) uint2 sBt[F32 ? 2 * 16 * NS : G::IMG];
     __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
     __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC], sWr[kC];
 
@@ -497,7 +476,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
     const Unit un = decode(a);
     const int g = un.h / a.heads_per_group;
 
-    Stager<NS, F32, false, false, !F32> st;   // permuted transposed images (bf16)
+    Stager<NS, F32, false, false> st;
     setup(st, a, un, g, tid, lane);
     const int nch = st.nchunks();
     const float A2 = a.A[un.h] * kLog2e;
@@ -514,7 +493,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
 
     st.issue(0, tid, wave, lane);
     for (int c = 0; c < nch; ++c) {
-        st.stage(tid, nullptr, nullptr, sBt, sXt);
+        st.stage(tid, sBt, nullptr, sBt, sXt);
         if (wave == 0)
             decay_sums<BOTH>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, sWr);
         __syncthreads();
@@ -524,9 +503,9 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         WOps<F32, T3> wf, wr;
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
-            s16x4 xh, xl;
+            s16x4 xh;
             f32x4 xv;
-            x_operand<F32>(sXt[F32 ? (4 * jt + grp) * kP + p : xt_slot(4 * jt + grp, p)], xh, xl, xv);
+            x_operand<F32>(sXt, jt, wave, lane, xh, xv);
             w_set(wf, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv);
             if constexpr (BOTH)
                 w_set(wr, jt,
@@ -534,10 +513,10 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_state_kernel(c
         }
         const float keep = ex2(tot);
         BtOps<F32> cur, nxt;
-        bt_read<NS, F32, !F32>(cur, sBt, 0, grp, col);
+        bt_read<NS, F32>(cur, sBt, 0, lane);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
-            if (q + 1 < QN) bt_read<NS, F32, !F32>(nxt, sBt, q + 1, grp, col);
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, lane);
             F[q] = bt_mma(cur, wf, F[q] * keep);
             if constexpr (BOTH) R[q] = bt_mma(cur, wr, R[q]);
             if (q + 1 < QN) cur = nxt;
@@ -571,7 +550,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
     constexpr int QN = G::QN;
     constexpr int IMG = G::IMG;
     __shared__ __align__(16) uint2 sB[(F32 ? 2 : 1) * IMG], sC[(F32 ? 2 : 1) * IMG];
-    __shared__ __align__(16) uint2 sBt[(F32 ? 2 : 1) * 16 * NS];
+    __shared__ __align__(16) uint2 sBt[F32 ? 2 * 16 * NS : 1];   // fp32: transposed B
     __shared__ __align__(16) typename XQuad<F32>::T sXt[16 * kP];
     __shared__ __align__(16) uint4 sM[kTiles * 64];
     __shared__ __align__(16) float sDt[kC], sCs[kC], sEc[kC], sWs[kC];
@@ -641,7 +620,10 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         if (wave == 0)
             decay_sums<false>(st.dt_value(), A2, lane, sDt, sCs, sEc, sWs, nullptr);
         __syncthreads();
-        if (c + 1 < nch) st.issue(c + 1, tid, wave, lane);
+        // the next chunk's loads (the reverse pass, which also holds the y values it adds
+        // onto, requests them after the Gram tiles instead: fewer registers live across the
+        // Gram and prefix phase)
+        if (!REV && c + 1 < nch) st.issue(c + 1, tid, wave, lane);
         // the reverse pass adds onto the forward pass's outputs: this lane's 16 of them are
         // requested now, before the chunk's products, and stored back with the sums (one
         // reader and writer per element, so the sum is exact fp32 and deterministic)
@@ -656,13 +638,17 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                         yv[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
                             rYl, oyf, ysoff(16 * (i >> 2) + (i & 3)), 0));
                 } else {
+                    // partial chunk (the segment's last): offsets formed here, not held in
+                    // registers across the loop
+                    uint32_t base = oy;
+                    int g4 = 4 * grp;
+                    asm volatile("" : "+v"(base), "+v"(g4));
 #pragma unroll
                     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             const int i = 16 * mt + r;
-                            const uint32_t o = 16 * mt + 4 * grp + r < lim
-                                                   ? oy - static_cast<uint32_t>(i * ytokB) : kOOB;
+                            const uint32_t o = i + g4 < lim ? base - static_cast<uint32_t>(i * ytokB) : kOOB;
                             yv[4 * mt + r] =
                                 __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rYl, o, 0, 0));
                         }
@@ -692,8 +678,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 s16x4 bq[QN], cq[QN];
 #pragma unroll
                 for (int q = 0; q < QN; ++q) {
-                    bq[q] = as_s16x4(sB[img_idx<QN, false>(jt, q, grp, col)]);
-                    cq[q] = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
+                    bq[q] = as_s16x4(sB[row_slot<QN>(16 * jt + col, 4 * q + grp)]);
+                    cq[q] = as_s16x4(sC[row_slot<QN>(16 * mt + col, 4 * q + grp)]);
                 }
                 gacc = mma_quads<QN>(bq, cq, gacc);
             }
@@ -741,8 +727,8 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 s16x4 c0[4], c1[4];
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
-                    c0[mt] = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
-                    c1[mt] = as_s16x4(sC[img_idx<QN, false>(mt, q + 1, grp, col)]);
+                    c0[mt] = as_s16x4(sC[row_slot<QN>(16 * mt + col, 4 * q + grp)]);
+                    c1[mt] = as_s16x4(sC[row_slot<QN>(16 * mt + col, 4 * q + 4 + grp)]);
                 }
                 s16x4 h0, l0, h1, l1;
                 split4(S[q], h0, l0);
@@ -757,7 +743,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                 split4(S[q], h0, l0);
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt) {
-                    const s16x4 c0 = as_s16x4(sC[img_idx<QN, false>(mt, q, grp, col)]);
+                    const s16x4 c0 = as_s16x4(sC[row_slot<QN>(16 * mt + col, 4 * q + grp)]);
                     Y[mt] = mma_k16(c0, h0, Y[mt]);
                     Y[mt] = mma_k16(c0, l0, Y[mt]);
                 }
@@ -770,14 +756,15 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             Y[mt] *= *reinterpret_cast<const f32x4 *>(&sEc[16 * mt + 4 * grp]);
         }
         __syncthreads();   // Gram tiles published
+        if (REV && c + 1 < nch) st.issue(c + 1, tid, wave, lane);
 
         // x operands of this wave's columns (tokens 16jt + 4grp .. +3)
-        s16x4 xh[4], xl[4];
+        s16x4 xh[4];
         f32x4 xvf[F32 ? 4 : 1];   // fp32 storage keeps the values; bf16 re-expands xh
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             f32x4 v;
-            x_operand<F32>(sXt[(4 * jt + grp) * kP + p], xh[jt], xl[jt], v);
+            x_operand<F32>(sXt, jt, wave, lane, xh[jt], v);
             if constexpr (F32) xvf[jt] = v;
         }
         auto xv = [&](int jt) -> f32x4 {
@@ -842,13 +829,17 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), rY, oyf,
                                                           ysoff(16 * (i >> 2) + (i & 3)), kNT);
             } else {
+                // partial chunk: offsets formed here, not held in registers across the loop
+                uint32_t base = oy;
+                int g4 = 4 * grp;
+                asm volatile("" : "+v"(base), "+v"(g4));
 #pragma unroll
                 for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int i = 16 * mt + r;   // + 4grp: this lane's local token
-                        const uint32_t o = 16 * mt + 4 * grp + r < lim
-                                               ? oy + static_cast<uint32_t>((REV ? -i : i) * ytokB)
+                        const uint32_t o = i + g4 < lim
+                                               ? base + static_cast<uint32_t>((REV ? -i : i) * ytokB)
                                                : kOOB;
                         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[4 * mt + r]), rY, o, 0, kNT);
                     }
@@ -884,7 +875,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                     BtOps<F32> cur;
 #pragma unroll
                     for (int q = 0; q < QN; ++q) {
-                        bt_read<NS, F32>(cur, sBt, q, grp, col);
+                        bt_read<NS, F32>(cur, F32 ? sBt : sB, q, lane);
                         f32x4 acc = S[q] * keepb;
                         if constexpr (F32) {
 #pragma unroll
@@ -923,11 +914,11 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
         for (int jt = 0; jt < 4; ++jt)
             w_set(wx, jt, *reinterpret_cast<const f32x4 *>(&sWs[16 * jt + 4 * grp]) * xv(jt));
         BtOps<F32> cur, nxt;
-        bt_read<NS, F32>(cur, sBt, 0, grp, col);
+        bt_read<NS, F32>(cur, F32 ? sBt : sB, 0, lane);
 #pragma unroll
         for (int q = 0; q < QN; ++q) {
             // the next tile's operands are read while this tile's MFMAs run
-            if (q + 1 < QN) bt_read<NS, F32>(nxt, sBt, q + 1, grp, col);
+            if (q + 1 < QN) bt_read<NS, F32>(nxt, F32 ? sBt : sB, q + 1, lane);
             S[q] = bt_mma(cur, wx, S[q] * keep);
             if (q + 1 < QN) cur = nxt;
             __builtin_amdgcn_sched_barrier(0);

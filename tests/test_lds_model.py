@@ -17,13 +17,12 @@ checks, per interval:
 * every byte read was written earlier in the same chunk (LDS is not cleared between
   workgroups: a byte not rewritten would hold whatever the previous workgroup on that
   CU left there);
-* the transposed B and x images of the sequence kernels: each (token, column) element
-  is read from the slot it was written to, under the plain and the permuted layouts.
-
-The permuted layouts are those of seg_state (used by it) and the same layouts applied
-to seg_out (a variant that was measured and not kept: outputs changed in their last
-bits from run to run).  The model finds no LDS hazard in either, so that variability did
-not come from LDS ordering in the source.
+* the sequence kernels' row images of B and x, read back with the LDS transpose read:
+  each (token, column quad) is read from the slot it was written to; separately, each
+  lane's transpose-read address composed with the instruction's lane permutation (as
+  measured on gfx950) gives exactly the MFMA operand element the kernels consume, and
+  the staging writes, operand reads and transpose reads of the row images touch 16
+  distinct 8-byte bank pairs per 16 lanes at dstate 64 and 128.
 """
 import collections
 
@@ -42,23 +41,35 @@ def img_idx(QN, f32, mt, q, grp, col):
     return (mt * QN + q) * 64 + grp * 16 + (col ^ (chunk & 15))
 
 
-def bt_slot(NS, tq, n):
-    """Permuted slot of element (token quad tq, column n) of the transposed B image."""
-    if NS == 16:
-        t = (tq >> 1) & 7
-    elif NS == 32:
-        t = (tq & 7) | ((tq & 1) << 4)
-    elif NS == 64:
-        t = ((tq & 1) << 4) | (((n >> 4) & 1) << 2) | (((tq >> 1) & 1) << 1) | ((n >> 5) & 1)
-    else:
-        t = ((tq & 1) << 4) | ((n >> 4) & 1) | (((n >> 5) & 3) << 1)
-    return tq * NS + (n ^ t)
+def row_slot(QN, t, Q):
+    """Slot of quad (local token t, dstate quad Q) in a bf16 row image of B or C of the
+    sequence kernels (bdlm_seq.hip, row_slot)."""
+    q, a = Q >> 2, Q & 3
+    return ((t >> 4) * QN + q) * 64 + a * 16 + ((t & 15) ^ (4 * a) ^ (q & 7))
 
 
-def xt_slot(tq, p):
-    """Permuted slot of element (token quad tq, column p) of the transposed x image."""
-    t = ((tq & 1) << 4) | ((p >> 4) & 1) | (((tq >> 1) & 1) << 1) | (((p >> 5) & 1) << 2)
-    return tq * P + (p ^ t)
+def x_slot(t, PQ):
+    """Slot of quad (local token t, column quad PQ) in the bf16 row image of x."""
+    w, a = PQ >> 2, PQ & 3
+    return ((t >> 4) * 4 + w) * 64 + a * 16 + ((t & 15) ^ (4 * a) ^ ((w & 1) | ((w & 2) << 1)))
+
+
+def tr_tok(lane):
+    """Token (within a 16-token tile) of the quad a lane reads for a transposed operand."""
+    return 4 * (lane >> 4) + ((lane & 15) >> 2)
+
+
+def tr_quad(lane):
+    """Column quad (within a 16-column tile) of the quad a lane reads."""
+    return lane & 3
+
+
+def tr_source(lane, r):
+    """LDS transpose read (ds_read_b64_tr_b16), as measured on gfx950: slot r of lane
+    16g + 4a + b holds element b of the 8 bytes read by lane 16g + a + 4r.  Returns
+    (source lane, element)."""
+    g, a, b = lane >> 4, (lane & 15) >> 2, lane & 3
+    return 16 * g + a + 4 * r, b
 
 
 # ------------------------------------------------------------------ the recorder
@@ -141,111 +152,94 @@ def new_model(arrays):
 
 
 # ------------------------------------------------------------- sequence kernels
-def stage_chunk(m, NS, swz, with_rows, instr0=0, with_wr=False):
-    """Stager::stage (bf16 storage): row images of B and C (with_rows), the transposed B
-    image and the transposed x image, from the registers of one chunk; plus wave 0's
-    decay sums."""
-    QN = NS // 16
+def stage_chunk(m, NS, with_c, instr0=0, with_wr=False):
+    """Stager::stage (bf16 storage): row images of B (and C when loaded) and of x from
+    the registers of one chunk; plus wave 0's decay sums."""
     BCPR = NS // 8
     BT = 16 * BCPR
     XCPR = P // 8
     XT = (KC // 2) * XCPR
+    QN = NS // 16
     for tid in range(THREADS):
         for k in range(max(1, BT // THREADS)):
             task = tid + THREADS * k
             if task >= BT:
                 continue
             g, pc = task // BCPR, task % BCPR
-            if with_rows:
-                for arr in ("sB", "sC"):
-                    for r in range(4):
-                        j = 4 * g + r
-                        q0, q1 = 2 * pc, 2 * pc + 1
-                        for qq in (q0, q1):
-                            slot = img_idx(QN, False, j >> 4, qq >> 2, qq & 3, j & 15)
-                            m.access(tid, "W", instr0 + 1, arr, slot * 8, 8,
-                                     tag=(arr, j, 4 * qq))
-            for d in range(4):
-                for h in range(2):     # lo / hi halves: columns pc*8 + 2d + h
-                    n = pc * 8 + 2 * d + h
-                    slot = bt_slot(NS, g, n) if swz else g * NS + n
-                    m.access(tid, "W", instr0 + 2, "sBt", slot * 8, 8, tag=("Bt", g, n))
+            for arr in ("sB", "sC") if with_c else ("sB",):
+                for r in range(4):
+                    j = 4 * g + r
+                    for qq in (2 * pc, 2 * pc + 1):
+                        m.access(tid, "W", instr0 + 1, arr, row_slot(QN, j, qq) * 8, 8,
+                                 tag=(arr, j, 4 * qq))
         for k in range(max(1, XT // THREADS)):
             task = tid + THREADS * k
             if task >= XT:
                 continue
             g, pc = task // XCPR, task % XCPR
-            for d in range(4):
-                for h in range(2):
-                    p = pc * 8 + 2 * d + h
-                    if swz:
-                        word = xt_slot(g >> 1, p) * 2 + (g & 1)
-                    else:
-                        word = ((g >> 1) * P + p) * 2 + (g & 1)
-                    m.access(tid, "W", instr0 + 3, "sXt", word * 4, 4, tag=("Xt", g, p))
+            for r in range(2):
+                t = 2 * g + r
+                for pq in (2 * pc, 2 * pc + 1):
+                    m.access(tid, "W", instr0 + 3, "sX", x_slot(t, pq) * 8, 8, tag=("sX", t, 4 * pq))
     for lane in range(64):                    # wave 0: decay sums
         for arr in ("sDt", "sCs", "sEc", "sWs") + (("sWr",) if with_wr else ()):
             if arr in m.arrays:
                 m.access(lane, "W", instr0 + 4, arr, lane * 4, 4, tag=(arr, lane))
 
 
-def read_bt(m, tid, NS, swz, instr):
-    """bt_read over every dstate tile: the transposed-B quads of tokens 16jt + 4grp ..,
-    column 16q + col, and the elements they hold."""
-    lane, grp, col = tid & 63, (tid & 63) >> 4, tid & 15
-    for q in range(NS // 16):
+def read_bt(m, tid, NS, instr):
+    """bt_read over every dstate tile: each lane's transpose-read quad of the B row
+    image (token 16jt + tr_tok, dstate quad 4q + tr_quad)."""
+    lane = tid & 63
+    QN = NS // 16
+    for q in range(QN):
         for jt in range(4):
-            tq, n = 4 * jt + grp, 16 * q + col
-            slot = bt_slot(NS, tq, n) if swz else tq * NS + n
-            # the quad holds tokens 4tq .. 4tq+3 of column n: written as element (tq, n)
-            m.access(tid, "R", instr, "sBt", slot * 8, 8, tag=("Bt", tq, n))
+            t, Q = 16 * jt + tr_tok(lane), 4 * q + tr_quad(lane)
+            m.access(tid, "R", instr, "sB", row_slot(QN, t, Q) * 8, 8, tag=("sB", t, 4 * Q))
 
 
-def read_xt(m, tid, swz, instr):
-    """x operands: tokens 16jt + 4grp .. +3 of column p = 16 wave + col."""
-    grp, col, wave = (tid & 63) >> 4, tid & 15, tid >> 6
-    p = 16 * wave + col
+def read_xt(m, tid, instr):
+    """x operands of wave w's columns: each lane's transpose-read quad of the x row
+    image (token 16jt + tr_tok, column quad 4w + tr_quad)."""
+    lane, wave = tid & 63, tid >> 6
     for jt in range(4):
-        tq = 4 * jt + grp
-        slot = xt_slot(tq, p) if swz else tq * P + p
-        # two words: token pair 2tq (word 0) and 2tq + 1 (word 1)
-        m.access(tid, "R", instr, "sXt", slot * 8, 4, tag=("Xt", 2 * tq, p))
-        m.access(tid, "R", instr, "sXt", slot * 8 + 4, 4, tag=("Xt", 2 * tq + 1, p))
+        t, pq = 16 * jt + tr_tok(lane), 4 * wave + tr_quad(lane)
+        m.access(tid, "R", instr, "sX", x_slot(t, pq) * 8, 8, tag=("sX", t, 4 * pq))
 
 
-def seg_state_model(NS, both, swz=True):
-    arrays = {"sBt": 16 * NS * 8, "sXt": 16 * P * 8}
+def seg_state_model(NS, both):
+    QN = NS // 16
+    arrays = {"sB": 4 * QN * 64 * 8, "sX": 16 * P * 8}
     for a in ("sDt", "sCs", "sEc", "sWs", "sWr"):
         arrays[a] = KC * 4
     m = new_model(arrays)
     m.barrier()                                # kernel start / previous chunk's last barrier
-    stage_chunk(m, NS, swz, with_rows=False, with_wr=both)
+    stage_chunk(m, NS, with_c=False, with_wr=both)
     m.barrier()
     for tid in range(THREADS):
         grp = (tid & 63) >> 4
         m.access(tid, "R", 10, "sCs", (KC - 1) * 4, 4, tag=("sCs", KC - 1))
-        read_xt(m, tid, swz, 11)
+        read_xt(m, tid, 11)
         for jt in range(4):
             for r in range(4):
                 t = 16 * jt + 4 * grp + r
                 m.access(tid, "R", 12, "sWs", t * 4, 4, tag=("sWs", t))
                 if both:
                     m.access(tid, "R", 12, "sWr", t * 4, 4, tag=("sWr", t))
-        read_bt(m, tid, NS, swz, 13)
+        read_bt(m, tid, NS, 13)
     m.barrier()                                # end of chunk
     return m
 
 
-def seg_out_model(NS, sub, swz, want_y=True, carry=True):
+def seg_out_model(NS, sub, want_y=True, carry=True):
     QN = NS // 16
     IMG = 4 * QN * 64
-    arrays = {"sB": IMG * 8, "sC": IMG * 8, "sBt": 16 * NS * 8, "sXt": 16 * P * 8,
-              "sM": 10 * 64 * 16}
+    arrays = {"sB": IMG * 8, "sC": IMG * 8, "sX": 16 * P * 8, "sM": 10 * 64 * 16}
     for a in ("sDt", "sCs", "sEc", "sWs"):
         arrays[a] = KC * 4
     m = new_model(arrays)
     m.barrier()
-    stage_chunk(m, NS, swz, with_rows=True)
+    stage_chunk(m, NS, with_c=True)
     m.barrier()
     # Gram tiles (wave w: tiles w, w + 4, w + 8) and the prefix term
     for tid in range(THREADS):
@@ -256,11 +250,10 @@ def seg_out_model(NS, sub, swz, want_y=True, carry=True):
                 mt = 0 if k < 1 else (1 if k < 3 else (2 if k < 6 else 3))
                 jt = k - mt * (mt + 1) // 2
                 for q in range(QN):
-                    sb = img_idx(QN, False, jt, q, grp, col)
-                    sc = img_idx(QN, False, mt, q, grp, col)
-                    # quad (tile, q, grp, col) holds rows 16 tile + col, columns 16q + 4grp ..
-                    m.access(tid, "R", 20, "sB", sb * 8, 8, tag=("sB", 16 * jt + col, 16 * q + 4 * grp))
-                    m.access(tid, "R", 20, "sC", sc * 8, 8, tag=("sC", 16 * mt + col, 16 * q + 4 * grp))
+                    # lane (grp, col) reads quad 4q + grp of rows 16 tile + col
+                    tb, tc, Q = 16 * jt + col, 16 * mt + col, 4 * q + grp
+                    m.access(tid, "R", 20, "sB", row_slot(QN, tb, Q) * 8, 8, tag=("sB", tb, 4 * Q))
+                    m.access(tid, "R", 20, "sC", row_slot(QN, tc, Q) * 8, 8, tag=("sC", tc, 4 * Q))
                 t = 16 * mt + col
                 m.access(tid, "R", 21, "sCs", t * 4, 4, tag=("sCs", t))
                 for r in range(4):
@@ -270,8 +263,8 @@ def seg_out_model(NS, sub, swz, want_y=True, carry=True):
                 m.access(tid, "W", 22, "sM", (k * 64 + lane) * 16, 16, tag=("sM", k, lane))
             for q in range(QN):
                 for mt in range(4):
-                    sc = img_idx(QN, False, mt, q, grp, col)
-                    m.access(tid, "R", 23, "sC", sc * 8, 8, tag=("sC", 16 * mt + col, 16 * q + 4 * grp))
+                    tc, Q = 16 * mt + col, 4 * q + grp
+                    m.access(tid, "R", 23, "sC", row_slot(QN, tc, Q) * 8, 8, tag=("sC", tc, 4 * Q))
             for mt in range(4):
                 for r in range(4):
                     t = 16 * mt + 4 * grp + r
@@ -280,7 +273,7 @@ def seg_out_model(NS, sub, swz, want_y=True, carry=True):
     for tid in range(THREADS):
         lane = tid & 63
         grp = lane >> 4
-        read_xt(m, tid, swz, 30)
+        read_xt(m, tid, 30)
         if want_y:
             for mt in range(4):
                 for jt in range(mt + 1):
@@ -294,14 +287,14 @@ def seg_out_model(NS, sub, swz, want_y=True, carry=True):
                         t = 16 * jt + 4 * grp + r
                         m.access(tid, "R", 32, "sCs", t * 4, 4, tag=("sCs", t))
                         m.access(tid, "R", 32, "sDt", t * 4, 4, tag=("sDt", t))
-                read_bt(m, tid, NS, swz, 33)
+                read_bt(m, tid, NS, 33)
         elif carry:
             m.access(tid, "R", 34, "sCs", (KC - 1) * 4, 4, tag=("sCs", KC - 1))
             for jt in range(4):
                 for r in range(4):
                     t = 16 * jt + 4 * grp + r
                     m.access(tid, "R", 34, "sWs", t * 4, 4, tag=("sWs", t))
-            read_bt(m, tid, NS, swz, 35)
+            read_bt(m, tid, NS, 35)
     m.barrier()                                # LDS is rewritten by the next chunk
     return m
 
@@ -613,21 +606,77 @@ def mask_model(NS, MT, commit, want_y=True):
 
 @pytest.mark.parametrize("NS", [16, 32, 64, 128])
 @pytest.mark.parametrize("both", [False, True])
-@pytest.mark.parametrize("swz", [False, True])
-def test_seg_state_lds(NS, both, swz):
-    assert seg_state_model(NS, both, swz).check() == []
+def test_seg_state_lds(NS, both):
+    assert seg_state_model(NS, both).check() == []
 
 
 @pytest.mark.parametrize("NS", [16, 32, 64, 128])
 @pytest.mark.parametrize("sub", [0, 16, 32])
-@pytest.mark.parametrize("swz", [False, True])
-def test_seg_out_lds(NS, sub, swz):
-    assert seg_out_model(NS, sub, swz).check() == []
+def test_seg_out_lds(NS, sub):
+    assert seg_out_model(NS, sub).check() == []
 
 
 @pytest.mark.parametrize("NS", [16, 128])
 def test_seg_out_lds_without_outputs(NS):
-    assert seg_out_model(NS, 0, False, want_y=False).check() == []
+    assert seg_out_model(NS, 0, want_y=False).check() == []
+
+
+@pytest.mark.parametrize("NS", [16, 32, 64, 128])
+def test_transpose_read_operands(NS):
+    """Each lane's transpose-read address, composed with the instruction's lane
+    permutation, yields the operands the MFMAs contract over tokens: lane (grp, col)
+    slot r holds B[16jt + 4grp + r][16q + col] (state update) and x[16jt + 4grp + r]
+    [16w + col] (intra term, skip term and state update of wave w)."""
+    QN = NS // 16
+    # what each row-image slot holds: (token, first column of its quad)
+    b_at = {row_slot(QN, t, Q): (t, 4 * Q) for t in range(KC) for Q in range(NS // 4)}
+    x_at = {x_slot(t, PQ): (t, 4 * PQ) for t in range(KC) for PQ in range(P // 4)}
+    assert len(b_at) == KC * NS // 4 and len(x_at) == KC * P // 4
+    for jt in range(4):
+        for lane in range(64):
+            grp, col = lane >> 4, lane & 15
+            for r in range(4):
+                src, e = tr_source(lane, r)
+                for q in range(QN):
+                    t, n0 = b_at[row_slot(QN, 16 * jt + tr_tok(src), 4 * q + tr_quad(src))]
+                    assert (t, n0 + e) == (16 * jt + 4 * grp + r, 16 * q + col)
+                for w in range(4):
+                    t, p0 = x_at[x_slot(16 * jt + tr_tok(src), 4 * w + tr_quad(src))]
+                    assert (t, p0 + e) == (16 * jt + 4 * grp + r, 16 * w + col)
+
+
+def _bank_pairs_distinct(slots16):
+    """8-byte accesses are served 16 lanes at a time over 32 four-byte banks: conflict
+    free when the 16 slots fall on 16 distinct bank pairs."""
+    return len({s % 16 for s in slots16}) == len(slots16)
+
+
+@pytest.mark.parametrize("NS", [64, 128])
+def test_row_images_are_bank_conflict_free(NS):
+    QN, BCPR = NS // 16, NS // 8
+    for r in range(4):                        # staging writes: one row r, one quad half
+        for h in range(2):
+            for base in range(0, THREADS, 16):
+                sl = [row_slot(QN, 4 * (tid // BCPR) + r, 2 * (tid % BCPR) + h)
+                      for tid in range(base, base + 16)]
+                assert _bank_pairs_distinct(sl)
+    for t0 in range(0, KC, 16):
+        for q in range(QN):
+            for grp in range(4):              # operand reads over dstate
+                assert _bank_pairs_distinct([row_slot(QN, t0 + col, 4 * q + grp) for col in range(16)])
+                # transpose reads: lanes 16grp .. 16grp + 15
+                assert _bank_pairs_distinct([row_slot(QN, t0 + tr_tok(16 * grp + s), 4 * q + tr_quad(s))
+                                             for s in range(16)])
+    for r in range(2):                        # x staging writes and transpose reads
+        for h in range(2):
+            for base in range(0, THREADS, 16):
+                assert _bank_pairs_distinct([x_slot(2 * (tid // 8) + r, 2 * (tid % 8) + h)
+                                             for tid in range(base, base + 16)])
+    for t0 in range(0, KC, 16):
+        for w in range(4):
+            for grp in range(4):
+                assert _bank_pairs_distinct([x_slot(t0 + tr_tok(16 * grp + s), 4 * w + tr_quad(s))
+                                             for s in range(16)])
 
 
 @pytest.mark.parametrize("LT,NS", [(16, 16), (16, 128), (32, 64), (32, 128), (64, 32), (64, 128)])
@@ -674,7 +723,7 @@ def test_the_model_catches_cross_wave_rewrites():
 def test_the_model_catches_planted_hazards():
     """The checks are live: a model with a missing barrier, a colliding write, an index
     past the end, a stale read or a mismatched slot is flagged."""
-    m = seg_out_model(32, 0, False)
+    m = seg_out_model(32, 0)
     assert m.check() == []
     # no barrier between the Gram tiles and their use: merge intervals 2 and 3
     merged = new_model(m.arrays)
