@@ -1074,14 +1074,19 @@ def span_per_node(disp, run_len: int) -> float | None:
     import statistics as st
     runs, cur = [], [disp[0]] if disp else []
     for d in disp[1:]:
-        if d[0] - cur[-1][1] < 20_000:      # within 20 us of the previous dispatch's end
+        if d[0] - cur[-1][1] < 100_000:     # within 100 us of the previous dispatch's end
             cur.append(d)
         else:
             runs.append(cur)
             cur = [d]
     if cur:
         runs.append(cur)
-    spans = [(r[-1][1] - r[0][0]) / 1e3 / len(r) for r in runs if len(r) == run_len]
+    runs = [r for r in runs if len(r) == run_len]
+    if not runs and disp and len(disp) % run_len == 0:
+        # replays closer together than the gap test separates: consecutive groups of
+        # run_len dispatches (every step dispatch of the run belongs to a replay)
+        runs = [disp[i:i + run_len] for i in range(0, len(disp), run_len)]
+    spans = [(r[-1][1] - r[0][0]) / 1e3 / len(r) for r in runs]
     return st.median(spans) if spans else None
 
 
