@@ -1,9 +1,11 @@
 """Bitwise run-to-run repeatability of every shipped kernel family on grids larger than
 the chip (so CUs run several workgroups in turn, in an order that varies between calls):
 ten calls each, outputs pre-filled differently before every call.  The kernels are
-deterministic by construction (no atomics except the reverse pass's single addend per
-element; LDS traffic modelled race-free in tests/test_lds_model.py); these repeats are
-the measurement that backs it."""
+deterministic by construction (no atomics: the reverse sequence pass reads and rewrites
+each output it adds onto, one reader and writer per element; LDS traffic modelled
+race-free in tests/test_lds_model.py; no MFMA accumulator handed between MFMA shapes,
+checked on the generated code by tests/test_mfma_chains.py); these repeats are the
+measurement that backs it."""
 import sys
 
 import numpy as np
@@ -87,6 +89,31 @@ def test_sequence_kernels_repeat():
                                          y_fwd=filled((4, 2048, 64, 64), r))
         return (s, yf)
     repeats(states)
+
+
+@pytest.mark.parametrize("N", [16, 64, 128])
+def test_single_chunk_windows_repeat(N):
+    """2,048 workgroups of one 64-token chunk each (batch 8, 256 heads): the shape on which
+    an MFMA accumulator handed from a 32-deep to a 16-deep MFMA showed up (outputs at
+    tokens 32 + {0, 1, 4, 5, 8, 9, 12, 13} of a chunk changed from call to call).  The full
+    window and the forward outputs of a prefill, ten calls each."""
+    import paper_2607_02805_amd as bd
+    w = bi.Workload("t", 8, 256, 64, N, 1, 64, 0, True, 1, 17500 + N)
+    v = to_dev(bi.block_inputs(w, 0))
+    say("single-chunk windows", dict(N=N))
+
+    def full(r):
+        y = filled((8, 64, 256, 64), r)
+        bd.scan_full_window(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], v["D_rev"], y=y)
+        return (y,)
+    repeats(full)
+
+    def pre(r):
+        c = bd.Cache(8, 256, N)
+        yf = filled((8, 64, 256, 64), r)
+        c.prefill(v["x"], v["dt"], v["A"], v["B"], v["C"], v["D"], y_fwd=yf)
+        return (c.h, yf)
+    repeats(pre)
 
 
 def test_long_block_and_variants_repeat():
