@@ -73,15 +73,6 @@ __device__ __forceinline__ f32x4 bf16x4_val(uint2 v) {
     return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
                  __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u)};
 }
-// c += A B over Q operand quads held as uint2 (16 contraction indices each)
-template <int Q>
-__device__ __forceinline__ f32x4 mma_u2(const uint2 (&a)[Q], const uint2 (&b)[Q], f32x4 c) {
-#pragma unroll
-    for (int q = 0; q + 1 < Q; q += 2)
-        c = mma_k32(as_s16x4(a[q]), as_s16x4(a[q + 1]), as_s16x4(b[q]), as_s16x4(b[q + 1]), c);
-    if constexpr (Q & 1) c = mma_k16(as_s16x4(a[Q - 1]), as_s16x4(b[Q - 1]), c);
-    return c;
-}
 // State quad (q, grp) of column p in the pool layout: s[p][16q + 4grp .. +3].
 __device__ __forceinline__ int quad_off(int q, int grp, int p) { return ((4 * q + grp) * kP + p) * 4; }
 // LDS image of B or C as 16-byte pairs of operand quads: entry (token tile mt, quad pair
@@ -458,8 +449,10 @@ bdlm_mask_block_kernel(const MaskArgs a) {
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
                     const s16x4 xq = as_s16x4(sXt[(4 * mt + grp) * kP + 16 * pt + col]);
-                    Y[m][pt] = mma_k16(th, xq, Y[m][pt]);
-                    Y[m][pt] = mma_k16(tl, xq, Y[m][pt]);
+                    // Y comes from 32-deep MFMAs: stay on that shape (zero upper half)
+                    constexpr s16x4 z = {0, 0, 0, 0};
+                    Y[m][pt] = mma_k32(th, z, xq, z, Y[m][pt]);
+                    Y[m][pt] = mma_k32(tl, z, xq, z, Y[m][pt]);
                 }
             }
 
