@@ -85,6 +85,13 @@ template <int QP>
 __device__ __forceinline__ int pair_idx(int mt, int qp, int grp, int col) {
     return (mt * QP + qp) * 64 + grp * 16 + (col ^ ((2 * qp + (grp >> 1)) & 15));
 }
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+// LDS transpose read (gfx950): every lane reads four bf16 at its own 8-byte-aligned
+// address, and within each group of 16 lanes, lane 4a + b receives element b of the words
+// read by lanes a, a + 4, a + 8 and a + 12 of its group, in that order.
+__device__ __forceinline__ s16x4 ds_read_tr(const uint2 *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(const_cast<uint2 *>(p)));
+}
 __device__ __forceinline__ f32x4 mma_pair(uint4 a, uint4 b, f32x4 c) {
     return mma_k32(as_s16x4(uint2{a.x, a.y}), as_s16x4(uint2{a.z, a.w}), as_s16x4(uint2{b.x, b.y}),
                    as_s16x4(uint2{b.z, b.w}), c);
@@ -503,8 +510,8 @@ bdlm_mask_block_kernel(const MaskArgs a) {
         if constexpr (COMMIT) {
             // ---- s_new[p, n] = 2^{cs_last} s[p, n] + sum_j B[j, n] wc_j x[j, p] on this
             // wave's tiles (columns 16 pt + col, pt = wave & 3 for every tile of the wave).
-            // A operand: lane (col, grp) holds B[16 jt + 4 grp + r][16 q + col], gathered from
-            // the B image.
+            // A operand: lane (col, grp) holds B[16 jt + 4 grp + r][16 q + col], read
+            // transposed from the B image.
             const float keep = ex2(sE[MT - 1]);
             const int pt = wave & 3;
             uint2 wh[MT], wm[MT], wl[MT];
@@ -518,28 +525,22 @@ bdlm_mask_block_kernel(const MaskArgs a) {
                 wm[jt] = as_u2(tm);
                 wl[jt] = as_u2(tl);
             }
-            const uint16_t *sBh = reinterpret_cast<const uint16_t *>(sB);
+            const uint2 *sB2 = reinterpret_cast<const uint2 *>(sB);
+            // the quad this lane reads for the transposed operand: token 16 jt + tt, dstate
+            // 16 q + 4 (lane % 4) .. +3 (lane group lane % 4 of the B image)
+            const int tt = 4 * (lane >> 4) + ((lane & 15) >> 2), ta = lane & 3;
 #pragma unroll
             for (int i = 0; i < NCT; ++i) {
                 const int k = wave + kMW * i;
                 if (k >= 4 * QN) break;
                 const int q = k >> 2;
-                // element (j, n) of the B image: entry (j / 16, q / 2, n % 16 / 4, j % 16), half
-                // q % 2, slot n % 4
-                const int nb = (q & 1) * 4 + (col & 3);
                 f32x4 acc = so[i] * keep;
 #pragma unroll
                 for (int jt = 0; jt < MT; jt += 2) {
-                    uint2 bt[2];
-#pragma unroll
-                    for (int d = 0; d < 2; ++d) {
-                        uint32_t e[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            e[r] = sBh[pair_idx<QP>(jt + d, q >> 1, col >> 2, 4 * grp + r) * 8 + nb];
-                        bt[d] = uint2{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
-                    }
-                    const s16x4 b0 = as_s16x4(bt[0]), b1 = as_s16x4(bt[1]);
+                    // B[16 (jt + d) + 4 grp + r][16 q + col], r = 0 .. 3, through the LDS
+                    // transpose read (one 8-byte read per lane)
+                    const s16x4 b0 = ds_read_tr(sB2 + 2 * pair_idx<QP>(jt, q >> 1, ta, tt) + (q & 1));
+                    const s16x4 b1 = ds_read_tr(sB2 + 2 * pair_idx<QP>(jt + 1, q >> 1, ta, tt) + (q & 1));
                     acc = mma_k32(b0, b1, as_s16x4(wh[jt]), as_s16x4(wh[jt + 1]), acc);
                     acc = mma_k32(b0, b1, as_s16x4(wm[jt]), as_s16x4(wm[jt + 1]), acc);
                     acc = mma_k32(b0, b1, as_s16x4(wl[jt]), as_s16x4(wl[jt + 1]), acc);

@@ -596,11 +596,11 @@ def mask_model(NS, MT, commit, want_y=True):
                 if kk >= 4 * QN:
                     break
                 q = kk >> 2
-                nb = (q & 1) * 4 + (col & 3)
+                tt, ta = tr_tok(lane), tr_quad(lane)
                 for jt in range(MT):
-                    for r in range(4):
-                        e = pair_idx(QP, jt, q >> 1, col >> 2, 4 * grp + r) * 8 + nb
-                        rd(63, "sB", e * 2, 2, tag=("sB", 16 * jt + 4 * grp + r, 16 * q + 4 * (col >> 2)))
+                    # one transpose read: the quad (token 16 jt + tt, dstate 16 q + 4 ta ..)
+                    e = 2 * pair_idx(QP, jt, q >> 1, ta, tt) + (q & 1)
+                    rd(63, "sB", e * 8, 8, tag=("sB", 16 * jt + tt, 16 * q + 4 * ta))
     m.barrier()
     return m
 
@@ -695,6 +695,23 @@ def test_mask_block_kernel_lds(NS, MT, commit):
     assert mask_model(NS, MT, commit).check() == []
     if commit:
         assert mask_model(NS, MT, True, want_y=False).check() == []
+
+
+@pytest.mark.parametrize("NS", [16, 32, 64, 128])
+def test_mask_commit_transpose_read_operand(NS):
+    """The masked long-block kernel's commit reads B transposed from its pair image: lane
+    (grp, col) must receive B[16jt + 4grp + r][16q + col] in slot r.  Each lane's read
+    (token 16jt + tr_tok, dstate quad piece tr_quad of quad q), composed with the
+    instruction's lane permutation, gives exactly that element."""
+    QN = NS // 16
+    for q in range(QN):
+        for jt in range(2):
+            for lane in range(64):
+                grp, col = lane >> 4, lane & 15
+                for r in range(4):
+                    src, e = tr_source(lane, r)
+                    token, n = 16 * jt + tr_tok(src), 16 * q + 4 * tr_quad(src) + e
+                    assert (token, n) == (16 * jt + 4 * grp + r, 16 * q + col)
 
 
 def test_the_model_catches_cross_wave_rewrites():
