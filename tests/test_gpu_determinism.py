@@ -128,3 +128,15 @@ def test_long_block_and_variants_repeat():
         bd.scan_block_step(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"], pool, y=y)
         return (y,)
     repeats(step)
+    say("256-token block commit, with and without its outputs")
+
+    def commit(r):
+        h, h2 = pool.clone(), pool.clone()
+        yc = filled((16, 256, 26, 64), r)
+        bd.commit_boundary(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"], h,
+                           np.zeros(16, np.int64), np.zeros(16, np.int64), y_clean=yc)
+        bd.commit_boundary(d["x"], d["dt"], d["A"], d["B"], d["C"], d["D"], d["D_rev"], h2,
+                           np.zeros(16, np.int64), np.zeros(16, np.int64))
+        assert torch.equal(h, h2)   # the outputs do not change the committed state
+        return (h, yc, h2)
+    repeats(commit)
