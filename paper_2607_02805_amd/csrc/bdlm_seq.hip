@@ -822,12 +822,16 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
             }
             // full chunks store at the lane's fixed offset plus a scalar offset with no per-row
             // test (the buffer range check does not cover the scalar offset, so a partial
-            // chunk takes the tested path)
+            // chunk takes the tested path).  The four waves write a token row's 256 bytes in
+            // 64-byte pieces at different times: the forward pass stores through the cache so
+            // the pieces meet in L2 before the line is written back (the reverse pass read the
+            // line first, so its nontemporal stores find it there)
+            constexpr int ypol = REV ? kNT : 0;
             if (lim == kC) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[i]), rY, oyf,
-                                                          ysoff(16 * (i >> 2) + (i & 3)), kNT);
+                                                          ysoff(16 * (i >> 2) + (i & 3)), ypol);
             } else {
                 // partial chunk: offsets formed here, not held in registers across the loop
                 uint32_t base = oy;
@@ -841,7 +845,7 @@ __global__ void __launch_bounds__(kThreads, F32 ? 1 : 2) bdlm_seg_out_kernel(con
                         const uint32_t o = i + g4 < lim
                                                ? base + static_cast<uint32_t>((REV ? -i : i) * ytokB)
                                                : kOOB;
-                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[4 * mt + r]), rY, o, 0, kNT);
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v[4 * mt + r]), rY, o, 0, ypol);
                     }
             }
         }
