@@ -501,7 +501,8 @@ bdlm_mask_block_kernel(const MaskArgs a) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const float out = ec[m][r] * Z[m][r] + Y[m][pt][r] + skip * xv[r];
-                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(out), rY, yo[m][r], 64 * pt, kNT);
+                        // through the cache: a row's four 64-byte pieces (pt) meet in L2
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(out), rY, yo[m][r], 64 * pt, 0);
                     }
                 }
             }
